@@ -1,0 +1,97 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case copies the oracle's C source, plants one mistake by a text
+substitution, builds the altered copy into a temporary library and runs the
+pins of test_oracle_pins.py against it: at least one pin must fail.  Only the
+CPU is involved; the real oracle library is untouched.
+"""
+import os
+import shutil
+import tempfile
+
+import pytest
+
+import test_oracle_pins as pins
+from oracle import build as obuild
+from oracle import oracle as O
+
+MUTANTS = [
+    ("scale divisor Q+1",
+     "absmax / (double)Q", "absmax / (double)(Q + 1)"),
+    ("code ties away from zero",
+     "rint((double)w[j] / s)", "round((double)w[j] / s)"),
+    ("no clamp of codes",
+     "if (r > Q)\n                r = Q;", ""),
+    ("max instead of absmax",
+     "if (fabs(v) > absmax)", "if (v > absmax)"),
+    ("NaN/Inf not rejected",
+     "if (!isfinite(v))\n            return ORC_ERR_RANGE;", ""),
+    ("fp16 encode rounds half up",
+     "rint(ldexp(a, 10 - E))", "floor(ldexp(a, 10 - E) + 0.5)"),
+    ("fp16 encode subnormal threshold",
+     "if (a < 0x1p-14) {", "if (a < 0x1p-15) {"),
+    ("fp16 decode exponent bias",
+     "ldexp((double)(man + 1024), ex - 25)", "ldexp((double)(man + 1024), ex - 24)"),
+    ("q4 nibbles stored swapped",
+     "    if (k & 1)\n        *p", "    if (!(k & 1))\n        *p"),
+    ("q4 code read unsigned",
+     "return nib >= 8 ? nib - 16 : nib;", "return nib;"),
+    ("forward drops the block scale",
+     "y += oracle_f16_to_f64(scales[n * nb + b]) * partial;", "y += partial;"),
+    ("forward uses the first block's scale for all",
+     "y += oracle_f16_to_f64(scales[n * nb + b]) * partial;",
+     "y += oracle_f16_to_f64(scales[n * nb]) * partial;"),
+    ("forward shifted activation index",
+     "partial += x_at(X, xdt, K, m, k)", "partial += x_at(X, xdt, K, m, (k + 1) % K)"),
+    ("forward reads the next block's codes",
+     "code_at(fmt, codes, K, n, k);\n        }", "code_at(fmt, codes, K, n, (k + ORC_BLOCK) % K);\n        }"),
+    ("bf16 decode shift",
+     "(uint32_t)b << 16", "(uint32_t)b << 15"),
+]
+
+
+def pin_cases():
+    F = [O.FMT_INT8, O.FMT_Q4]
+    cases = []
+    cases += [(pins.test_range_errors, (f,)) for f in F]
+    cases += [(pins.test_shape_errors, ())]
+    cases += [(pins.test_q4_packing_layout, ())]
+    cases += [(pins.test_half_integer_ties_go_to_even, ())]
+    cases += [(pins.test_power_of_two_weights_exact, (f,)) for f in F]
+    cases += [(pins.test_unit_scale_integer_matmul, (f,)) for f in F]
+    cases += [(pins.test_invariants_roundtrip_maxcode_idempotent, (f,)) for f in F]
+    cases += [(pins.test_forward_matches_dequantized_matmul, (f, x)) for f in F for x in (0, 1)]
+    cases += [(pins.test_forward_bruteforce_tiny, (f, 32)) for f in F]
+    cases += [(pins.test_bf16_decode, ())]
+    cases += [(pins.test_scales_and_codes_bruteforce, (f,)) for f in F]
+    cases += [(pins.test_f16_encode_special_values, ())]
+    cases += [(pins.test_f16_decode_all_patterns, ())]
+    cases += [(pins.test_f16_encode_exact_values_roundtrip, ())]
+    cases += [(pins.test_f16_encode_midpoints_and_neighbours, ())]
+    return cases
+
+
+@pytest.fixture(scope="module")
+def tmpdir_mut():
+    d = tempfile.mkdtemp(prefix="oracle_mut_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmpdir_mut, name, old, new):
+    src = open(obuild.SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/found: {old!r}"
+    tag = "".join(ch if ch.isalnum() else "_" for ch in name)
+    csrc = os.path.join(tmpdir_mut, f"{tag}.c")
+    lib = os.path.join(tmpdir_mut, f"lib{tag}.so")
+    with open(csrc, "w") as f:
+        f.write(src.replace(old, new))
+    obuild.build(src=csrc, out=lib, extra_flags=("-w",))
+    mut = O.Oracle(lib)
+    for fn, args in pin_cases():
+        try:
+            fn(mut, *args)
+        except (AssertionError, O.OracleError, ValueError, IndexError, OverflowError):
+            return  # caught
+    pytest.fail(f"no pin caught the planted mistake: {name}")
