@@ -1,0 +1,133 @@
+/*
+ * qlinear.h — block-quantized linear layers (int8 / 4-bit weights with
+ * per-block fp16 scales) for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper: Methodology, "The aria runtime" and "Quantization
+ * and its evaluation"): the diffusion transformer's weights are stored as
+ * 8-bit or 4-bit integers (q8 / q4) instead of half precision; the
+ * compressed copy owns its own memory so that the full-precision source can
+ * be released once packed, and the linear layers are evaluated from it.  The
+ * paper does not fix the encoding; this library uses symmetric absmax
+ * quantization over blocks of 32 consecutive weights along the reduction
+ * dimension K with one fp16 scale per block:
+ *
+ *     s[n][b] = fp16 nearest to max_{k in b} |W[n][k]| / Q   (ties to even)
+ *     c[n][k] = clamp(nearest integer to W[n][k] / s[n][b], -Q, Q)
+ *               (ties to even; all codes 0 when s == 0)
+ *     Q = 127 (QL_FMT_INT8) or 7 (QL_FMT_Q4)
+ *
+ * and the forward product of one linear layer (no bias)
+ *
+ *     Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k]
+ *
+ * with W [N][K] (out x in, like a framework's Linear weight), X [M][K] and
+ * Y [M][N], all row-major.
+ *
+ * Data formats (all buffers are DEVICE memory owned by the caller):
+ *   W       fp32 [N][K]
+ *   codes   QL_FMT_INT8: int8 [N][K], two's complement
+ *           QL_FMT_Q4:   uint8 [N][K/2]; byte j of a row holds code 2j in its
+ *                        low nibble and code 2j+1 in its high nibble, both
+ *                        two's complement (the stored codes -128 / -8 are
+ *                        accepted by the forward pass, never produced)
+ *   scales  fp16 bit patterns, uint16 [N][K/32]
+ *   X       QL_DT_BF16: bf16 bit patterns, uint16 [M][K]; QL_DT_F32: fp32
+ *   Y       fp32 [M][N]
+ *
+ * Conventions shared by every entry point:
+ *   - Every function returns a ql_status (an int) and never aborts or throws.
+ *   - All argument checks happen before anything is enqueued; a call that
+ *     returns an error has enqueued nothing.
+ *   - Alignment: codes and X must be 16-byte aligned, scales 2-byte and Y
+ *     4-byte aligned (QL_ERR_ALIGN otherwise).
+ *   - Work runs on the caller's HIP stream; only qlinear_quantize waits for
+ *     its own work.  Buffers must stay alive until the stream has passed the
+ *     enqueued work.  Asynchronous device faults surface at the caller's next
+ *     synchronization, as in HIP itself.
+ *   - The library keeps no pointer after a call returns.
+ */
+#ifndef QLINEAR_H
+#define QLINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    QL_OK = 0,
+    QL_ERR_INVALID = 1,     /* null pointer, unknown enum value, n_lin out of range */
+    QL_ERR_SHAPE = 2,       /* K % 32 != 0, N <= 0, K <= 0, M < 0 */
+    QL_ERR_ALIGN = 3,       /* pointer alignment (see above) */
+    QL_ERR_RANGE = 4,       /* weight NaN/Inf, or a block's scale overflows fp16 */
+    QL_ERR_UNSUPPORTED = 5, /* size beyond what the kernels index (see below) */
+    QL_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+} ql_status;
+
+typedef enum { QL_FMT_Q4 = 4, QL_FMT_INT8 = 8 } ql_fmt;   /* block fixed at 32 along K */
+typedef enum { QL_DT_F32 = 0, QL_DT_BF16 = 1 } ql_dtype; /* activation dtype; Y is fp32 */
+
+#define QL_BLOCK 32
+
+/* Bytes of the packed codes of an N x K weight: N*K (int8) or N*K/2 (q4).
+ * Returns 0 for an unknown format or a non-positive size. */
+size_t qlinear_codes_bytes(int fmt, int64_t N, int64_t K);
+
+/* Bytes of the fp16 scales of an N x K weight: N * (K/32) * 2.
+ * Returns 0 when K % 32 != 0 or a size is non-positive. */
+size_t qlinear_scales_bytes(int64_t N, int64_t K);
+
+/* Quantize W (fp32 [N][K], device) into codes and scales (device), by the
+ * rule at the top of this file.  Synchronous: waits for its own work on
+ * `stream` and reports QL_ERR_RANGE if W holds a NaN/Inf or a block's
+ * scale rounds to +inf (absmax / Q >= 65520); the outputs are then
+ * unspecified.  Once it returns QL_OK the caller may free W: the codes and
+ * scales replace the full-precision copy (paper: the compressed copy owns its
+ * memory and the source is released once packed).  Allocates and frees one
+ * 4-byte device status word per call (a load-time operation, not a per-step
+ * one).  Sizes: N * K < 2^40. */
+int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K,
+                     void *codes, uint16_t *scales, hipStream_t stream);
+
+/* Y[M][N] (fp32) = X[M][K] * dequant(codes, scales)^T, the forward pass of
+ * one quantized linear layer.  Asynchronous on `stream`; allocates nothing
+ * and does not synchronize.  M == 0 is a successful no-op.  Y must not alias
+ * X, codes or scales.  Sizes: M, N < 2^31, K < 2^31. */
+int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K,
+                    const void *codes, const uint16_t *scales, int64_t N,
+                    float *Y, hipStream_t stream);
+
+/* One quantized linear layer for qlinear_block_forward. */
+typedef struct {
+    int fmt;                /* ql_fmt */
+    const void *X;          /* [M][K], dtype xdt */
+    int xdt;                /* ql_dtype */
+    int64_t M, K, N;
+    const void *codes;
+    const uint16_t *scales;
+    float *Y;               /* [M][N] */
+} ql_linear;
+
+#define QL_MAX_GROUP 8
+
+/* The linear layers of one transformer block (QKV projection, attention
+ * output, FFN up and FFN down: the set the paper quantizes) evaluated as one
+ * grouped launch.  The n_lin (1..QL_MAX_GROUP) products are independent:
+ * no Y may alias any X, codes, scales or other Y of the group.  Layers that
+ * share fmt and xdt run in one launch over their combined tiles; otherwise
+ * the call falls back to one launch per layer.  Asynchronous on `stream`,
+ * allocates nothing.  Each entry is checked as in qlinear_forward. */
+int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream);
+
+/* Static description of a status code. */
+const char *qlinear_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLINEAR_H */

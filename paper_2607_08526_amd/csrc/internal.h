@@ -1,0 +1,42 @@
+// Internal declarations shared by the HIP translation units of the library.
+// Not part of the public interface (that is include/qlinear.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "qlinear.h"
+
+namespace qlk {
+
+// Activations and packed codes of one linear layer as the kernels see it.
+struct LinDesc {
+    const void *X;
+    const uint8_t *codes;
+    const uint16_t *scales;
+    float *Y;
+    int M, N, K;
+    int tiles_m, tiles_n;
+    int tile_begin;  // first logical tile of this layer in a grouped launch
+};
+
+struct GroupArgs {
+    LinDesc d[QL_MAX_GROUP];
+    int n;
+    int total_tiles;
+};
+
+// Tile shapes of the MFMA kernel (see qgemm.hip): BM rows of X by BN rows of
+// W.  fp32 activations support TILE_M16..TILE_M64 only.
+enum TileCfg { TILE_M16 = 0, TILE_M32 = 1, TILE_M64 = 2, TILE_M128 = 3 };
+
+int tile_bm(TileCfg t);
+int tile_bn(TileCfg t);
+
+hipError_t launch_quantize(int fmt, const float *W, int64_t N, int64_t K, uint8_t *codes,
+                           uint16_t *scales, int *status, hipStream_t stream);
+
+hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
+                        hipStream_t stream);
+
+}  // namespace qlk

@@ -1,0 +1,187 @@
+// C-ABI entry points of the block-quantized linear library (include/qlinear.h):
+// argument checks, tile-shape choice and launch.  Every check happens before
+// anything is enqueued; no entry point throws or aborts.
+#include <algorithm>
+
+#include "internal.h"
+
+using namespace qlk;
+
+namespace {
+
+constexpr int64_t I31 = (int64_t)1 << 31;
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+bool fmt_ok(int f) { return f == QL_FMT_INT8 || f == QL_FMT_Q4; }
+
+int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
+                 const uint16_t *scales, int64_t N, const float *Y)
+{
+    if (!fmt_ok(fmt) || (xdt != QL_DT_F32 && xdt != QL_DT_BF16))
+        return QL_ERR_INVALID;
+    if (M < 0 || N <= 0 || K <= 0 || K % QL_BLOCK)
+        return QL_ERR_SHAPE;
+    if (M >= I31 || N >= I31 || K >= I31)
+        return QL_ERR_UNSUPPORTED;
+    if (!codes || !scales || (M > 0 && (!X || !Y)))
+        return QL_ERR_INVALID;
+    if (!aligned(codes, 16) || !aligned(scales, 2) || (M > 0 && (!aligned(X, 16) ||
+                                                                 !aligned(Y, 4))))
+        return QL_ERR_ALIGN;
+    return QL_OK;
+}
+
+TileCfg choose_tile(int64_t M, bool xf32)
+{
+    if (M <= 16)
+        return TILE_M16;
+    if (M <= 32)
+        return TILE_M32;
+    if (M <= 64 || xf32)
+        return TILE_M64;
+    return TILE_M128;
+}
+
+// One grouped launch over layers that share fmt and xdt (M > 0 each).
+int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
+{
+    if (n == 0)
+        return QL_OK;
+    const bool xf32 = ls[0]->xdt == QL_DT_F32;
+    int64_t maxM = 0;
+    for (int i = 0; i < n; ++i)
+        maxM = std::max(maxM, ls[i]->M);
+    const TileCfg t = choose_tile(maxM, xf32);
+    const int bm = tile_bm(t), bn = tile_bn(t);
+
+    // longest reduction first, so the long tiles start early
+    const ql_linear *ord[QL_MAX_GROUP];
+    std::copy(ls, ls + n, ord);
+    std::stable_sort(ord, ord + n,
+                     [](const ql_linear *a, const ql_linear *b) { return a->K > b->K; });
+
+    GroupArgs a{};
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        d.X = ord[i]->X;
+        d.codes = (const uint8_t *)ord[i]->codes;
+        d.scales = ord[i]->scales;
+        d.Y = ord[i]->Y;
+        d.M = (int)ord[i]->M;
+        d.N = (int)ord[i]->N;
+        d.K = (int)ord[i]->K;
+        d.tiles_m = (int)((ord[i]->M + bm - 1) / bm);
+        d.tiles_n = (int)((ord[i]->N + bn - 1) / bn);
+        d.tile_begin = (int)total;
+        total += (int64_t)d.tiles_m * d.tiles_n;
+    }
+    if (total >= I31)
+        return QL_ERR_UNSUPPORTED;
+    a.n = n;
+    a.total_tiles = (int)total;
+    return launch_qgemm(ord[0]->fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t qlinear_codes_bytes(int fmt, int64_t N, int64_t K)
+{
+    if (!fmt_ok(fmt) || N <= 0 || K <= 0)
+        return 0;
+    return fmt == QL_FMT_INT8 ? (size_t)N * (size_t)K : (size_t)N * (size_t)(K / 2);
+}
+
+size_t qlinear_scales_bytes(int64_t N, int64_t K)
+{
+    if (N <= 0 || K <= 0 || K % QL_BLOCK)
+        return 0;
+    return (size_t)N * (size_t)(K / QL_BLOCK) * 2;
+}
+
+int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K, void *codes,
+                     uint16_t *scales, hipStream_t stream)
+{
+    if (!fmt_ok(fmt))
+        return QL_ERR_INVALID;
+    if (N <= 0 || K <= 0 || K % QL_BLOCK)
+        return QL_ERR_SHAPE;
+    if (N >= ((int64_t)1 << 40) / K)
+        return QL_ERR_UNSUPPORTED;
+    if (!W || !codes || !scales)
+        return QL_ERR_INVALID;
+    if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2))
+        return QL_ERR_ALIGN;
+
+    int *dstatus = nullptr;
+    if (hipMalloc(&dstatus, sizeof(int)) != hipSuccess)
+        return QL_ERR_HIP;
+    int hstatus = QL_OK;
+    bool ok = hipMemsetAsync(dstatus, 0, sizeof(int), stream) == hipSuccess;
+    ok = ok && launch_quantize(fmt, W, N, K, (uint8_t *)codes, scales, dstatus, stream) ==
+                   hipSuccess;
+    ok = ok && hipMemcpyAsync(&hstatus, dstatus, sizeof(int), hipMemcpyDeviceToHost, stream) ==
+                   hipSuccess;
+    ok = ok && hipStreamSynchronize(stream) == hipSuccess;
+    hipFree(dstatus);
+    if (!ok)
+        return QL_ERR_HIP;
+    return hstatus;
+}
+
+int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
+                    const uint16_t *scales, int64_t N, float *Y, hipStream_t stream)
+{
+    const int st = check_linear(fmt, X, xdt, M, K, codes, scales, N, Y);
+    if (st != QL_OK || M == 0)
+        return st;
+    ql_linear l{fmt, X, xdt, M, K, N, codes, scales, Y};
+    const ql_linear *p = &l;
+    return launch_group(&p, 1, stream);
+}
+
+int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
+{
+    if (!lin || n_lin < 1 || n_lin > QL_MAX_GROUP)
+        return QL_ERR_INVALID;
+    for (int i = 0; i < n_lin; ++i) {
+        const ql_linear &l = lin[i];
+        const int st = check_linear(l.fmt, l.X, l.xdt, l.M, l.K, l.codes, l.scales, l.N, l.Y);
+        if (st != QL_OK)
+            return st;
+    }
+    // partition the non-empty layers by (fmt, xdt); each class is one launch
+    const ql_linear *cls[4][QL_MAX_GROUP];
+    int cnt[4] = {0, 0, 0, 0};
+    for (int i = 0; i < n_lin; ++i) {
+        if (lin[i].M == 0)
+            continue;
+        const int c = (lin[i].fmt == QL_FMT_INT8 ? 2 : 0) + (lin[i].xdt == QL_DT_BF16 ? 1 : 0);
+        cls[c][cnt[c]++] = &lin[i];
+    }
+    for (int c = 0; c < 4; ++c) {
+        const int st = launch_group(cls[c], cnt[c], stream);
+        if (st != QL_OK)
+            return st;
+    }
+    return QL_OK;
+}
+
+const char *qlinear_status_string(int status)
+{
+    switch (status) {
+    case QL_OK: return "ok";
+    case QL_ERR_INVALID: return "invalid argument (null pointer, unknown enum, bad count)";
+    case QL_ERR_SHAPE: return "bad shape (K must be a positive multiple of 32, N > 0, M >= 0)";
+    case QL_ERR_ALIGN: return "misaligned pointer (codes/X 16 B, scales 2 B, Y 4 B)";
+    case QL_ERR_RANGE: return "weights hold NaN/Inf or a block scale overflows fp16";
+    case QL_ERR_UNSUPPORTED: return "size beyond what the kernels index";
+    case QL_ERR_HIP: return "HIP runtime or launch failure";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

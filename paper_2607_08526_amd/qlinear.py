@@ -1,0 +1,198 @@
+"""Python binding of libqlinear.so (include/qlinear.h).
+
+Argument marshalling only: every step of quantization and of the forward
+product runs in the library's HIP kernels.  PyTorch provides device memory
+and the current HIP stream.  There is no fallback: if the library is missing
+or the process has no GPU, calls raise.
+"""
+import ctypes
+import os
+
+import torch
+
+from . import build as _build
+
+FMT_Q4 = 4
+FMT_INT8 = 8
+DT_F32 = 0
+DT_BF16 = 1
+BLOCK = 32
+MAX_GROUP = 8
+
+STATUS = {
+    0: "QL_OK", 1: "QL_ERR_INVALID", 2: "QL_ERR_SHAPE", 3: "QL_ERR_ALIGN",
+    4: "QL_ERR_RANGE", 5: "QL_ERR_UNSUPPORTED", 6: "QL_ERR_HIP",
+}
+
+EXPORTS = [
+    "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
+    "qlinear_forward", "qlinear_block_forward", "qlinear_status_string",
+]
+
+
+class QLinearError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class _Linear(ctypes.Structure):
+    _fields_ = [
+        ("fmt", ctypes.c_int),
+        ("X", ctypes.c_void_p),
+        ("xdt", ctypes.c_int),
+        ("M", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+        ("N", ctypes.c_int64),
+        ("codes", ctypes.c_void_p),
+        ("scales", ctypes.c_void_p),
+        ("Y", ctypes.c_void_p),
+    ]
+
+
+_LIB = None
+
+
+def lib_path():
+    return _build.LIB
+
+
+def _hip_runtimes_mapped():
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            p = line.split()[-1] if len(line.split()) >= 6 else ""
+            if "libamdhip64.so" in p:
+                paths.add(os.path.realpath(p))
+    return paths
+
+
+def load():
+    """Load libqlinear.so (built in-tree by build.py); raises if absent."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with "
+                          "`python -m paper_2607_08526_amd.build` (no CPU fallback exists)")
+    # torch's HIP runtime is loaded first (import above), so the library's
+    # libamdhip64.so.7 dependency resolves to that same copy: device pointers
+    # and streams from torch are then valid inside the library.
+    lib = ctypes.CDLL(path)
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.qlinear_codes_bytes.argtypes = [ci, i64, i64]
+    lib.qlinear_codes_bytes.restype = ctypes.c_size_t
+    lib.qlinear_scales_bytes.argtypes = [i64, i64]
+    lib.qlinear_scales_bytes.restype = ctypes.c_size_t
+    lib.qlinear_quantize.argtypes = [ci, vp, i64, i64, vp, vp, vp]
+    lib.qlinear_quantize.restype = ci
+    lib.qlinear_forward.argtypes = [ci, vp, ci, i64, i64, vp, vp, i64, vp, vp]
+    lib.qlinear_forward.restype = ci
+    lib.qlinear_block_forward.argtypes = [ctypes.POINTER(_Linear), ci, vp]
+    lib.qlinear_block_forward.restype = ci
+    lib.qlinear_status_string.argtypes = [ci]
+    lib.qlinear_status_string.restype = ctypes.c_char_p
+    if len(_hip_runtimes_mapped()) > 1:
+        raise ImportError(f"two HIP runtimes are mapped: {_hip_runtimes_mapped()}")
+    _LIB = lib
+    return lib
+
+
+def _check(status):
+    if status != 0:
+        raise QLinearError(status, load().qlinear_status_string(status).decode())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def codes_bytes(fmt, N, K):
+    return int(load().qlinear_codes_bytes(fmt, N, K))
+
+
+def scales_bytes(N, K):
+    return int(load().qlinear_scales_bytes(N, K))
+
+
+def empty_codes(fmt, N, K, device="cuda"):
+    return torch.empty((N, K) if fmt == FMT_INT8 else (N, K // 2), dtype=torch.uint8,
+                       device=device)
+
+
+def empty_scales(N, K, device="cuda"):
+    # fp16 bit patterns; int16 storage so torch never reinterprets them
+    return torch.empty((N, K // BLOCK), dtype=torch.int16, device=device)
+
+
+def quantize(fmt, W, codes=None, scales=None, stream=None):
+    """Quantize fp32 W [N][K] (device) -> (codes, scales).  Synchronous."""
+    N, K = W.shape
+    codes = empty_codes(fmt, N, K, W.device) if codes is None else codes
+    scales = empty_scales(N, K, W.device) if scales is None else scales
+    _check(load().qlinear_quantize(fmt, _ptr(W), N, K, _ptr(codes), _ptr(scales),
+                                   _stream(stream)))
+    return codes, scales
+
+
+def _xdt(X):
+    if X.dtype == torch.float32:
+        return DT_F32
+    if X.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return DT_BF16
+    raise TypeError(f"activations must be float32 or bfloat16, not {X.dtype}")
+
+
+def forward(fmt, X, codes, scales, N, Y=None, stream=None):
+    """Y [M][N] fp32 = X [M][K] . dequant(codes, scales)^T.  Asynchronous."""
+    M, K = X.shape
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    _check(load().qlinear_forward(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
+                                  _ptr(Y), _stream(stream)))
+    return Y
+
+
+def make_group(entries):
+    """ctypes array for block_forward from (fmt, X, codes, scales, N, Y) tuples.
+    The tensors must outlive every use of the returned array."""
+    arr = (_Linear * len(entries))()
+    for i, (fmt, X, codes, scales, N, Y) in enumerate(entries):
+        M, K = X.shape
+        arr[i] = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
+                         scales.data_ptr(), Y.data_ptr())
+    return arr
+
+
+def block_forward(entries, stream=None, group=None):
+    """Grouped forward of up to 8 independent linears (one DiT block's QKV,
+    out, FFN-up, FFN-down).  entries: (fmt, X, codes, scales, N, Y) tuples.
+    Asynchronous.  A prepared `group` (make_group) skips re-marshalling."""
+    arr = group if group is not None else make_group(entries)
+    _check(load().qlinear_block_forward(arr, len(arr), _stream(stream)))
+    return [e[5] for e in entries] if entries is not None else None
+
+
+class QuantizedLinear:
+    """A linear layer's weight held only as codes + scales on the device.
+
+    from_float() quantizes and keeps no full-precision copy: the compressed
+    weight replaces the original (the caller drops its fp32 tensor).
+    """
+
+    def __init__(self, fmt, codes, scales, N, K):
+        self.fmt, self.codes, self.scales, self.N, self.K = fmt, codes, scales, N, K
+
+    @classmethod
+    def from_float(cls, W, fmt):
+        codes, scales = quantize(fmt, W)
+        return cls(fmt, codes, scales, W.shape[0], W.shape[1])
+
+    def __call__(self, X, Y=None, stream=None):
+        return forward(self.fmt, X, self.codes, self.scales, self.N, Y, stream)

@@ -1,0 +1,122 @@
+"""The C-ABI library loads, exports every function include/qlinear.h declares,
+and rejects bad arguments before touching the GPU (CPU only: no call here
+reaches a kernel launch or any HIP runtime call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qlinear.h")
+LIB = os.path.join(ROOT, "paper_2607_08526_amd", "libqlinear.so")
+
+OK, INVALID, SHAPE, ALIGN, RANGE, UNSUPPORTED, HIP = range(7)
+Q4, INT8, F32, BF16 = 4, 8, 0, 1
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(qlinear_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail(f"{LIB} not built (run __graft_entry__.build())")
+    import torch  # noqa: F401  (same HIP runtime the GPU tests use)
+    lib = ctypes.CDLL(LIB)
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.qlinear_codes_bytes.argtypes = [ci, i64, i64]
+    lib.qlinear_codes_bytes.restype = ctypes.c_size_t
+    lib.qlinear_scales_bytes.argtypes = [i64, i64]
+    lib.qlinear_scales_bytes.restype = ctypes.c_size_t
+    lib.qlinear_quantize.argtypes = [ci, vp, i64, i64, vp, vp, vp]
+    lib.qlinear_forward.argtypes = [ci, vp, ci, i64, i64, vp, vp, i64, vp, vp]
+    lib.qlinear_status_string.restype = ctypes.c_char_p
+    return lib
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted([
+        "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
+        "qlinear_forward", "qlinear_block_forward", "qlinear_status_string"])
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_size_helpers(lib):
+    assert lib.qlinear_codes_bytes(INT8, 6144, 2048) == 6144 * 2048
+    assert lib.qlinear_codes_bytes(Q4, 6144, 2048) == 6144 * 1024
+    assert lib.qlinear_codes_bytes(5, 6144, 2048) == 0
+    assert lib.qlinear_scales_bytes(6144, 2048) == 6144 * 64 * 2
+    assert lib.qlinear_scales_bytes(6144, 2047) == 0
+    assert lib.qlinear_scales_bytes(0, 64) == 0
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert lib.qlinear_status_string(s)
+    assert lib.qlinear_status_string(99) == b"unknown status"
+
+
+# fake, never dereferenced device addresses (every call below fails its checks
+# before any HIP call, or is the M == 0 no-op)
+A16 = 0x10000
+A2 = 0x10002
+A1 = 0x10001
+
+
+def fwd(lib, fmt=INT8, X=A16, xdt=BF16, M=4, K=64, codes=A16, scales=A16, N=16, Y=A16):
+    return lib.qlinear_forward(fmt, X, xdt, M, K, codes, scales, N, Y, None)
+
+
+def test_forward_argument_errors(lib):
+    assert fwd(lib, fmt=5) == INVALID
+    assert fwd(lib, xdt=2) == INVALID
+    assert fwd(lib, K=48) == SHAPE
+    assert fwd(lib, K=0) == SHAPE
+    assert fwd(lib, N=0) == SHAPE
+    assert fwd(lib, M=-1) == SHAPE
+    assert fwd(lib, X=None) == INVALID
+    assert fwd(lib, codes=None) == INVALID
+    assert fwd(lib, scales=None) == INVALID
+    assert fwd(lib, Y=None) == INVALID
+    assert fwd(lib, X=A2) == ALIGN
+    assert fwd(lib, codes=A2) == ALIGN
+    assert fwd(lib, scales=A1) == ALIGN
+    assert fwd(lib, Y=A2) == ALIGN
+    assert fwd(lib, M=1 << 31) == UNSUPPORTED
+    # M == 0 is a successful no-op even without activation/output buffers
+    assert fwd(lib, M=0, X=None, Y=None) == OK
+
+
+def test_quantize_argument_errors(lib):
+    q = lambda fmt=INT8, W=A16, N=8, K=64, c=A16, s=A16: lib.qlinear_quantize(fmt, W, N, K, c, s, None)
+    assert q(fmt=3) == INVALID
+    assert q(K=40) == SHAPE
+    assert q(N=0) == SHAPE
+    assert q(W=None) == INVALID
+    assert q(c=None) == INVALID
+    assert q(W=A2) == ALIGN
+    assert q(c=A2) == ALIGN
+    assert q(s=A1) == ALIGN
+    assert q(N=1 << 40) == UNSUPPORTED
+
+
+def test_block_forward_argument_errors(lib):
+    from paper_2607_08526_amd.qlinear import _Linear
+    arr = (_Linear * 2)()
+    arr[0] = _Linear(INT8, A16, BF16, 4, 64, 16, A16, A16, A16)
+    arr[1] = _Linear(INT8, A16, BF16, 4, 48, 16, A16, A16, A16)  # bad K
+    assert lib.qlinear_block_forward(arr, 2, None) == SHAPE
+    assert lib.qlinear_block_forward(arr, 0, None) == INVALID
+    assert lib.qlinear_block_forward(arr, 9, None) == INVALID
+    assert lib.qlinear_block_forward(None, 1, None) == INVALID
+    empty = (_Linear * 1)()
+    empty[0] = _Linear(Q4, None, BF16, 0, 64, 16, A16, A16, None)
+    assert lib.qlinear_block_forward(empty, 1, None) == OK  # all layers empty: no-op

@@ -1,0 +1,305 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Codes and scales must match the oracle bit for bit.  Outputs must satisfy
+max |Y_gpu - Y_ref| / max |Y_ref| <= 2e-3 for bf16 activations and <= 1e-5
+for fp32 activations (Y_ref the fp64 oracle result); constructions whose
+exact answer is representable must match exactly.
+"""
+import numpy as np
+import pytest
+
+import synth_inputs as si
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+TOL = {O.DT_BF16: 2e-3, O.DT_F32: 1e-5}
+QMAX = {O.FMT_INT8: 127, O.FMT_Q4: 7}
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU (run with -m 'not gpu' on a CPU host)")
+    from paper_2607_08526_amd import qlinear as ql
+    ql.load()
+    return torch, ql
+
+
+def dev_w(torch, W):
+    return torch.from_numpy(np.ascontiguousarray(W, dtype=np.float32)).cuda()
+
+
+def dev_x(torch, X, xdt):
+    if xdt == O.DT_F32:
+        return torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).cuda()
+    return torch.from_numpy(np.ascontiguousarray(X, dtype=np.uint16).view(np.int16)).cuda()
+
+
+def host_codes(c):
+    return c.cpu().numpy().astype(np.uint8)
+
+
+def host_scales(s):
+    return s.cpu().numpy().view(np.uint16)
+
+
+def rel_err(Yg, Yr):
+    return float(np.max(np.abs(Yg.astype(np.float64) - Yr)) / np.max(np.abs(Yr)))
+
+
+def quantize_both(gpu, orc, fmt, W):
+    torch, ql = gpu
+    cg, sg = ql.quantize(fmt, dev_w(torch, W))
+    cr, sr = orc.quantize(fmt, W)
+    cg, sg = host_codes(cg), host_scales(sg)
+    assert np.array_equal(sg, sr), f"scales differ at {np.argwhere(sg != sr)[:5]}"
+    assert np.array_equal(cg, cr), f"codes differ at {np.argwhere(cg != cr)[:5]}"
+    return cr, sr
+
+
+def forward_gpu(gpu, fmt, X, xdt, codes, scales, N):
+    torch, ql = gpu
+    cd = torch.from_numpy(codes).cuda()
+    sd = torch.from_numpy(scales.view(np.int16)).cuda()
+    Y = ql.forward(fmt, dev_x(torch, X, xdt), cd, sd, N)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy()
+
+
+# --------------------------------------------------------------------------
+# quantizer: bit-exact
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+@pytest.mark.parametrize("N,K", [(1, 32), (3, 96), (70, 320), (257, 1024)])
+def test_quantize_bitexact_small(gpu, orc, fmt, N, K):
+    W, _ = si.small_case(N * 7 + K + fmt, 1, N, K)
+    quantize_both(gpu, orc, fmt, W)
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_quantize_bitexact_adversarial(gpu, orc, fmt):
+    import test_oracle_pins as pins
+    blocks = pins.adversarial_blocks(QMAX[fmt])
+    blocks += list(pins.random_blocks(fmt + 1, 64, 3.0)) + list(pins.random_blocks(fmt + 2, 64, 1e-5))
+    W = np.stack(blocks).astype(np.float32).reshape(-1, 64)  # two blocks per row
+    quantize_both(gpu, orc, fmt, W)
+
+
+@pytest.mark.parametrize("name", ["single_int8", "single_q4"])
+def test_quantize_bitexact_single_configs(gpu, orc, name):
+    cfg = getattr(si, name)()
+    quantize_both(gpu, orc, cfg["fmt"], cfg["W"])
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_quantize_range_errors(gpu, fmt):
+    torch, ql = gpu
+    W = np.zeros((4, 64), np.float32)
+    for bad in (np.nan, np.inf):
+        Wb = W.copy(); Wb[2, 33] = bad
+        with pytest.raises(ql.QLinearError) as e:
+            ql.quantize(fmt, dev_w(torch, Wb))
+        assert e.value.status == 4
+    Wb = W.copy(); Wb[1, 0] = np.float32(65520.0 * QMAX[fmt])
+    with pytest.raises(ql.QLinearError) as e:
+        ql.quantize(fmt, dev_w(torch, Wb))
+    assert e.value.status == 4
+    Wb = W.copy(); Wb[1, 0] = np.float32(65504.0 * QMAX[fmt])
+    ql.quantize(fmt, dev_w(torch, Wb))  # the largest finite scale is fine
+
+
+# --------------------------------------------------------------------------
+# forward: ragged shapes across every tile configuration
+# --------------------------------------------------------------------------
+
+MS = [1, 2, 15, 16, 17, 33, 64, 65, 127, 130, 257]
+NKS = [(16, 32), (70, 96), (200, 320)]
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+@pytest.mark.parametrize("xdt", [O.DT_BF16, O.DT_F32])
+@pytest.mark.parametrize("N,K", NKS)
+def test_forward_ragged(gpu, orc, fmt, xdt, N, K):
+    for M in MS:
+        W, X = si.small_case(1000 + M + N + K + fmt + xdt, M, N, K, xdt)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, xdt, codes, scales, N)
+        Yr = orc.forward(fmt, X, xdt, codes, scales, N)
+        e = rel_err(Yg, Yr)
+        assert e <= TOL[xdt], (M, N, K, e)
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+@pytest.mark.parametrize("xdt", [O.DT_BF16, O.DT_F32])
+def test_forward_power_of_two_exact(gpu, orc, fmt, xdt):
+    """W = c * 2^-12, integer X: the exact result is representable, so the
+    GPU must reproduce it exactly."""
+    Q = QMAX[fmt]
+    rng = np.random.default_rng(17 + fmt + xdt)
+    N, K = 80, 512
+    for M in (5, 40, 200):
+        C = rng.integers(-Q, Q + 1, (N, K))
+        C.reshape(N, K // 32, 32)[:, :, 3] = rng.choice([-Q, Q], (N, K // 32))
+        W = (C * 2.0 ** -12).astype(np.float32)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Xi = rng.integers(-8, 9, (M, K)).astype(np.float32)
+        X = Xi if xdt == O.DT_F32 else si.f32_to_bf16_bits(Xi)
+        Yg = forward_gpu(gpu, fmt, X, xdt, codes, scales, N)
+        want = (Xi.astype(np.int64) @ C.T).astype(np.float64) * 2.0 ** -12
+        assert np.array_equal(Yg.astype(np.float64), want)
+        assert np.array_equal(Yg.astype(np.float64), orc.forward(fmt, X, xdt, codes, scales, N))
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_stored_extreme_codes_exact(gpu, orc, fmt):
+    """Codes set by hand (including the never-produced -128 / -8) with unit
+    scales and integer activations: Y is an exact integer matmul."""
+    Q = QMAX[fmt]
+    rng = np.random.default_rng(23 + fmt)
+    M, N, K = 37, 48, 96
+    C = rng.integers(-Q - 1, Q + 1, (N, K))
+    C[:, 0] = -Q - 1
+    if fmt == O.FMT_INT8:
+        codes = C.astype(np.int8).view(np.uint8)
+    else:
+        u = (C & 0xF).astype(np.uint8)
+        codes = (u[:, 0::2] | (u[:, 1::2] << 4)).astype(np.uint8)
+    scales = np.full((N, K // 32), 0x3C00, np.uint16)
+    Xi = rng.integers(-100, 101, (M, K)).astype(np.float32)
+    for xdt, X in ((O.DT_F32, Xi), (O.DT_BF16, si.f32_to_bf16_bits(Xi))):
+        Yg = forward_gpu(gpu, fmt, X, xdt, codes, scales, N)
+        assert np.array_equal(Yg.astype(np.int64), Xi.astype(np.int64) @ C.T)
+
+
+def test_forward_deterministic(gpu, orc):
+    torch, ql = gpu
+    W, X = si.small_case(5, 300, 520, 1024, O.DT_BF16)
+    codes, scales = orc.quantize(O.FMT_Q4, W)
+    a = forward_gpu(gpu, O.FMT_Q4, X, O.DT_BF16, codes, scales, 520)
+    b = forward_gpu(gpu, O.FMT_Q4, X, O.DT_BF16, codes, scales, 520)
+    assert np.array_equal(a, b)
+
+
+def test_forward_on_side_stream(gpu, orc):
+    torch, ql = gpu
+    W, X = si.small_case(6, 50, 130, 256, O.DT_BF16)
+    codes, scales = orc.quantize(O.FMT_INT8, W)
+    s = torch.cuda.Stream()
+    cd = torch.from_numpy(codes).cuda()
+    sd = torch.from_numpy(scales.view(np.int16)).cuda()
+    xd = dev_x(torch, X, O.DT_BF16)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        Y = ql.forward(O.FMT_INT8, xd, cd, sd, 130)
+    s.synchronize()
+    e = rel_err(Y.cpu().numpy(), orc.forward(O.FMT_INT8, X, O.DT_BF16, codes, scales, 130))
+    assert e <= TOL[O.DT_BF16]
+
+
+# --------------------------------------------------------------------------
+# the workload configurations
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["single_int8", "single_q4"])
+def test_single_linear_configs(gpu, orc, name):
+    cfg = getattr(si, name)()
+    fmt, W, X, xdt = cfg["fmt"], cfg["W"], cfg["X"], cfg["xdt"]
+    codes, scales = quantize_both(gpu, orc, fmt, W)
+    Yg = forward_gpu(gpu, fmt, X, xdt, codes, scales, W.shape[0])
+    Yr = orc.forward(fmt, X, xdt, codes, scales, W.shape[0])
+    e = rel_err(Yg, Yr)
+    print(f"{name}: max err / |y|inf = {e:.3e}")
+    assert e <= TOL[xdt]
+
+
+def sample_rows(M, k, seed):
+    rng = np.random.default_rng(seed)
+    rows = set([0, M - 1]) | set(rng.choice(M, size=min(k, M), replace=False).tolist())
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def run_block(gpu, orc, fmt, weights, xa, xb, rows, check_codes=True):
+    """One DiT block's four linears through qlinear_block_forward; checks the
+    sampled rows of every output against the oracle."""
+    torch, ql = gpu
+    xa_d, xb_d = dev_x(torch, xa, O.DT_BF16), dev_x(torch, xb, O.DT_BF16)
+    entries, host = [], []
+    for i, W in enumerate(weights):
+        N, K = W.shape
+        cd, sd = ql.quantize(fmt, dev_w(torch, W))
+        if check_codes:
+            cr, sr = orc.quantize(fmt, W)
+            assert np.array_equal(host_scales(sd), sr)
+            assert np.array_equal(host_codes(cd), cr)
+        else:
+            cr, sr = host_codes(cd), host_scales(sd)
+        Y = torch.empty((xa.shape[0], N), dtype=torch.float32, device="cuda")
+        entries.append((fmt, xb_d if K == 4 * xa.shape[1] else xa_d, cd, sd, N, Y))
+        host.append((cr, sr, N, K))
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    errs = []
+    for (fmt_, X_d, cd, sd, N, Y), (cr, sr, N_, K) in zip(entries, host):
+        X = xb if K == 4 * xa.shape[1] else xa
+        Yr = orc.forward(fmt, X, O.DT_BF16, cr, sr, N, rows=rows)
+        Yg = Y.cpu().numpy()[rows]
+        errs.append(rel_err(Yg, Yr))
+    return errs
+
+
+def test_block_int8_config(gpu, orc):
+    xa, xb = si.block_activations()
+    weights = [si.block_int8_weight(i) for i in range(4)]
+    rows = sample_rows(xa.shape[0], 14, 0)
+    errs = run_block(gpu, orc, O.FMT_INT8, weights, xa, xb, rows)
+    print("block int8 errs", errs)
+    assert max(errs) <= TOL[O.DT_BF16]
+
+
+@pytest.mark.parametrize("blk", [0, 23])
+def test_step_q4_config_sampled_blocks(gpu, orc, blk):
+    xa, xb = si.block_activations()
+    weights = [si.step_q4_weight(blk, i) for i in range(4)]
+    rows = sample_rows(xa.shape[0], 6, blk)
+    errs = run_block(gpu, orc, O.FMT_Q4, weights, xa, xb, rows)
+    print(f"step q4 block {blk} errs", errs)
+    assert max(errs) <= TOL[O.DT_BF16]
+
+
+@pytest.mark.parametrize("v,fmt,N,K", si.skinny_variants())
+def test_skinny_configs(gpu, orc, v, fmt, N, K):
+    W = si.skinny_weight(v, N, K)
+    codes, scales = quantize_both(gpu, orc, fmt, W)
+    for M in si.SKINNY_M:
+        X = si.skinny_activations(M, K)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        rows = np.arange(M) if M <= 32 else sample_rows(M, 30, M)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N, rows=rows)
+        e = rel_err(Yg[rows], Yr)
+        print(f"skinny v{v} M={M}: {e:.3e}")
+        assert e <= TOL[O.DT_BF16]
+
+
+def test_block_forward_mixed_group(gpu, orc):
+    """Layers of different formats / activation dtypes in one call."""
+    torch, ql = gpu
+    specs = [(O.FMT_INT8, O.DT_BF16, 40, 96, 64), (O.FMT_Q4, O.DT_BF16, 40, 200, 128),
+             (O.FMT_INT8, O.DT_F32, 17, 64, 96), (O.FMT_Q4, O.DT_F32, 3, 48, 32),
+             (O.FMT_Q4, O.DT_BF16, 0, 16, 32)]
+    entries, refs = [], []
+    for i, (fmt, xdt, M, N, K) in enumerate(specs):
+        W, X = si.small_case(300 + i, M, N, K, xdt)
+        cd, sd = ql.quantize(fmt, dev_w(torch, W))
+        cr, sr = orc.quantize(fmt, W)
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        entries.append((fmt, dev_x(torch, X, xdt), cd, sd, N, Y))
+        refs.append(orc.forward(fmt, X, xdt, cr, sr, N) if M > 0 else None)
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    for (fmt, xdt, M, N, K), e, Yr in zip(specs, entries, refs):
+        if M == 0:
+            continue
+        assert rel_err(e[5].cpu().numpy(), Yr) <= TOL[xdt]
