@@ -1,0 +1,326 @@
+#!/usr/bin/env python3
+"""Throughput of the block-quantized linear layers on one MI355X.
+
+A step is one pass of the linear stack of one DiT denoising step: 24 blocks
+at width d = 2048, each block's QKV (2048->6144), attention-out
+(2048->2048), FFN-up (2048->8192) and FFN-down (8192->2048) as one grouped
+qlinear_block_forward launch; q4 weights (block 32, fp16 scales,
+~N(0, 0.02)), bf16 activations of 2048 tokens (2 guidance branches x 1024
+latent frames, ~N(0, 1)).  Weights are quantized once on the GPU before
+timing (quantization is a load-time step) and everything is resident in HBM
+when the timed region starts.  The line also carries the skinny-M sweep
+(int8 / q4, M in {1, 8, 32, 128}), the int8 single-block workload, the
+dominant kernel's roofline position and the fp64 oracle timed on the host.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+ROT_BYTES = 512 << 20  # rotate weight copies past the 256 MB last-level cache
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_step_q4.txt")
+KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm.hip", "paper_2607_08526_amd/csrc/internal.h",
+                  "paper_2607_08526_amd/csrc/qlinear.hip"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-sweeps", action="store_true", help="time the step only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target duration of the oracle's timed sample")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain device copy of known size (counter calibration)")
+    return ap.parse_args()
+
+
+class Step:
+    """The 24-block q4 linear stack, quantized and resident on the GPU."""
+
+    def __init__(self, torch, ql, si, keep_host_block0=True):
+        self.torch, self.ql = torch, ql
+        dev = torch.device("cuda")
+        xa, xb = si.block_activations()
+        self.xa_host, self.xb_host = xa, xb
+        self.xa = torch.from_numpy(xa.view("int16")).to(dev)
+        self.xb = torch.from_numpy(xb.view("int16")).to(dev)
+        lin = si.block_linears()
+        M = xa.shape[0]
+        self.Y = [torch.empty((M, N), dtype=torch.float32, device=dev) for _, N, _ in lin]
+        self.blocks, self.groups = [], []
+        self.W0 = []
+        self.weight_bytes = 0
+        t0 = time.time()
+        import concurrent.futures as cf
+        jobs = [(blk, i) for blk in range(si.N_BLOCKS) for i in range(len(lin))]
+        pool = cf.ThreadPoolExecutor(max_workers=8)
+        gen = pool.map(lambda bi: si.step_q4_weight(*bi), jobs)  # drawn in parallel, in order
+        for blk in range(si.N_BLOCKS):
+            ents = []
+            for i, (name, N, K) in enumerate(lin):
+                W = next(gen)
+                if blk == 0 and keep_host_block0:
+                    self.W0.append(W)
+                codes, scales = ql.quantize(ql.FMT_Q4, torch.from_numpy(W).to(dev))
+                self.weight_bytes += codes.numel() + 2 * scales.numel()
+                X = self.xb if K == 4 * si.D_MODEL else self.xa
+                ents.append((ql.FMT_Q4, X, codes, scales, N, self.Y[i]))
+            self.blocks.append(ents)
+            self.groups.append(ql.make_group(ents))
+        pool.shutdown()
+        torch.cuda.synchronize()
+        log(f"step weights quantized on the GPU in {time.time() - t0:.1f}s "
+            f"({self.weight_bytes / 1e6:.1f} MB of codes + scales)")
+        self.flops_per_block = sum(2.0 * M * N * K for _, N, K in lin)
+        self.flops = self.flops_per_block * si.N_BLOCKS
+        self.M = M
+
+    def run(self, events=None):
+        for b, g in enumerate(self.groups):
+            if events is not None:
+                events[b][0].record()
+            self.ql.block_forward(None, group=g)
+            if events is not None:
+                events[b][1].record()
+
+
+def time_step(torch, step, steps, warmup):
+    for _ in range(warmup):
+        step.run()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in step.groups] for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(steps):
+        step.run(ev[s])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start.elapsed_time(end)
+    launch_ms = [a.elapsed_time(b) for row in ev for a, b in row]
+    return total_ms, launch_ms, wall
+
+
+def graph_time(torch, fn, reps=20, warm=5):
+    """Capture fn() (a sequence of launches) in a HIP graph, replay it and
+    return the median replay time in ms."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    for _ in range(warm):
+        g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    ts.sort()
+    return ts[len(ts) // 2], ts[0], ts[-1]
+
+
+def skinny_sweep(torch, ql, si):
+    out = []
+    dev = torch.device("cuda")
+    for v, fmt, N, K in si.skinny_variants():
+        W = si.skinny_weight(v, N, K)
+        codes, scales = ql.quantize(fmt, torch.from_numpy(W).to(dev))
+        wbytes = codes.numel() + 2 * scales.numel()
+        R = max(1, -(-ROT_BYTES // wbytes))
+        copies = [(codes.clone(), scales.clone()) for _ in range(R)]
+        for M in si.SKINNY_M:
+            X = torch.from_numpy(si.skinny_activations(M, K).view("int16")).to(dev)
+            Y = torch.empty((M, N), dtype=torch.float32, device=dev)
+
+            def fn():
+                for c, s in copies:
+                    ql.forward(fmt, X, c, s, N, Y)
+
+            med, lo, hi = graph_time(torch, fn)
+            t = med / R * 1e-3
+            algo_bytes = wbytes + M * K * 2 + M * N * 4
+            flops = 2.0 * M * N * K
+            out.append({
+                "fmt": "int8" if fmt == ql.FMT_INT8 else "q4", "N": N, "K": K, "M": M,
+                "us_per_call": round(t * 1e6, 3),
+                "weight_GBps": round(wbytes / t / 1e9, 1),
+                "hbm_GBps": round(algo_bytes / t / 1e9, 1),
+                "hbm_frac": round(algo_bytes / t / 1e9 / HBM_PEAK_GBPS, 4),
+                "TFLOPs": round(flops / t / 1e12, 3),
+                "rotation_copies": R,
+            })
+            log(f"skinny {out[-1]}")
+        del copies
+        torch.cuda.empty_cache()
+    return out
+
+
+def block_int8(torch, ql, si):
+    dev = torch.device("cuda")
+    xa, xb = si.block_activations()
+    xa_d = torch.from_numpy(xa.view("int16")).to(dev)
+    xb_d = torch.from_numpy(xb.view("int16")).to(dev)
+    ents, wbytes = [], 0
+    for i, (name, N, K) in enumerate(si.block_linears()):
+        codes, scales = ql.quantize(ql.FMT_INT8, torch.from_numpy(si.block_int8_weight(i)).to(dev))
+        wbytes += codes.numel() + 2 * scales.numel()
+        Y = torch.empty((xa.shape[0], N), dtype=torch.float32, device=dev)
+        ents.append((ql.FMT_INT8, xb_d if K == 4 * si.D_MODEL else xa_d, codes, scales, N, Y))
+    grp = ql.make_group(ents)
+    med, lo, hi = graph_time(torch, lambda: ql.block_forward(None, group=grp))
+    flops = sum(2.0 * xa.shape[0] * N * K for _, N, K in si.block_linears())
+    t = med * 1e-3
+    return {"us_per_block": round(med * 1e3, 2), "TFLOPs": round(flops / t / 1e12, 1),
+            "mfma_frac": round(flops / t / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+            "weight_GBps": round(wbytes / t / 1e9, 1)}
+
+
+def cpu_baseline(step, si, target_s):
+    """The fp64 oracle on a bounded sample of the same workload: rows of
+    block 0's four linears (all N), after the oracle's own quantization."""
+    import numpy as np
+    from oracle import oracle as O
+    orc = O.default()
+    t0 = time.perf_counter()
+    q = [orc.quantize(O.FMT_Q4, W) for W in step.W0]
+    tq = time.perf_counter() - t0
+    lin = si.block_linears()
+
+    def run(rows):
+        t = time.perf_counter()
+        for (name, N, K), (codes, scales) in zip(lin, q):
+            X = step.xb_host if K == 4 * si.D_MODEL else step.xa_host
+            orc.forward(O.FMT_Q4, X, O.DT_BF16, codes, scales, N, rows=np.arange(rows))
+        return time.perf_counter() - t
+
+    t1 = run(1)
+    rows = int(max(1, min(step.M, target_s / max(t1, 1e-3))))
+    t = run(rows)
+    flops = rows * sum(2.0 * N * K for _, N, K in lin)
+    return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
+            "kind": "oracle",
+            "sample": f"fp64 oracle forward of {rows} of 2048 token rows through block 0's four "
+                      f"q4 linears (all outputs), {t:.1f}s; the oracle's own quantization of "
+                      f"those 50.3M weights took {tq:.1f}s (not in the rate)"}
+
+
+def traffic_entry():
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+
+    import synth_inputs as si
+    from paper_2607_08526_amd import qlinear as ql
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    ql.load()
+
+    if args.calib_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    step = Step(torch, ql, si, keep_host_block0=not args.no_cpu_baseline)
+    total_ms, launch_ms, wall = time_step(torch, step, args.steps, args.warmup)
+    ms_per_step = total_ms / args.steps
+    tflops = step.flops / (ms_per_step * 1e-3) / 1e12
+    avg_launch_ms = sum(launch_ms) / len(launch_ms)
+    achieved = step.flops_per_block / (avg_launch_ms * 1e-3) / 1e12
+    log(f"step: {ms_per_step:.3f} ms, {tflops:.1f} TFLOP/s; grouped launch avg {avg_launch_ms:.4f} ms "
+        f"-> {achieved:.1f} TFLOP/s; host wall {wall:.2f}s")
+
+    res = {
+        "metric": "quantized-linear TFLOP/s, one DiT denoising step's linear stack "
+                  "(q4 block-32 weights, bf16 activations)",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "step_q4: 24 DiT blocks at d=2048 (QKV 2048->6144, out 2048->2048, "
+                        "FFN-up 2048->8192, FFN-down 8192->2048) = 1.208B q4 weights "
+                        "(block 32 along K, fp16 scales) ~N(0,0.02); bf16 activations, "
+                        "2048 tokens (2 CFG branches x 1024 latent frames) ~N(0,1); "
+                        "one grouped launch per block",
+            "global_batch": step.M, "seq_len": 1024, "parallelism": "none (1 GPU)",
+        },
+        "weight_GBps": round(step.weight_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "roofline": {
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
+            "traffic": traffic_entry(),
+            "kernel": "qgemm_kernel<q4, bf16 X, 128x128 tile> (one grouped launch per block)",
+            "flops_per_launch": step.flops_per_block,
+            "avg_launch_ms": round(avg_launch_ms, 5),
+        },
+    }
+    if not args.no_sweeps:
+        res["skinny"] = skinny_sweep(torch, ql, si)
+        res["block_int8"] = block_int8(torch, ql, si)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(step, si, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -49,6 +49,8 @@ def load(path=None):
         lib.oracle_forward_rows.argtypes = [ctypes.c_int, p, ctypes.c_int, i64, i64, p, p,
                                             i64, p, i64, p]
         lib.oracle_forward_rows.restype = ctypes.c_int
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
     return _LIBS[path]
 
@@ -73,6 +75,9 @@ class Oracle:
 
     def __init__(self, path=None):
         self.lib = load(path)
+
+    def num_threads(self):
+        return int(self.lib.oracle_num_threads())
 
     # number formats
     def f64_to_f16(self, v):

@@ -276,3 +276,16 @@ int oracle_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K,
 {
     return oracle_forward_rows(fmt, X, xdt, M, K, codes, scales, N, NULL, M, Y);
 }
+
+/* Number of threads the parallel loops above use (reported beside timings). */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

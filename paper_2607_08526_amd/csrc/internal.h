@@ -39,4 +39,9 @@ hipError_t launch_quantize(int fmt, const float *W, int64_t N, int64_t K, uint8_
 hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
                         hipStream_t stream);
 
+// Large-M kernel (bf16 activations): 128 x 256 tiles, direct-to-LDS pipeline.
+int big_tile_bm();
+int big_tile_bn();
+hipError_t launch_qgemm_big(int fmt, const GroupArgs &args, hipStream_t stream);
+
 }  // namespace qlk

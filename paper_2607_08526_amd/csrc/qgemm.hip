@@ -182,13 +182,20 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
     __shared__ __align__(16) float ts[2][2][XF32 ? 1 : BM];
 
     // ---- tile of this workgroup ------------------------------------------
-    const int L = logical_tile((int)blockIdx.x, (int)gridDim.x);
+    // workgroup p belongs to the layer whose tile range holds p, so every
+    // layer (long reductions first) is spread over all 8 XCDs; within the
+    // layer, each XCD takes a contiguous range of its tiles
+    const int p = (int)blockIdx.x;
     LinDesc d = args.d[0];
+    int end = args.total_tiles;
 #pragma unroll
-    for (int t = 1; t < QL_MAX_GROUP; ++t)
-        if (t < args.n && L >= args.d[t].tile_begin)
+    for (int t = 1; t < QL_MAX_GROUP; ++t) {
+        if (t < args.n && p >= args.d[t].tile_begin)
             d = args.d[t];
-    const int local = L - d.tile_begin;
+        if (t < args.n && p < args.d[t].tile_begin && end == args.total_tiles)
+            end = args.d[t].tile_begin;
+    }
+    const int local = logical_tile(p - d.tile_begin, end - d.tile_begin);
     const int tm = local % d.tiles_m;
     const int tn = local / d.tiles_m;
     const int M = d.M, N = d.N, K = d.K;
@@ -322,6 +329,9 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
                                                   : cvt_q4_off(*(uint32_t *)&cr[bi][j]);
                     sc[j] = (float)__builtin_bit_cast(_Float16, sr[bi][j]);
                 }
+                // all MFMAs of this block first (independent partials), then
+                // the per-block scale, so MFMA latency overlaps the FMAs
+                f32x4 P[MSUB][NSUB];
 #pragma unroll
                 for (int i = 0; i < MSUB; ++i) {
                     const int ro = (i * 16 + l16) * RS + lg * 8;
@@ -341,9 +351,14 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
                             p = mfma(a1, B[j], p);
                             p = mfma(a2, B[j], p);
                         }
-                        acc[i][j] += sc[j] * p;
+                        P[i][j] = p;
                     }
                 }
+#pragma unroll
+                for (int i = 0; i < MSUB; ++i)
+#pragma unroll
+                    for (int j = 0; j < NSUB; ++j)
+                        acc[i][j] += sc[j] * P[i][j];
             }
         }
         if (more) {

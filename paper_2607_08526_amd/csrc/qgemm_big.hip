@@ -1,0 +1,379 @@
+// Quantized linear forward, large-M tile (bf16 activations, M > 64).
+//
+//   Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k]
+//
+// Numerics as in qgemm.hip: one v_mfma_f32_16x16x32_bf16 per 32-wide K block
+// contracts the bf16 activations with the exact integer codes (every code is
+// an integer of at most 8 bits, exact in bf16); the fp16 block scale is then
+// applied to the fp32 partial with one FMA per output element per block.
+//
+// Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 256 of Y.  Each
+// wavefront owns a 128 x 64 strip (8 x 4 MFMA subtiles), so every converted
+// code fragment feeds 8 MFMAs and every activation fragment 4.
+//
+// Memory pipeline: activations and codes move from HBM to LDS with the
+// gfx950 direct-to-LDS loads (global_load_lds_dwordx4: no VGPRs, no VALU),
+// through a ring of 3 stages of 64 k (two scale blocks) each; scales (two per
+// weight row per stage) go to registers.  A stage is issued two steps before
+// it is consumed, and the main loop is unrolled by the ring depth so each
+// stage's registers and LDS slot are fixed.  One s_waitcnt vmcnt + s_barrier
+// per step: the wait lets the two younger stages stay in flight (a
+// __syncthreads() would drain them).
+//
+// LDS layouts are XOR-swizzled at 16-byte granularity so that the fragment
+// reads (16 rows x 16 B per 16 lanes) hit distinct banks.  Since a
+// direct-to-LDS load writes lane t's 16 bytes to slot base + t, the swizzle is
+// applied by choosing which global chunk each lane fetches.
+//
+// Tile order: groups of 4 row-tiles x all column tiles, walked row-tile
+// fastest, and the 8 XCDs each take a contiguous range of that order, so the
+// workgroups resident on one XCD share activation and weight tiles in its L2.
+#include "internal.h"
+
+namespace qlk {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int MSUB = 8, NSUB = 2, BM = 16 * MSUB, BN = 64 * NSUB, NST = 3, GROUP_M = 4;
+
+template <int FMT>
+struct Geo {
+    static constexpr int XBYTES = BM * 64 * 2;                 // activations per stage
+    static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : 32;  // code bytes per row per stage
+    static constexpr int CBYTES = BN * CROW;
+    static constexpr int SBYTES = BN * 4;                      // both scales of a step, per row
+    static constexpr int STAGE = XBYTES + CBYTES + SBYTES;
+    static constexpr int XLOADS = XBYTES / 16 / 256;
+    static constexpr int CLOADS = CBYTES / 16 / 256;
+    static constexpr int LOADS = XLOADS + CLOADS + 1;          // direct-to-LDS loads per stage
+    static_assert(XBYTES % (16 * 256) == 0 && CBYTES % (16 * 256) == 0,
+                  "every thread issues the same number of 16-byte loads per stage");
+    static_assert(BN % 64 == 0 && BN <= 256, "one scale dword per weight row per stage");
+};
+
+__device__ inline constexpr int vmcnt_imm(int v)
+{
+    // gfx9 s_waitcnt encoding: vmcnt[3:0] + vmcnt[5:4] at bits 15:14;
+    // expcnt (bits 6:4) and lgkmcnt (bits 11:8) left at "no wait"
+    return (v & 15) | (((v >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
+}
+
+// Direct-to-LDS loads: lane t's data lands at LDS address lds + t * size.
+// Issued from inline asm so that the compiler's wait insertion, which cannot
+// tell the ring stages apart and would drain every load in flight before each
+// LDS read, stays out of the way; the kernel waits for each stage explicitly
+// (s_waitcnt vmcnt + s_barrier).  Nothing else in these kernels uses M0.
+__device__ inline void dma16(const void *src, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "memory");
+}
+
+__device__ inline void dma4(const void *src, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :
+                 : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "memory");
+}
+
+__device__ inline uint32_t lds_addr(const void *p)
+{
+    // a generic pointer into LDS carries the LDS offset in its low 32 bits
+    return (uint32_t)(uintptr_t)p;
+}
+
+__device__ inline f32x4 mfma(u32x4 a, u32x4 b)
+{
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), z, 0, 0, 0);
+}
+
+__device__ inline uint32_t pack_bf16(float lo, float hi)
+{
+    // lo, hi are small integers: exact in bf16, which is the fp32 high half
+    return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+}
+
+// Signed bit field [lo, lo + w) of x as a float (exact: |value| < 2^7).
+template <int LO, int W>
+__device__ inline float sfield(uint32_t x)
+{
+    return (float)((int32_t)(x << (32 - LO - W)) >> (32 - W));
+}
+
+// 8 int8 codes (k0..k7) -> 8 bf16, natural order.
+__device__ inline u32x4 cvt_int8(uint32_t a, uint32_t b)
+{
+    u32x4 r;
+    r[0] = pack_bf16(sfield<0, 8>(a), sfield<8, 8>(a));
+    r[1] = pack_bf16(sfield<16, 8>(a), sfield<24, 8>(a));
+    r[2] = pack_bf16(sfield<0, 8>(b), sfield<8, 8>(b));
+    r[3] = pack_bf16(sfield<16, 8>(b), sfield<24, 8>(b));
+    return r;
+}
+
+// 8 q4 codes (one dword, k0 in bits 0-3) -> 8 bf16, natural order.
+__device__ inline u32x4 cvt_q4(uint32_t c)
+{
+    u32x4 r;
+    r[0] = pack_bf16(sfield<0, 4>(c), sfield<4, 4>(c));
+    r[1] = pack_bf16(sfield<8, 4>(c), sfield<12, 4>(c));
+    r[2] = pack_bf16(sfield<16, 4>(c), sfield<20, 4>(c));
+    r[3] = pack_bf16(sfield<24, 4>(c), sfield<28, 4>(c));
+    return r;
+}
+
+__device__ inline int logical_tile(int p, int G)
+{
+    const int q = G >> 3, r = G & 7;
+    const int xcd = p & 7, idx = p >> 3;
+    return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+template <int FMT>
+struct Ctx {
+    const uint16_t *X;
+    const uint8_t *codes;
+    const uint16_t *scales;
+    int M, N, K, nb, nsteps, m0, n0;
+    int tid, wave, lane, l16, lg;
+};
+
+// Issue the direct-to-LDS loads of step s into one ring stage.
+template <int FMT>
+__device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
+{
+    using G = Geo<FMT>;
+    const uint32_t base = lds_addr(stage);
+    // activations: slot = bi*512 + row*4 + (g ^ swz(row))
+#pragma unroll
+    for (int r = 0; r < G::XLOADS; ++r) {
+        const int slot = r * 256 + c.tid;
+        const int bi = slot >> 9, rem = slot & 511, row = rem >> 2;
+        const int g = (rem & 3) ^ ((row >> 2) & 3);
+        const int m = min(c.m0 + row, c.M - 1);
+        const int kb = min(2 * s + bi, c.nb - 1);
+        dma16(c.X + (int64_t)m * c.K + kb * 32 + g * 8, base + (r * 256 + c.wave * 64) * 16);
+    }
+    // codes
+#pragma unroll
+    for (int r = 0; r < G::CLOADS; ++r) {
+        const int slot = r * 256 + c.tid;
+        const uint8_t *src;
+        if (FMT == QL_FMT_INT8) {
+            const int row = slot >> 2;
+            const int ch = (slot & 3) ^ ((row >> 2) & 3);    // logical 16-B chunk of 64 k
+            const int n = min(c.n0 + row, c.N - 1);
+            src = c.codes + (int64_t)n * c.K + s * 64 + ch * 16;
+        } else {
+            const int row = slot >> 1;
+            const int ch = (slot & 1) ^ ((row >> 3) & 1);
+            const int n = min(c.n0 + row, c.N - 1);
+            src = c.codes + (int64_t)n * (c.K / 2) + s * 32 + ch * 16;
+        }
+        dma16(src, base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
+    }
+    // scales: one dword (blocks 2s, 2s+1) per weight row; slot = row.  When
+    // BN < 256 the surplus wavefronts repeat the first rows (identical data
+    // to the same slots), so every wavefront issues the same number of loads
+    // and the per-wavefront vmcnt accounting holds.
+    {
+        const int row = c.tid % BN;
+        const int n = min(c.n0 + row, c.N - 1);
+        dma4(c.scales + (int64_t)n * c.nb + 2 * s,
+             base + G::XBYTES + G::CBYTES + (c.wave % (BN / 64)) * 256);
+    }
+}
+
+template <int FMT>
+__device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
+                                     f32x4 (&acc)[MSUB][NSUB])
+{
+    using G = Geo<FMT>;
+    uint32_t sc[NSUB];
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j)
+        sc[j] = *reinterpret_cast<const uint32_t *>(stage + G::XBYTES + G::CBYTES +
+                                                    (c.wave * (16 * NSUB) + j * 16 + c.l16) * 4);
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+        u32x4 B[NSUB];
+        float sf[NSUB];
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j) {
+            const int row = c.wave * (16 * NSUB) + j * 16 + c.l16;
+            if (FMT == QL_FMT_INT8) {
+                const int ch = (bi * 2 + (c.lg >> 1)) ^ ((row >> 2) & 3);
+                const uint2 v = *reinterpret_cast<const uint2 *>(
+                    stage + G::XBYTES + row * 64 + ch * 16 + (c.lg & 1) * 8);
+                B[j] = cvt_int8(v.x, v.y);
+            } else {
+                const int ch = bi ^ ((row >> 3) & 1);
+                const uint32_t v = *reinterpret_cast<const uint32_t *>(
+                    stage + G::XBYTES + row * 32 + ch * 16 + c.lg * 4);
+                B[j] = cvt_q4(v);
+            }
+            sf[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(sc[j] >> (16 * bi)));
+        }
+        // software pipeline over the row subtiles: the activation fragment of
+        // subtile i+1 is read while subtile i's MFMAs run, and subtile i-1's
+        // partials are scaled into the accumulators behind them; the
+        // scheduling fences keep the compiler from hoisting every LDS read of
+        // the step (which would exhaust the register file)
+        auto read_a = [&](int i) {
+            const int row = i * 16 + c.l16;
+            const int slot = bi * 512 + row * 4 + (c.lg ^ ((row >> 2) & 3));
+            return *reinterpret_cast<const u32x4 *>(stage + slot * 16);
+        };
+        u32x4 a = read_a(0);
+        f32x4 P[NSUB], Pp[NSUB];
+#pragma unroll
+        for (int i = 0; i < MSUB; ++i) {
+            const u32x4 an = i + 1 < MSUB ? read_a(i + 1) : a;
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j)
+                P[j] = mfma(a, B[j]);
+            if (i > 0) {
+#pragma unroll
+                for (int j = 0; j < NSUB; ++j)
+                    acc[i - 1][j] += sf[j] * Pp[j];
+            }
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j)
+                Pp[j] = P[j];
+            a = an;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j)
+            acc[MSUB - 1][j] += sf[j] * Pp[j];
+    }
+}
+
+template <int FMT>
+__global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
+{
+    using G = Geo<FMT>;
+    // one array per ring stage: the compiler's alias check between the
+    // direct-to-LDS loads in flight and the fragment reads is per object, so
+    // distinct arrays keep it from draining the younger stages before reads
+    __shared__ __align__(16) uint8_t lds0[G::STAGE];
+    __shared__ __align__(16) uint8_t lds1[G::STAGE];
+    __shared__ __align__(16) uint8_t lds2[G::STAGE];
+    uint8_t *const lds[NST] = {lds0, lds1, lds2};
+
+    // workgroup p belongs to the layer whose tile range holds p, so every
+    // layer (long reductions first) is spread over all 8 XCDs; within the
+    // layer, each XCD takes a contiguous range of its tiles
+    const int p = (int)blockIdx.x;
+    LinDesc d = args.d[0];
+    int end = args.total_tiles;
+#pragma unroll
+    for (int t = 1; t < QL_MAX_GROUP; ++t) {
+        if (t < args.n && p >= args.d[t].tile_begin)
+            d = args.d[t];
+        if (t < args.n && p < args.d[t].tile_begin && end == args.total_tiles)
+            end = args.d[t].tile_begin;
+    }
+    const int local = logical_tile(p - d.tile_begin, end - d.tile_begin);
+    const int per_group = GROUP_M * d.tiles_n;
+    const int gid = local / per_group;
+    const int first_m = gid * GROUP_M;
+    const int gsz = min(d.tiles_m - first_m, GROUP_M);
+    const int within = local - gid * per_group;
+    const int tm = first_m + within % gsz;
+    const int tn = within / gsz;
+
+    Ctx<FMT> c;
+    c.X = reinterpret_cast<const uint16_t *>(d.X);
+    c.codes = d.codes;
+    c.scales = d.scales;
+    c.M = d.M;
+    c.N = d.N;
+    c.K = d.K;
+    c.nb = d.K >> 5;
+    c.nsteps = c.nb >> 1;  // the host routes odd block counts elsewhere
+    c.m0 = tm * BM;
+    c.n0 = tn * BN;
+    c.tid = threadIdx.x;
+    c.wave = c.tid >> 6;
+    c.lane = c.tid & 63;
+    c.l16 = c.lane & 15;
+    c.lg = c.lane >> 4;
+
+    f32x4 acc[MSUB][NSUB];
+#pragma unroll
+    for (int i = 0; i < MSUB; ++i)
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int ns = c.nsteps;
+    issue_stage<FMT>(c, lds[0], 0);
+    if (ns > 1)
+        issue_stage<FMT>(c, lds[1], 1);
+
+    // one step: wait for stage s (vector-memory loads complete in issue order,
+    // so allowing the LOADS youngest ones, which are stage s+1's, to remain
+    // outstanding means all of stage s has landed), barrier, refill the slot
+    // that step s-1 read with step s+2, compute stage s
+#define QL_STEP(Q)                                                                  \
+    {                                                                               \
+        const int s = s0 + (Q);                                                     \
+        if (s >= ns)                                                                \
+            break;                                                                  \
+        if (s + 1 < ns)                                                             \
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS));                        \
+        else                                                                        \
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));                               \
+        __builtin_amdgcn_s_barrier();                                               \
+        if (s + 2 < ns)                                                             \
+            issue_stage<FMT>(c, lds[((Q) + 2) % NST], s + 2);                       \
+        compute_stage<FMT>(c, lds[(Q)], acc);                                       \
+    }
+
+    for (int s0 = 0; s0 < ns; s0 += NST) {
+        QL_STEP(0)
+        QL_STEP(1)
+        QL_STEP(2)
+    }
+#undef QL_STEP
+
+    const int n_wave = c.n0 + c.wave * (16 * NSUB);
+#pragma unroll
+    for (int i = 0; i < MSUB; ++i)
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j) {
+            const int n = n_wave + j * 16 + c.l16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = c.m0 + i * 16 + c.lg * 4 + r;
+                if (m < c.M && n < c.N)
+                    d.Y[(int64_t)m * c.N + n] = acc[i][j][r];
+            }
+        }
+}
+
+}  // namespace
+
+int big_tile_bm() { return BM; }
+int big_tile_bn() { return BN; }
+
+hipError_t launch_qgemm_big(int fmt, const GroupArgs &args, hipStream_t stream)
+{
+    dim3 grid((unsigned)args.total_tiles), block(256);
+    if (fmt == QL_FMT_INT8)
+        hipLaunchKernelGGL(qgemm_big_kernel<QL_FMT_INT8>, grid, block, 0, stream, args);
+    else
+        hipLaunchKernelGGL(qgemm_big_kernel<QL_FMT_Q4>, grid, block, 0, stream, args);
+    return hipGetLastError();
+}
+
+}  // namespace qlk

@@ -53,7 +53,12 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->M);
     const TileCfg t = choose_tile(maxM, xf32);
-    const int bm = tile_bm(t), bn = tile_bn(t);
+    // the large-M kernel moves two scale blocks per row as one aligned dword
+    bool big = !xf32 && t == TILE_M128;
+    for (int i = 0; i < n; ++i)
+        big = big && ls[i]->K % 64 == 0 && aligned(ls[i]->scales, 4);
+    const int bm = big ? big_tile_bm() : tile_bm(t);
+    const int bn = big ? big_tile_bn() : tile_bn(t);
 
     // longest reduction first, so the long tiles start early
     const ql_linear *ord[QL_MAX_GROUP];
@@ -81,7 +86,9 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
-    return launch_qgemm(ord[0]->fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+    const hipError_t e = big ? launch_qgemm_big(ord[0]->fmt, a, stream)
+                             : launch_qgemm(ord[0]->fmt, xf32, t, a, stream);
+    return e == hipSuccess ? QL_OK : QL_ERR_HIP;
 }
 
 }  // namespace
