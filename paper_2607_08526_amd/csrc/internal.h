@@ -44,4 +44,9 @@ int big_tile_bm();
 int big_tile_bn();
 hipError_t launch_qgemm_big(int fmt, const GroupArgs &args, hipStream_t stream);
 
+// Few-row kernel (bf16 activations, M <= skinny_max_m()): one layer per
+// launch, workgroups of 16 weight rows with K split over their wavefronts.
+int skinny_max_m();
+hipError_t launch_qgemm_skinny(int fmt, const LinDesc &d, hipStream_t stream);
+
 }  // namespace qlk

@@ -7,9 +7,9 @@
 // an integer of at most 8 bits, exact in bf16); the fp16 block scale is then
 // applied to the fp32 partial with one FMA per output element per block.
 //
-// Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 256 of Y.  Each
-// wavefront owns a 128 x 64 strip (8 x 4 MFMA subtiles), so every converted
-// code fragment feeds 8 MFMAs and every activation fragment 4.
+// Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 128 of Y.  Each
+// wavefront owns a 128 x 32 strip (8 x 2 MFMA subtiles), so every converted
+// code fragment feeds 8 MFMAs and every activation fragment 2.
 //
 // Memory pipeline: activations and codes move from HBM to LDS with the
 // gfx950 direct-to-LDS loads (global_load_lds_dwordx4: no VGPRs, no VALU),

@@ -52,6 +52,25 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     int64_t maxM = 0;
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->M);
+    if (!xf32 && maxM <= skinny_max_m()) {
+        // few rows: streaming-bound, one launch per layer
+        for (int i = 0; i < n; ++i) {
+            LinDesc d{};
+            d.X = ls[i]->X;
+            d.codes = (const uint8_t *)ls[i]->codes;
+            d.scales = ls[i]->scales;
+            d.Y = ls[i]->Y;
+            d.M = (int)ls[i]->M;
+            d.N = (int)ls[i]->N;
+            d.K = (int)ls[i]->K;
+            if (launch_qgemm_skinny(ls[i]->fmt, d, stream) != hipSuccess)
+                return QL_ERR_HIP;
+        }
+        return QL_OK;
+    }
+    maxM = 0;
+    for (int i = 0; i < n; ++i)
+        maxM = std::max(maxM, ls[i]->M);
     const TileCfg t = choose_tile(maxM, xf32);
     // the large-M kernel moves two scale blocks per row as one aligned dword
     bool big = !xf32 && t == TILE_M128;
