@@ -1,33 +1,44 @@
-// Quantized linear forward, large-M tile (bf16 activations, M > 64).
+// Quantized linear forward, large-M tile (bf16 activations, M > 64,
+// K a multiple of 64, 4-byte aligned scales).
 //
 //   Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k]
 //
-// Numerics as in qgemm.hip: one v_mfma_f32_16x16x32_bf16 per 32-wide K block
-// contracts the bf16 activations with the exact integer codes (every code is
-// an integer of at most 8 bits, exact in bf16); the fp16 block scale is then
-// applied to the fp32 partial with one FMA per output element per block.
+// Numerics: one v_mfma_f32_16x16x32_bf16 per 32-wide K block contracts the
+// bf16 activations with integer codes that are exact in bf16; the fp16 block
+// scale is then applied to the fp32 partial with one FMA per output element
+// per block.  int8 codes are converted exactly (sign-extending
+// v_cvt_f32_i32 on each byte, fp32 high halves packed by v_perm).  q4 codes
+// take the cheaper offset form 0x4300 | (nibble ^ 8) = bf16(136 + c), two
+// codes per AND-OR; the offset's contribution -136 * sum_{k in b} X[m][k]
+// comes from one extra MFMA of the activation fragment against a constant
+// -136 matrix and enters each main MFMA as its C operand.  The kernel is
+// bound by VALU issue (the per-block scale FMAs cost as much issue time as
+// the MFMAs), so trading conversion work for matrix-core work pays.
 //
 // Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 128 of Y.  Each
 // wavefront owns a 128 x 32 strip (8 x 2 MFMA subtiles), so every converted
 // code fragment feeds 8 MFMAs and every activation fragment 2.
 //
-// Memory pipeline: activations and codes move from HBM to LDS with the
-// gfx950 direct-to-LDS loads (global_load_lds_dwordx4: no VGPRs, no VALU),
-// through a ring of 3 stages of 64 k (two scale blocks) each; scales (two per
-// weight row per stage) go to registers.  A stage is issued two steps before
-// it is consumed, and the main loop is unrolled by the ring depth so each
-// stage's registers and LDS slot are fixed.  One s_waitcnt vmcnt + s_barrier
-// per step: the wait lets the two younger stages stay in flight (a
-// __syncthreads() would drain them).
+// Memory pipeline: activations, codes and scales move from HBM to LDS with
+// the gfx950 direct-to-LDS loads (no VGPRs, no VALU), through a ring of 3
+// stages of 64 k (two scale blocks) each; a stage is issued two steps before
+// it is consumed and the main loop is unrolled by the ring depth so each
+// stage's LDS slot is fixed.  Each lane's global offset within the tile is
+// computed once; per step only the wave-uniform base address (an SGPR pair)
+// advances.  The loads are issued from inline asm so that the compiler's wait
+// insertion, which cannot tell the ring stages apart and would drain every
+// load in flight before each LDS read, stays out of the way: the kernel waits
+// for each stage explicitly (s_waitcnt vmcnt + s_barrier; a __syncthreads()
+// would also drain the ring).  Nothing else in these kernels uses M0.
 //
 // LDS layouts are XOR-swizzled at 16-byte granularity so that the fragment
-// reads (16 rows x 16 B per 16 lanes) hit distinct banks.  Since a
-// direct-to-LDS load writes lane t's 16 bytes to slot base + t, the swizzle is
-// applied by choosing which global chunk each lane fetches.
+// reads (16 rows x 16 B per 16 lanes) hit distinct banks.  A direct-to-LDS
+// load writes lane t's data to slot base + t, so the swizzle is applied by
+// choosing which global chunk each lane fetches.
 //
-// Tile order: groups of 4 row-tiles x all column tiles, walked row-tile
-// fastest, and the 8 XCDs each take a contiguous range of that order, so the
-// workgroups resident on one XCD share activation and weight tiles in its L2.
+// Tile order: within a layer, groups of 4 row tiles walked row-tile fastest;
+// each of the 8 XCDs takes a contiguous range of one layer's tiles (L2
+// reuse), and every layer of a grouped launch is spread over all XCDs.
 #include "internal.h"
 
 namespace qlk {
@@ -61,24 +72,21 @@ __device__ inline constexpr int vmcnt_imm(int v)
     return (v & 15) | (((v >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
 }
 
-// Direct-to-LDS loads: lane t's data lands at LDS address lds + t * size.
-// Issued from inline asm so that the compiler's wait insertion, which cannot
-// tell the ring stages apart and would drain every load in flight before each
-// LDS read, stays out of the way; the kernel waits for each stage explicitly
-// (s_waitcnt vmcnt + s_barrier).  Nothing else in these kernels uses M0.
-__device__ inline void dma16(const void *src, uint32_t lds)
+// Direct-to-LDS loads from (wave-uniform base + per-lane 32-bit offset):
+// lane t's data lands at LDS address lds + t * size.
+__device__ inline void dma16(const void *base, uint32_t off, uint32_t lds)
 {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
-                 : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory");
 }
 
-__device__ inline void dma4(const void *src, uint32_t lds)
+__device__ inline void dma4(const void *base, uint32_t off, uint32_t lds)
 {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
                  :
-                 : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory");
 }
 
@@ -88,45 +96,47 @@ __device__ inline uint32_t lds_addr(const void *p)
     return (uint32_t)(uintptr_t)p;
 }
 
-__device__ inline f32x4 mfma(u32x4 a, u32x4 b)
+__device__ inline f32x4 mfma(u32x4 a, u32x4 b, f32x4 c)
 {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), z, 0, 0, 0);
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-__device__ inline uint32_t pack_bf16(float lo, float hi)
+// fp32 high halves of (lo, hi) as a bf16 pair (exact for small integers)
+__device__ inline uint32_t pack_hi(float lo, float hi)
 {
-    // lo, hi are small integers: exact in bf16, which is the fp32 high half
-    return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
 }
 
-// Signed bit field [lo, lo + w) of x as a float (exact: |value| < 2^7).
-template <int LO, int W>
-__device__ inline float sfield(uint32_t x)
+// Signed byte J of x as a float.
+template <int J>
+__device__ inline float sbyte(uint32_t x)
 {
-    return (float)((int32_t)(x << (32 - LO - W)) >> (32 - W));
+    return (float)((int32_t)(x << (24 - 8 * J)) >> 24);
 }
 
-// 8 int8 codes (k0..k7) -> 8 bf16, natural order.
+// 8 int8 codes (k0..k7) -> 8 bf16, exact, natural order.
 __device__ inline u32x4 cvt_int8(uint32_t a, uint32_t b)
 {
     u32x4 r;
-    r[0] = pack_bf16(sfield<0, 8>(a), sfield<8, 8>(a));
-    r[1] = pack_bf16(sfield<16, 8>(a), sfield<24, 8>(a));
-    r[2] = pack_bf16(sfield<0, 8>(b), sfield<8, 8>(b));
-    r[3] = pack_bf16(sfield<16, 8>(b), sfield<24, 8>(b));
+    r[0] = pack_hi(sbyte<0>(a), sbyte<1>(a));
+    r[1] = pack_hi(sbyte<2>(a), sbyte<3>(a));
+    r[2] = pack_hi(sbyte<0>(b), sbyte<1>(b));
+    r[3] = pack_hi(sbyte<2>(b), sbyte<3>(b));
     return r;
 }
 
-// 8 q4 codes (one dword, k0 in bits 0-3) -> 8 bf16, natural order.
-__device__ inline u32x4 cvt_q4(uint32_t c)
+// 8 q4 codes (k0 in bits 0-3) -> bf16 of 136 + c, natural order: byte j of
+// x holds codes 2j and 2j+1; v_perm puts byte j of x and of x >> 4 in the two
+// 16-bit halves, the AND keeps one nibble in each, the OR adds bf16 128.
+__device__ inline u32x4 cvt_q4_off(uint32_t c)
 {
+    const uint32_t x = c ^ 0x88888888u, y = x >> 4;
     u32x4 r;
-    r[0] = pack_bf16(sfield<0, 4>(c), sfield<4, 4>(c));
-    r[1] = pack_bf16(sfield<8, 4>(c), sfield<12, 4>(c));
-    r[2] = pack_bf16(sfield<16, 4>(c), sfield<20, 4>(c));
-    r[3] = pack_bf16(sfield<24, 4>(c), sfield<28, 4>(c));
+    r[0] = (__builtin_amdgcn_perm(y, x, 0x0C040C00u) & 0x000F000Fu) | 0x43004300u;
+    r[1] = (__builtin_amdgcn_perm(y, x, 0x0C050C01u) & 0x000F000Fu) | 0x43004300u;
+    r[2] = (__builtin_amdgcn_perm(y, x, 0x0C060C02u) & 0x000F000Fu) | 0x43004300u;
+    r[3] = (__builtin_amdgcn_perm(y, x, 0x0C070C03u) & 0x000F000Fu) | 0x43004300u;
     return r;
 }
 
@@ -139,11 +149,11 @@ __device__ inline int logical_tile(int p, int G)
 
 template <int FMT>
 struct Ctx {
-    const uint16_t *X;
-    const uint8_t *codes;
-    const uint16_t *scales;
-    int M, N, K, nb, nsteps, m0, n0;
-    int tid, wave, lane, l16, lg;
+    // wave-uniform bases of this tile (advanced per step by the caller)
+    const uint8_t *xbase, *cbase, *sbase;
+    // per-lane byte offsets from those bases, fixed for the whole K loop
+    uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff;
+    int wave, l16, lg;
 };
 
 // Issue the direct-to-LDS loads of step s into one ring stage.
@@ -152,44 +162,16 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
 {
     using G = Geo<FMT>;
     const uint32_t base = lds_addr(stage);
-    // activations: slot = bi*512 + row*4 + (g ^ swz(row))
+    const uint8_t *xb = c.xbase + s * 128;              // 64 bf16 per row per step
+    const uint8_t *cb = c.cbase + s * G::CROW;
+    const uint8_t *sb = c.sbase + s * 4;
 #pragma unroll
-    for (int r = 0; r < G::XLOADS; ++r) {
-        const int slot = r * 256 + c.tid;
-        const int bi = slot >> 9, rem = slot & 511, row = rem >> 2;
-        const int g = (rem & 3) ^ ((row >> 2) & 3);
-        const int m = min(c.m0 + row, c.M - 1);
-        const int kb = min(2 * s + bi, c.nb - 1);
-        dma16(c.X + (int64_t)m * c.K + kb * 32 + g * 8, base + (r * 256 + c.wave * 64) * 16);
-    }
-    // codes
+    for (int r = 0; r < G::XLOADS; ++r)
+        dma16(xb, c.xoff[r], base + (r * 256 + c.wave * 64) * 16);
 #pragma unroll
-    for (int r = 0; r < G::CLOADS; ++r) {
-        const int slot = r * 256 + c.tid;
-        const uint8_t *src;
-        if (FMT == QL_FMT_INT8) {
-            const int row = slot >> 2;
-            const int ch = (slot & 3) ^ ((row >> 2) & 3);    // logical 16-B chunk of 64 k
-            const int n = min(c.n0 + row, c.N - 1);
-            src = c.codes + (int64_t)n * c.K + s * 64 + ch * 16;
-        } else {
-            const int row = slot >> 1;
-            const int ch = (slot & 1) ^ ((row >> 3) & 1);
-            const int n = min(c.n0 + row, c.N - 1);
-            src = c.codes + (int64_t)n * (c.K / 2) + s * 32 + ch * 16;
-        }
-        dma16(src, base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
-    }
-    // scales: one dword (blocks 2s, 2s+1) per weight row; slot = row.  When
-    // BN < 256 the surplus wavefronts repeat the first rows (identical data
-    // to the same slots), so every wavefront issues the same number of loads
-    // and the per-wavefront vmcnt accounting holds.
-    {
-        const int row = c.tid % BN;
-        const int n = min(c.n0 + row, c.N - 1);
-        dma4(c.scales + (int64_t)n * c.nb + 2 * s,
-             base + G::XBYTES + G::CBYTES + (c.wave % (BN / 64)) * 256);
-    }
+    for (int r = 0; r < G::CLOADS; ++r)
+        dma16(cb, c.coff[r], base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
+    dma4(sb, c.soff, base + G::XBYTES + G::CBYTES + (c.wave % (BN / 64)) * 256);
 }
 
 template <int FMT>
@@ -197,6 +179,9 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
                                      f32x4 (&acc)[MSUB][NSUB])
 {
     using G = Geo<FMT>;
+    constexpr bool OFFSET = FMT == QL_FMT_Q4;
+    const u32x4 bneg = {0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u};  // bf16 -136
+
     uint32_t sc[NSUB];
 #pragma unroll
     for (int j = 0; j < NSUB; ++j)
@@ -218,7 +203,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
                 const int ch = bi ^ ((row >> 3) & 1);
                 const uint32_t v = *reinterpret_cast<const uint32_t *>(
                     stage + G::XBYTES + row * 32 + ch * 16 + c.lg * 4);
-                B[j] = cvt_q4(v);
+                B[j] = cvt_q4_off(v);
             }
             sf[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(sc[j] >> (16 * bi)));
         }
@@ -237,9 +222,12 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
 #pragma unroll
         for (int i = 0; i < MSUB; ++i) {
             const u32x4 an = i + 1 < MSUB ? read_a(i + 1) : a;
+            f32x4 T = {0.f, 0.f, 0.f, 0.f};
+            if (OFFSET)
+                T = mfma(a, bneg, T);
 #pragma unroll
             for (int j = 0; j < NSUB; ++j)
-                P[j] = mfma(a, B[j]);
+                P[j] = mfma(a, B[j], T);
             if (i > 0) {
 #pragma unroll
                 for (int j = 0; j < NSUB; ++j)
@@ -258,12 +246,10 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
 }
 
 template <int FMT>
-__global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
+__global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
-    // one array per ring stage: the compiler's alias check between the
-    // direct-to-LDS loads in flight and the fragment reads is per object, so
-    // distinct arrays keep it from draining the younger stages before reads
+    // one array per ring stage (distinct LDS objects)
     __shared__ __align__(16) uint8_t lds0[G::STAGE];
     __shared__ __align__(16) uint8_t lds1[G::STAGE];
     __shared__ __align__(16) uint8_t lds2[G::STAGE];
@@ -291,22 +277,51 @@ __global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
     const int tm = first_m + within % gsz;
     const int tn = within / gsz;
 
+    const int M = d.M, N = d.N, K = d.K, nb = K >> 5;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int tid = threadIdx.x;
+    const int crow_bytes = FMT == QL_FMT_INT8 ? K : K / 2;
+
     Ctx<FMT> c;
-    c.X = reinterpret_cast<const uint16_t *>(d.X);
-    c.codes = d.codes;
-    c.scales = d.scales;
-    c.M = d.M;
-    c.N = d.N;
-    c.K = d.K;
-    c.nb = d.K >> 5;
-    c.nsteps = c.nb >> 1;  // the host routes odd block counts elsewhere
-    c.m0 = tm * BM;
-    c.n0 = tn * BN;
-    c.tid = threadIdx.x;
-    c.wave = c.tid >> 6;
-    c.lane = c.tid & 63;
-    c.l16 = c.lane & 15;
-    c.lg = c.lane >> 4;
+    c.wave = tid >> 6;
+    c.l16 = tid & 15;
+    c.lg = (tid & 63) >> 4;
+    c.xbase = reinterpret_cast<const uint8_t *>(d.X) + (int64_t)m0 * K * 2;
+    c.cbase = d.codes + (int64_t)n0 * crow_bytes;
+    c.sbase = reinterpret_cast<const uint8_t *>(d.scales) + (int64_t)n0 * nb * 2;
+    // activations: stage slot = bi*512 + row*4 + (g ^ swz(row)); rows past M
+    // repeat the last row (their outputs are never stored)
+#pragma unroll
+    for (int r = 0; r < G::XLOADS; ++r) {
+        const int slot = r * 256 + tid;
+        const int bi = slot >> 9, rem = slot & 511, row = rem >> 2;
+        const int g = (rem & 3) ^ ((row >> 2) & 3);
+        const int m = min(m0 + row, M - 1) - m0;
+        c.xoff[r] = (uint32_t)(m * K * 2 + bi * 64 + g * 16);
+    }
+    // codes: stage slot = row*(CROW/16) + (chunk ^ swz(row)); rows past N
+    // repeat the last row
+#pragma unroll
+    for (int r = 0; r < G::CLOADS; ++r) {
+        const int slot = r * 256 + tid;
+        int row, ch;
+        if (FMT == QL_FMT_INT8) {
+            row = slot >> 2;
+            ch = (slot & 3) ^ ((row >> 2) & 3);
+        } else {
+            row = slot >> 1;
+            ch = (slot & 1) ^ ((row >> 3) & 1);
+        }
+        const int n = min(n0 + row, N - 1) - n0;
+        c.coff[r] = (uint32_t)(n * crow_bytes + ch * 16);
+    }
+    {
+        // scales: one dword (blocks 2s, 2s+1) per weight row; surplus
+        // wavefronts repeat the first rows (identical data, same slots), so
+        // every wavefront issues the same number of loads per stage
+        const int n = min(n0 + tid % BN, N - 1) - n0;
+        c.soff = (uint32_t)(n * nb * 2);
+    }
 
     f32x4 acc[MSUB][NSUB];
 #pragma unroll
@@ -315,15 +330,15 @@ __global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
         for (int j = 0; j < NSUB; ++j)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int ns = c.nsteps;
+    const int ns = nb >> 1;  // the host routes odd block counts elsewhere
     issue_stage<FMT>(c, lds[0], 0);
     if (ns > 1)
         issue_stage<FMT>(c, lds[1], 1);
 
-    // one step: wait for stage s (vector-memory loads complete in issue order,
-    // so allowing the LOADS youngest ones, which are stage s+1's, to remain
-    // outstanding means all of stage s has landed), barrier, refill the slot
-    // that step s-1 read with step s+2, compute stage s
+    // one step: wait for stage s (loads complete in issue order, so allowing
+    // the LOADS youngest ones, which are stage s+1's, to remain outstanding
+    // means all of stage s has landed), barrier, refill the slot that step
+    // s-1 read with step s+2, compute stage s
 #define QL_STEP(Q)                                                                  \
     {                                                                               \
         const int s = s0 + (Q);                                                     \
@@ -346,7 +361,7 @@ __global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
     }
 #undef QL_STEP
 
-    const int n_wave = c.n0 + c.wave * (16 * NSUB);
+    const int n_wave = n0 + c.wave * (16 * NSUB);
 #pragma unroll
     for (int i = 0; i < MSUB; ++i)
 #pragma unroll
@@ -354,9 +369,9 @@ __global__ __launch_bounds__(256, 1) void qgemm_big_kernel(const GroupArgs args)
             const int n = n_wave + j * 16 + c.l16;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int m = c.m0 + i * 16 + c.lg * 4 + r;
-                if (m < c.M && n < c.N)
-                    d.Y[(int64_t)m * c.N + n] = acc[i][j][r];
+                const int m = m0 + i * 16 + c.lg * 4 + r;
+                if (m < M && n < N)
+                    d.Y[(int64_t)m * N + n] = acc[i][j][r];
             }
         }
 }
