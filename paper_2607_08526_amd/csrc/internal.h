@@ -18,6 +18,7 @@ struct LinDesc {
     int M, N, K;
     int tiles_m, tiles_n;
     int tile_begin;  // first logical tile of this layer in a grouped launch
+    const int *xexp; // fp16 path: per-row power-of-two shift of X (see xprep.hip)
 };
 
 struct GroupArgs {
@@ -42,7 +43,13 @@ hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
 // Large-M kernel (bf16 activations): 128 x 256 tiles, direct-to-LDS pipeline.
 int big_tile_bm();
 int big_tile_bn();
-hipError_t launch_qgemm_big(int fmt, const GroupArgs &args, hipStream_t stream);
+// f16: X points to fp16 activations prepared by launch_xprep and xexp to
+// their per-row shifts.
+hipError_t launch_qgemm_big(int fmt, bool f16, const GroupArgs &args, hipStream_t stream);
+
+// bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M].
+hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
+                        hipStream_t stream);
 
 // Few-row kernel (bf16 activations, M <= skinny_max_m()): one layer per
 // launch, workgroups of 16 weight rows with K split over their wavefronts.

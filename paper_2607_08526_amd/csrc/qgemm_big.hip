@@ -36,6 +36,16 @@
 // load writes lane t's data to slot base + t, so the swizzle is applied by
 // choosing which global chunk each lane fetches.
 //
+// fp16 variant (F16): the host first converts the activations exactly to
+// fp16 with a per-row power-of-two shift (xprep.hip); the kernel pre-scans the
+// tile's scales for a shift f that keeps every |c * s * 2^-f| <= Q * smax *
+// 2^-f < 2^15, dequantizes each weight to fp16 (c exact in fp16 by a
+// magic-number add, then one rounded packed multiply by s * 2^-f), and
+// accumulates the whole K inside v_mfma_f32_16x16x32_f16, so the per-block
+// scale FMAs disappear.  The only rounding beyond fp32 accumulation is that
+// of c * s to 11 significant bits (~2e-4 of max|Y| at the DiT shapes,
+// against the 2e-3 tolerance).  The epilogue applies both shifts exactly.
+//
 // Tile order: within a layer, groups of 4 row tiles walked row-tile fastest;
 // each of the 8 XCDs takes a contiguous range of one layer's tiles (L2
 // reuse), and every layer of a grouped launch is spread over all XCDs.
@@ -47,6 +57,8 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
 constexpr int MSUB = 8, NSUB = 2, BM = 16 * MSUB, BN = 64 * NSUB, NST = 3, GROUP_M = 4;
 
@@ -71,6 +83,14 @@ __device__ inline constexpr int vmcnt_imm(int v)
     // expcnt (bits 6:4) and lgkmcnt (bits 11:8) left at "no wait"
     return (v & 15) | (((v >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
 }
+
+// activation chunk swizzle: the 16 rows one MFMA operand read touches land
+// on distinct banks whether the LDS serves 8 lanes of a 16-byte read per
+// clock from 32 banks or 16 lanes from 64 banks
+__device__ inline int xswz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+
+// s_waitcnt lgkmcnt(0) with vmcnt and expcnt left at "no wait"
+__device__ inline constexpr int lgkm0_imm() { return 15 | (3 << 14) | (7 << 4); }
 
 // Direct-to-LDS loads from (wave-uniform base + per-lane 32-bit offset):
 // lane t's data lands at LDS address lds + t * size.
@@ -100,6 +120,47 @@ __device__ inline f32x4 mfma(u32x4 a, u32x4 b, f32x4 c)
 {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ inline f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+                                                  __builtin_bit_cast(half8, b), c, 0, 0, 0);
+}
+
+__device__ inline uint32_t h2mul_add(uint32_t v, half2v bias, half2v sp)
+{
+    // (v + bias) exact (an fp16 integer), then one rounded multiply
+    return __builtin_bit_cast(uint32_t, (__builtin_bit_cast(half2v, v) + bias) * sp);
+}
+
+// 8 int8 codes -> 8 fp16 of c * s', natural order.  byte ^ 0x80 = c + 128 is
+// placed under the fp16 pattern 0x64 (= 1024 + (c + 128)) by v_perm; adding
+// -1152 leaves c exactly.
+__device__ inline u32x4 deq_int8_f16(uint32_t a, uint32_t b, half2v sp)
+{
+    const uint32_t x = a ^ 0x80808080u, y = b ^ 0x80808080u, hi = 0x64646464u;
+    const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
+    u32x4 r;
+    r[0] = h2mul_add(__builtin_amdgcn_perm(hi, x, 0x04010400u), bias, sp);
+    r[1] = h2mul_add(__builtin_amdgcn_perm(hi, x, 0x04030402u), bias, sp);
+    r[2] = h2mul_add(__builtin_amdgcn_perm(hi, y, 0x04010400u), bias, sp);
+    r[3] = h2mul_add(__builtin_amdgcn_perm(hi, y, 0x04030402u), bias, sp);
+    return r;
+}
+
+// 8 q4 codes -> 8 fp16 of c * s', natural order: nibble ^ 8 = c + 8 under
+// the fp16 pattern 0x6400 (= 1024 + c + 8); adding -1032 leaves c exactly.
+__device__ inline u32x4 deq_q4_f16(uint32_t c, half2v sp)
+{
+    const uint32_t x = c ^ 0x88888888u, y = x >> 4;
+    const half2v bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
+    u32x4 r;
+    r[0] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C040C00u) & 0x000F000Fu) | 0x64006400u, bias, sp);
+    r[1] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C050C01u) & 0x000F000Fu) | 0x64006400u, bias, sp);
+    r[2] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C060C02u) & 0x000F000Fu) | 0x64006400u, bias, sp);
+    r[3] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C070C03u) & 0x000F000Fu) | 0x64006400u, bias, sp);
+    return r;
 }
 
 // fp32 high halves of (lo, hi) as a bf16 pair (exact for small integers)
@@ -154,6 +215,7 @@ struct Ctx {
     // per-lane byte offsets from those bases, fixed for the whole K loop
     uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff;
     int wave, l16, lg;
+    int negf;  // F16: weights enter as c * s * 2^negf
 };
 
 // Issue the direct-to-LDS loads of step s into one ring stage.
@@ -172,6 +234,49 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
     for (int r = 0; r < G::CLOADS; ++r)
         dma16(cb, c.coff[r], base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
     dma4(sb, c.soff, base + G::XBYTES + G::CBYTES + (c.wave % (BN / 64)) * 256);
+}
+
+template <int FMT>
+__device__ inline void compute_stage_f16(const Ctx<FMT> &c, const uint8_t *stage,
+                                         f32x4 (&acc)[MSUB][NSUB])
+{
+    using G = Geo<FMT>;
+    uint32_t sc[NSUB];
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j)
+        sc[j] = *reinterpret_cast<const uint32_t *>(stage + G::XBYTES + G::CBYTES +
+                                                    (c.wave * (16 * NSUB) + j * 16 + c.l16) * 4);
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+        u32x4 B[NSUB];
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j) {
+            const int row = c.wave * (16 * NSUB) + j * 16 + c.l16;
+            const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(sc[j] >> (16 * bi)));
+            const _Float16 sp1 = (_Float16)__builtin_amdgcn_ldexpf(s, c.negf);
+            const half2v sp = {sp1, sp1};
+            if (FMT == QL_FMT_INT8) {
+                const int ch = (bi * 2 + (c.lg >> 1)) ^ ((row >> 2) & 3);
+                const uint2 v = *reinterpret_cast<const uint2 *>(
+                    stage + G::XBYTES + row * 64 + ch * 16 + (c.lg & 1) * 8);
+                B[j] = deq_int8_f16(v.x, v.y, sp);
+            } else {
+                const int ch = bi ^ ((row >> 3) & 1);
+                const uint32_t v = *reinterpret_cast<const uint32_t *>(
+                    stage + G::XBYTES + row * 32 + ch * 16 + c.lg * 4);
+                B[j] = deq_q4_f16(v, sp);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < MSUB; ++i) {
+            const int row = i * 16 + c.l16;
+            const int slot = bi * 512 + row * 4 + (c.lg ^ xswz(c.l16));
+            const u32x4 a = *reinterpret_cast<const u32x4 *>(stage + slot * 16);
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j)
+                acc[i][j] = mfma_f16(a, B[j], acc[i][j]);
+        }
+    }
 }
 
 template <int FMT>
@@ -214,7 +319,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
         // the step (which would exhaust the register file)
         auto read_a = [&](int i) {
             const int row = i * 16 + c.l16;
-            const int slot = bi * 512 + row * 4 + (c.lg ^ ((row >> 2) & 3));
+            const int slot = bi * 512 + row * 4 + (c.lg ^ xswz(row));
             return *reinterpret_cast<const u32x4 *>(stage + slot * 16);
         };
         u32x4 a = read_a(0);
@@ -245,7 +350,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
     }
 }
 
-template <int FMT>
+template <int FMT, bool F16>
 __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
@@ -295,7 +400,7 @@ __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
     for (int r = 0; r < G::XLOADS; ++r) {
         const int slot = r * 256 + tid;
         const int bi = slot >> 9, rem = slot & 511, row = rem >> 2;
-        const int g = (rem & 3) ^ ((row >> 2) & 3);
+        const int g = (rem & 3) ^ xswz(row);
         const int m = min(m0 + row, M - 1) - m0;
         c.xoff[r] = (uint32_t)(m * K * 2 + bi * 64 + g * 16);
     }
@@ -335,6 +440,37 @@ __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
     if (ns > 1)
         issue_stage<FMT>(c, lds[1], 1);
 
+    c.negf = 0;
+    if (F16) {
+        // largest scale of this tile's weight rows (fp16 bit patterns of
+        // non-negative values compare as integers) -> shift keeping every
+        // dequantized weight below 2^15 in magnitude.  Issued behind the
+        // first two stages so its latency overlaps theirs.
+        __shared__ uint32_t wmax[4];
+        const int count = min(BN, N - n0) * nb / 2;  // dwords, contiguous
+        const uint32_t *sp = reinterpret_cast<const uint32_t *>(c.sbase);
+        uint32_t mx = 0;
+        for (int q = tid; q < count; q += 256) {
+            const uint32_t v = sp[q];
+            mx = max(mx, max(v & 0x7FFFu, (v >> 16) & 0x7FFFu));
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
+        if ((tid & 63) == 0)
+            wmax[tid >> 6] = mx;
+        // LDS write visible, then barrier (no fence: the ring stays in flight)
+        __builtin_amdgcn_s_waitcnt(lgkm0_imm());
+        __builtin_amdgcn_s_barrier();
+        mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+        const float smax = (float)__builtin_bit_cast(_Float16, (uint16_t)mx);
+        if (smax > 0.f) {
+            int E;
+            (void)__builtin_frexpf(smax * (float)(FMT == QL_FMT_INT8 ? 127 : 7), &E);
+            c.negf = 15 - E;  // Q * smax * 2^negf in [2^14, 2^15)
+        }
+    }
+
     // one step: wait for stage s (loads complete in issue order, so allowing
     // the LOADS youngest ones, which are stage s+1's, to remain outstanding
     // means all of stage s has landed), barrier, refill the slot that step
@@ -351,7 +487,10 @@ __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
         __builtin_amdgcn_s_barrier();                                               \
         if (s + 2 < ns)                                                             \
             issue_stage<FMT>(c, lds[((Q) + 2) % NST], s + 2);                       \
-        compute_stage<FMT>(c, lds[(Q)], acc);                                       \
+        if (F16)                                                                    \
+            compute_stage_f16<FMT>(c, lds[(Q)], acc);                               \
+        else                                                                        \
+            compute_stage<FMT>(c, lds[(Q)], acc);                                   \
     }
 
     for (int s0 = 0; s0 < ns; s0 += NST) {
@@ -371,7 +510,9 @@ __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
             for (int r = 0; r < 4; ++r) {
                 const int m = m0 + i * 16 + c.lg * 4 + r;
                 if (m < M && n < N)
-                    d.Y[(int64_t)m * N + n] = acc[i][j][r];
+                    d.Y[(int64_t)m * N + n] =
+                        F16 ? __builtin_amdgcn_ldexpf(acc[i][j][r], d.xexp[m] - c.negf)
+                            : acc[i][j][r];
             }
         }
 }
@@ -381,13 +522,20 @@ __global__ __launch_bounds__(256, 2) void qgemm_big_kernel(const GroupArgs args)
 int big_tile_bm() { return BM; }
 int big_tile_bn() { return BN; }
 
-hipError_t launch_qgemm_big(int fmt, const GroupArgs &args, hipStream_t stream)
+hipError_t launch_qgemm_big(int fmt, bool f16, const GroupArgs &args, hipStream_t stream)
 {
     dim3 grid((unsigned)args.total_tiles), block(256);
-    if (fmt == QL_FMT_INT8)
-        hipLaunchKernelGGL(qgemm_big_kernel<QL_FMT_INT8>, grid, block, 0, stream, args);
-    else
-        hipLaunchKernelGGL(qgemm_big_kernel<QL_FMT_Q4>, grid, block, 0, stream, args);
+    if (fmt == QL_FMT_INT8) {
+        if (f16)
+            hipLaunchKernelGGL((qgemm_big_kernel<QL_FMT_INT8, true>), grid, block, 0, stream, args);
+        else
+            hipLaunchKernelGGL((qgemm_big_kernel<QL_FMT_INT8, false>), grid, block, 0, stream, args);
+    } else {
+        if (f16)
+            hipLaunchKernelGGL((qgemm_big_kernel<QL_FMT_Q4, true>), grid, block, 0, stream, args);
+        else
+            hipLaunchKernelGGL((qgemm_big_kernel<QL_FMT_Q4, false>), grid, block, 0, stream, args);
+    }
     return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // argument checks, tile-shape choice and launch.  Every check happens before
 // anything is enqueued; no entry point throws or aborts.
 #include <algorithm>
+#include <mutex>
 
 #include "internal.h"
 
@@ -31,6 +32,39 @@ int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const vo
         return QL_ERR_ALIGN;
     return QL_OK;
 }
+
+// Stream-ordered pool (one per device) for the fp16 copies of the
+// activations that the large-M bf16 path works from.  The pool keeps what it
+// has grown to, so steady-state calls reuse memory without touching the
+// driver; allocations are freed in stream order right after their launch.
+hipMemPool_t workspace_pool()
+{
+    constexpr int MAXDEV = 64;
+    static std::mutex mu;
+    static hipMemPool_t pools[MAXDEV] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV)
+        return nullptr;
+    std::lock_guard<std::mutex> g(mu);
+    if (!pools[dev]) {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t p = nullptr;
+        if (hipMemPoolCreate(&p, &props) != hipSuccess)
+            return nullptr;
+        uint64_t keep = UINT64_MAX;
+        if (hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) {
+            hipMemPoolDestroy(p);
+            return nullptr;
+        }
+        pools[dev] = p;
+    }
+    return pools[dev];
+}
+
+size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 TileCfg choose_tile(int64_t M, bool xf32)
 {
@@ -73,9 +107,11 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         maxM = std::max(maxM, ls[i]->M);
     const TileCfg t = choose_tile(maxM, xf32);
     // the large-M kernel moves two scale blocks per row as one aligned dword
+    // and addresses a tile's rows with 32-bit offsets
     bool big = !xf32 && t == TILE_M128;
     for (int i = 0; i < n; ++i)
-        big = big && ls[i]->K % 64 == 0 && aligned(ls[i]->scales, 4);
+        big = big && ls[i]->K % 64 == 0 && ls[i]->K < ((int64_t)1 << 23) &&
+              aligned(ls[i]->scales, 4);
     const int bm = big ? big_tile_bm() : tile_bm(t);
     const int bn = big ? big_tile_bn() : tile_bn(t);
 
@@ -105,9 +141,56 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
-    const hipError_t e = big ? launch_qgemm_big(ord[0]->fmt, a, stream)
-                             : launch_qgemm(ord[0]->fmt, xf32, t, a, stream);
-    return e == hipSuccess ? QL_OK : QL_ERR_HIP;
+    if (!big)
+        return launch_qgemm(ord[0]->fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+
+    // fp16 path: one exact, row-shifted fp16 copy per distinct activation
+    // tensor (layers reading the same X share it)
+    int src[QL_MAX_GROUP];
+    size_t off[QL_MAX_GROUP], bytes = 0;
+    for (int i = 0; i < n; ++i) {
+        src[i] = i;
+        for (int j = 0; j < i; ++j)
+            if (a.d[j].X == a.d[i].X && a.d[j].M == a.d[i].M && a.d[j].K == a.d[i].K) {
+                src[i] = j;
+                break;
+            }
+        if (src[i] == i) {
+            off[i] = bytes;
+            bytes += round256((size_t)a.d[i].M * a.d[i].K * 2) + round256((size_t)a.d[i].M * 4);
+        }
+    }
+    hipMemPool_t pool = workspace_pool();
+    if (!pool)
+        return QL_ERR_HIP;
+    void *ws = nullptr;
+    if (hipMallocFromPoolAsync(&ws, bytes, pool, stream) != hipSuccess)
+        return QL_ERR_HIP;
+    hipError_t e = hipSuccess;
+    const void *xs[QL_MAX_GROUP];
+    const int *es[QL_MAX_GROUP];
+    for (int i = 0; i < n; ++i) {
+        if (src[i] != i) {
+            xs[i] = xs[src[i]];
+            es[i] = es[src[i]];
+            continue;
+        }
+        uint8_t *base = (uint8_t *)ws + off[i];
+        uint16_t *xh = (uint16_t *)base;
+        int *ex = (int *)(base + round256((size_t)a.d[i].M * a.d[i].K * 2));
+        if (e == hipSuccess)
+            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, xh, ex, stream);
+        xs[i] = xh;
+        es[i] = ex;
+    }
+    for (int i = 0; i < n; ++i) {
+        a.d[i].X = xs[i];
+        a.d[i].xexp = es[i];
+    }
+    if (e == hipSuccess)
+        e = launch_qgemm_big(ord[0]->fmt, true, a, stream);
+    const hipError_t ef = hipFreeAsync(ws, stream);
+    return e == hipSuccess && ef == hipSuccess ? QL_OK : QL_ERR_HIP;
 }
 
 }  // namespace

@@ -1,0 +1,80 @@
+// Activation pre-pass of the large-M forward: bf16 X [M][K] -> fp16 X' [M][K]
+// with a per-row power-of-two shift e[m], X'[m][k] = X[m][k] * 2^-e[m].
+//
+// bf16 carries 8 significant bits and fp16 11, so the conversion is exact
+// whenever the shifted value lands in fp16's normal range.  e[m] puts the
+// row's largest magnitude in [2^14, 2^15): nothing overflows, and only values
+// below 2^-29 of the row maximum (fp16 subnormals after the shift) are
+// rounded, by at most 2^-25 of the shifted scale.  The forward kernel
+// multiplies its fp32 results back by 2^e[m] exactly.
+//
+// One workgroup per row: a max-reduction pass, then a convert-and-store pass
+// (the second read hits L2).
+#include "internal.h"
+
+namespace qlk {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__ X, int K,
+                                                    uint16_t *__restrict__ Xh,
+                                                    int *__restrict__ rexp)
+{
+    const int m = blockIdx.x;
+    const u32x4 *row = reinterpret_cast<const u32x4 *>(X + (int64_t)m * K);
+    u32x4 *out = reinterpret_cast<u32x4 *>(Xh + (int64_t)m * K);
+    const int n16 = K / 8;  // 16-byte chunks per row (K % 32 == 0)
+
+    // largest |x| of the row, compared as bf16 bit patterns (monotone for
+    // non-NaN magnitudes)
+    uint32_t mx = 0;
+    for (int i = threadIdx.x; i < n16; i += 256) {
+        const u32x4 v = row[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            mx = max(mx, v[j] & 0x7FFFu);
+            mx = max(mx, (v[j] >> 16) & 0x7FFFu);
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
+    __shared__ uint32_t wmax[4];
+    if ((threadIdx.x & 63) == 0)
+        wmax[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+
+    // exponent of the row maximum (bf16: value in [2^(E-127), 2^(E-126)));
+    // zero, subnormal-only or non-finite rows keep e = 0
+    const int E = (int)(mx >> 7);
+    const int e = (E >= 1 && E <= 254) ? (E - 127) - 14 : 0;
+    if (threadIdx.x == 0)
+        rexp[m] = e;
+
+    for (int i = threadIdx.x; i < n16; i += 256) {
+        const u32x4 v = row[i];
+        half8 h;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            h[2 * j] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] << 16), -e);
+            h[2 * j + 1] =
+                (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] & 0xFFFF0000u), -e);
+        }
+        out[i] = __builtin_bit_cast(u32x4, h);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
+                        hipStream_t stream)
+{
+    hipLaunchKernelGGL(xprep_kernel, dim3((unsigned)M), dim3(256), 0, stream,
+                       reinterpret_cast<const uint16_t *>(X), K, Xh, rexp);
+    return hipGetLastError();
+}
+
+}  // namespace qlk
