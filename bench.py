@@ -29,8 +29,14 @@ HBM_PEAK_GBPS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 ROT_BYTES = 512 << 20  # rotate weight copies past the 256 MB last-level cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_step_q4.txt")
-KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm.hip", "paper_2607_08526_amd/csrc/internal.h",
-                  "paper_2607_08526_amd/csrc/qlinear.hip"]
+# the kernels one step launch runs (activation pre-pass + large-M GEMM) and
+# the host code that picks and configures them; the recorded traffic is only
+# valid for the sources it was measured on
+KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm_big.hip", "paper_2607_08526_amd/csrc/xprep.hip",
+                  "paper_2607_08526_amd/csrc/internal.h", "paper_2607_08526_amd/csrc/qlinear.hip"]
+GEMM_KERNEL = "qgemm_big_kernel"
+PREP_KERNEL = "xprep_kernel"
+COPY_BYTES = 1 << 30  # the calibration copy: 1 GiB read + 1 GiB written
 
 
 def kernel_source_hash():
@@ -56,7 +62,86 @@ def parse():
                     help="target duration of the oracle's timed sample")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain device copy of known size (counter calibration)")
+    ap.add_argument("--summarize-stats", metavar="DIR",
+                    help="print a kernel summary of a rocprofv3 --stats output dir and exit")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
+                         "'bench.py --calib-copy' into the traffic record and exit")
     return ap.parse_args()
+
+
+def _csvs(d, suffix):
+    import glob
+    return sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+
+
+def summarize_stats(d):
+    """Kernel table of a rocprofv3 --kernel-trace --stats run."""
+    import csv
+    rows = []
+    for p in _csvs(d, "kernel_stats.csv"):
+        rows += list(csv.DictReader(open(p)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    out = [f"{'calls':>6} {'avg_us':>10} {'min_us':>10} {'max_us':>10} {'total_ms':>10} {'pct':>6}  kernel"]
+    for r in rows:
+        name = r["Name"].replace("(anonymous namespace)::", "")
+        short = name.split("(")[0][:90]
+        out.append(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.2f} "
+                   f"{float(r['MinNs']) / 1e3:10.2f} {float(r['MaxNs']) / 1e3:10.2f} "
+                   f"{float(r['TotalDurationNs']) / 1e6:10.3f} {float(r['Percentage']):6.2f}  {short}")
+    return "\n".join(out)
+
+
+def _counter_avg(d, counter):
+    """Per-dispatch average of one counter, by kernel (KiB for FETCH/WRITE_SIZE)."""
+    import csv, collections
+    acc = collections.defaultdict(list)
+    for p in _csvs(d, "counter_collection.csv"):
+        for r in csv.DictReader(open(p)):
+            if r["Counter_Name"] == counter:
+                acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return acc
+
+
+def summarize_traffic(fetch_dir, write_dir):
+    """HBM bytes of one step launch (the pre-pass dispatches and the GEMM of
+    one block call), each counter scaled by what it reads for a plain copy of
+    COPY_BYTES."""
+    f = _counter_avg(fetch_dir, "FETCH_SIZE")
+    w = _counter_avg(write_dir, "WRITE_SIZE")
+
+    def pick(acc, key, pred=None):
+        ks = [k for k in acc if key in k and (pred is None or pred(acc[k]))]
+        if not ks:
+            raise SystemExit(f"no dispatches of {key} in the counter output")
+        vals = [v for k in ks for v in acc[k]]
+        return vals
+
+    # the calibration copy: the largest single dispatch of a copy kernel
+    def copy_val(acc):
+        ks = [k for k in acc if "copy" in k.lower()]
+        if not ks:
+            raise SystemExit("no copy kernel in the counter output (run with --calib-copy)")
+        return max(v for k in ks for v in acc[k])
+
+    fcal = copy_val(f) * 1024 / COPY_BYTES
+    wcal = copy_val(w) * 1024 / COPY_BYTES
+    gf, gw = pick(f, GEMM_KERNEL), pick(w, GEMM_KERNEL)
+    pf, pw = pick(f, PREP_KERNEL), pick(w, PREP_KERNEL)
+    # each block call runs one GEMM dispatch and one pre-pass per distinct X
+    prep_per_call = len(pf) / len(gf)
+    gemm_b = (sum(gf) / len(gf) * 1024 / fcal) + (sum(gw) / len(gw) * 1024 / wcal)
+    prep_b = prep_per_call * ((sum(pf) / len(pf) * 1024 / fcal) + (sum(pw) / len(pw) * 1024 / wcal))
+    return {
+        "kernel_source_sha256": kernel_source_hash(),
+        "hbm_bytes_per_launch": round(gemm_b + prep_b),
+        "gemm_bytes_per_dispatch": round(gemm_b),
+        "prep_bytes_per_call": round(prep_b),
+        "prep_dispatches_per_call": prep_per_call,
+        "fetch_calibration": round(fcal, 4),
+        "write_calibration": round(wcal, 4),
+        "gemm_dispatches": len(gf),
+    }
 
 
 class Step:
@@ -254,6 +339,12 @@ def traffic_entry():
 
 def main():
     args = parse()
+    if args.summarize_stats:
+        print(summarize_stats(args.summarize_stats))
+        return
+    if args.summarize_traffic:
+        print(json.dumps(summarize_traffic(*args.summarize_traffic), indent=1))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -309,7 +400,8 @@ def main():
             "bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
             "traffic": traffic_entry(),
-            "kernel": "qgemm_kernel<q4, bf16 X, 128x128 tile> (one grouped launch per block)",
+            "kernel": "one block call: xprep_kernel (bf16 -> row-shifted fp16, per distinct X) "
+                      "+ qgemm_big_kernel<q4, fp16> (128x128 tiles, 4 linears grouped)",
             "flops_per_launch": step.flops_per_block,
             "avg_launch_ms": round(avg_launch_ms, 5),
         },

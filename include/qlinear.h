@@ -23,6 +23,15 @@
  * with W [N][K] (out x in, like a framework's Linear weight), X [M][K] and
  * Y [M][N], all row-major.
  *
+ * Accuracy of the forward product against the exact sum above: fp32
+ * activations and bf16 activations at M <= 64 (or when K % 64 != 0) are
+ * contracted with the exact codes and fp32 block partials (error a few fp32
+ * roundings).  bf16 activations at larger M take the fp16 path: X is copied
+ * exactly to fp16 with a power-of-two shift per row, each weight enters the
+ * matrix cores as fp16(c * s * 2^f) with one shift f per 128-row weight tile,
+ * so the one extra rounding is that of c * s to 11 significant bits
+ * (relative 2^-12 per weight; about 2e-4 of max |Y| at transformer shapes).
+ *
  * Data formats (all buffers are DEVICE memory owned by the caller):
  *   W       fp32 [N][K]
  *   codes   QL_FMT_INT8: int8 [N][K], two's complement
@@ -45,6 +54,13 @@
  *     enqueued work.  Asynchronous device faults surface at the caller's next
  *     synchronization, as in HIP itself.
  *   - The library keeps no pointer after a call returns.
+ *   - Workspace: the fp16 path (above) needs M * K * 2 + M * 4 bytes per
+ *     distinct activation tensor of a call.  It is taken stream-ordered from
+ *     a memory pool the library owns (one per device, created on first use)
+ *     and returned to it, in stream order, right after the launch; the pool
+ *     keeps what it has grown to, so steady-state calls do not reach the
+ *     driver.  No other forward path uses device memory beyond its
+ *     arguments.  Allocation failure returns QL_ERR_HIP.
  */
 #ifndef QLINEAR_H
 #define QLINEAR_H
@@ -94,8 +110,9 @@ int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K,
                      void *codes, uint16_t *scales, hipStream_t stream);
 
 /* Y[M][N] (fp32) = X[M][K] * dequant(codes, scales)^T, the forward pass of
- * one quantized linear layer.  Asynchronous on `stream`; allocates nothing
- * and does not synchronize.  M == 0 is a successful no-op.  Y must not alias
+ * one quantized linear layer.  Asynchronous on `stream`; does not
+ * synchronize, and allocates nothing outside the workspace pool described
+ * above.  M == 0 is a successful no-op.  Y must not alias
  * X, codes or scales.  Sizes: M, N < 2^31, K < 2^31. */
 int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K,
                     const void *codes, const uint16_t *scales, int64_t N,
@@ -119,8 +136,9 @@ typedef struct {
  * grouped launch.  The n_lin (1..QL_MAX_GROUP) products are independent:
  * no Y may alias any X, codes, scales or other Y of the group.  Layers that
  * share fmt and xdt run in one launch over their combined tiles; otherwise
- * the call falls back to one launch per layer.  Asynchronous on `stream`,
- * allocates nothing.  Each entry is checked as in qlinear_forward. */
+ * the call falls back to one launch per layer; layers reading the same X
+ * share its fp16 copy.  Asynchronous on `stream`, workspace as above.  Each
+ * entry is checked as in qlinear_forward. */
 int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream);
 
 /* Static description of a status code. */
