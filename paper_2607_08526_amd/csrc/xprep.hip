@@ -8,8 +8,8 @@
 // rounded, by at most 2^-25 of the shifted scale.  The forward kernel
 // multiplies its fp32 results back by 2^e[m] exactly.
 //
-// One workgroup per row: a max-reduction pass, then a convert-and-store pass
-// (the second read hits L2).
+// One workgroup per row; rows up to 16384 wide are read once and held in
+// registers between the max-reduction and the convert-and-store.
 #include "internal.h"
 
 namespace qlk {
@@ -18,6 +18,47 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+__device__ inline uint32_t bf16_absmax2(uint32_t v)
+{
+    return max(v & 0x7FFFu, (v >> 16) & 0x7FFFu);
+}
+
+// largest |x| of the row, compared as bf16 bit patterns (monotone for
+// non-NaN magnitudes), reduced over the workgroup -> the row's shift e
+__device__ inline int row_shift(uint32_t mx, int *rexp, int m)
+{
+    __shared__ uint32_t wmax[4];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
+    if ((threadIdx.x & 63) == 0)
+        wmax[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+    // exponent of the row maximum (bf16: value in [2^(E-127), 2^(E-126)));
+    // zero, subnormal-only or non-finite rows keep e = 0
+    const int E = (int)(mx >> 7);
+    const int e = (E >= 1 && E <= 254) ? (E - 127) - 14 : 0;
+    if (threadIdx.x == 0)
+        rexp[m] = e;
+    return e;
+}
+
+__device__ inline u32x4 to_f16(u32x4 v, int e)
+{
+    half8 h;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        h[2 * j] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] << 16), -e);
+        h[2 * j + 1] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] & 0xFFFF0000u), -e);
+    }
+    return __builtin_bit_cast(u32x4, h);
+}
+
+// R > 0: the row (K / 8 16-byte chunks <= 256 * R) is read once into
+// registers.  R == 0: any K, a max pass and a convert pass (the second read
+// of the row hits L2).
+template <int R>
 __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__ X, int K,
                                                     uint16_t *__restrict__ Xh,
                                                     int *__restrict__ rexp)
@@ -25,45 +66,36 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
     const int m = blockIdx.x;
     const u32x4 *row = reinterpret_cast<const u32x4 *>(X + (int64_t)m * K);
     u32x4 *out = reinterpret_cast<u32x4 *>(Xh + (int64_t)m * K);
-    const int n16 = K / 8;  // 16-byte chunks per row (K % 32 == 0)
-
-    // largest |x| of the row, compared as bf16 bit patterns (monotone for
-    // non-NaN magnitudes)
+    const int n16 = K / 8;
+    const int t = threadIdx.x;
     uint32_t mx = 0;
-    for (int i = threadIdx.x; i < n16; i += 256) {
-        const u32x4 v = row[i];
+    if (R > 0) {
+        u32x4 v[R > 0 ? R : 1];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            mx = max(mx, v[j] & 0x7FFFu);
-            mx = max(mx, (v[j] >> 16) & 0x7FFFu);
+        for (int r = 0; r < R; ++r) {
+            const int i = t + r * 256;
+            v[r] = i < n16 ? row[i] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                mx = max(mx, bf16_absmax2(v[r][j]));
         }
-    }
+        const int e = row_shift(mx, rexp, m);
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1)
-        mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
-    __shared__ uint32_t wmax[4];
-    if ((threadIdx.x & 63) == 0)
-        wmax[threadIdx.x >> 6] = mx;
-    __syncthreads();
-    mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
-
-    // exponent of the row maximum (bf16: value in [2^(E-127), 2^(E-126)));
-    // zero, subnormal-only or non-finite rows keep e = 0
-    const int E = (int)(mx >> 7);
-    const int e = (E >= 1 && E <= 254) ? (E - 127) - 14 : 0;
-    if (threadIdx.x == 0)
-        rexp[m] = e;
-
-    for (int i = threadIdx.x; i < n16; i += 256) {
-        const u32x4 v = row[i];
-        half8 h;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            h[2 * j] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] << 16), -e);
-            h[2 * j + 1] =
-                (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] & 0xFFFF0000u), -e);
+        for (int r = 0; r < R; ++r) {
+            const int i = t + r * 256;
+            if (i < n16)
+                out[i] = to_f16(v[r], e);
         }
-        out[i] = __builtin_bit_cast(u32x4, h);
+    } else {
+        for (int i = t; i < n16; i += 256) {
+            const u32x4 v = row[i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                mx = max(mx, bf16_absmax2(v[j]));
+        }
+        const int e = row_shift(mx, rexp, m);
+        for (int i = t; i < n16; i += 256)
+            out[i] = to_f16(row[i], e);
     }
 }
 
@@ -72,8 +104,19 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
 hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
                         hipStream_t stream)
 {
-    hipLaunchKernelGGL(xprep_kernel, dim3((unsigned)M), dim3(256), 0, stream,
-                       reinterpret_cast<const uint16_t *>(X), K, Xh, rexp);
+    const uint16_t *x = reinterpret_cast<const uint16_t *>(X);
+    const int n16 = K / 8;
+    const dim3 grid((unsigned)M), block(256);
+    if (n16 <= 256)
+        hipLaunchKernelGGL(xprep_kernel<1>, grid, block, 0, stream, x, K, Xh, rexp);
+    else if (n16 <= 512)
+        hipLaunchKernelGGL(xprep_kernel<2>, grid, block, 0, stream, x, K, Xh, rexp);
+    else if (n16 <= 1024)
+        hipLaunchKernelGGL(xprep_kernel<4>, grid, block, 0, stream, x, K, Xh, rexp);
+    else if (n16 <= 2048)
+        hipLaunchKernelGGL(xprep_kernel<8>, grid, block, 0, stream, x, K, Xh, rexp);
+    else
+        hipLaunchKernelGGL(xprep_kernel<0>, grid, block, 0, stream, x, K, Xh, rexp);
     return hipGetLastError();
 }
 

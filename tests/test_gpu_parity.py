@@ -132,6 +132,44 @@ def test_forward_ragged(gpu, orc, fmt, xdt, N, K):
         assert e <= TOL[xdt], (M, N, K, e)
 
 
+@pytest.mark.parametrize("K", [4096, 16384, 16448])
+def test_forward_long_rows(gpu, orc, K):
+    """Large-M bf16 path at reduction lengths that exercise every row width
+    of the activation pre-pass (held in registers up to K = 16384, two reads
+    beyond)."""
+    M, N = 80, 48
+    for fmt in (O.FMT_INT8, O.FMT_Q4):
+        W, X = si.small_case(40 + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        assert rel_err(Yg, Yr) <= TOL[O.DT_BF16], (fmt, K)
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_row_scales_far_apart(gpu, orc, fmt):
+    """Activation rows scaled by 2^-100 .. 2^100 (and one all-zero row): each
+    row's own relative error stays within the tolerance, on the small-M path
+    and on the large-M path (per-row power-of-two shifts)."""
+    rng = np.random.default_rng(91 + fmt)
+    N, K = 96, 256
+    for M in (40, 200):
+        W, X0 = si.small_case(92 + M + fmt, M, N, K, O.DT_F32)
+        e = rng.integers(-100, 101, M).astype(np.float64)
+        Xf = (X0.astype(np.float64) * 2.0 ** e[:, None]).astype(np.float32)
+        Xf[M // 2] = 0.0
+        X = si.f32_to_bf16_bits(Xf)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N).astype(np.float64)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        assert np.all(Yg[M // 2] == 0.0)
+        for m in range(M):
+            if m == M // 2:
+                continue
+            err = np.max(np.abs(Yg[m] - Yr[m])) / np.max(np.abs(Yr[m]))
+            assert err <= TOL[O.DT_BF16], (M, m, err)
+
+
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 @pytest.mark.parametrize("xdt", [O.DT_BF16, O.DT_F32])
 def test_forward_power_of_two_exact(gpu, orc, fmt, xdt):
