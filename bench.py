@@ -32,9 +32,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_step_q4.txt")
 # the kernels one step launch runs (activation pre-pass + large-M GEMM) and
 # the host code that picks and configures them; the recorded traffic is only
 # valid for the sources it was measured on
-KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm_big.hip", "paper_2607_08526_amd/csrc/xprep.hip",
+KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm_wide.hip", "paper_2607_08526_amd/csrc/xprep.hip",
                   "paper_2607_08526_amd/csrc/internal.h", "paper_2607_08526_amd/csrc/qlinear.hip"]
-GEMM_KERNEL = "qgemm_big_kernel"
+GEMM_KERNEL = "qgemm_wide_kernel"
 PREP_KERNEL = "xprep_kernel"
 COPY_BYTES = 1 << 30  # the calibration copy: 1 GiB read + 1 GiB written
 
@@ -401,7 +401,7 @@ def main():
             "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
             "traffic": traffic_entry(),
             "kernel": "one block call: xprep_kernel (bf16 -> row-shifted fp16, per distinct X) "
-                      "+ qgemm_big_kernel<q4, fp16> (128x128 tiles, 4 linears grouped)",
+                      "+ qgemm_wide_kernel<q4> (fp16 MFMA, 128x256 tiles, 4 linears grouped)",
             "flops_per_launch": step.flops_per_block,
             "avg_launch_ms": round(avg_launch_ms, 5),
         },

@@ -40,12 +40,13 @@ hipError_t launch_quantize(int fmt, const float *W, int64_t N, int64_t K, uint8_
 hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
                         hipStream_t stream);
 
-// Large-M kernel (bf16 activations): 128 x 256 tiles, direct-to-LDS pipeline.
-int big_tile_bm();
-int big_tile_bn();
-// f16: X points to fp16 activations prepared by launch_xprep and xexp to
-// their per-row shifts.
-hipError_t launch_qgemm_big(int fmt, bool f16, const GroupArgs &args, hipStream_t stream);
+// Large-M kernel of the fp16 path (bf16 activations): 128 x 256 tiles,
+// direct-to-LDS pipeline.  Each LinDesc's X points to the fp16 activations
+// prepared by launch_xprep and xexp to their per-row shifts; K % 256 == 0 and
+// 16-byte aligned scales.
+int wide_tile_bm();
+int wide_tile_bn();
+hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
 // bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M].
 hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,

@@ -106,14 +106,14 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->M);
     const TileCfg t = choose_tile(maxM, xf32);
-    // the large-M kernel moves two scale blocks per row as one aligned dword
-    // and addresses a tile's rows with 32-bit offsets
-    bool big = !xf32 && t == TILE_M128;
+    // the fp16 path's kernel reads each weight row's scales as 16-byte
+    // chunks and addresses a tile's rows with 32-bit offsets
+    bool wide = !xf32 && t == TILE_M128;
     for (int i = 0; i < n; ++i)
-        big = big && ls[i]->K % 64 == 0 && ls[i]->K < ((int64_t)1 << 23) &&
-              aligned(ls[i]->scales, 4);
-    const int bm = big ? big_tile_bm() : tile_bm(t);
-    const int bn = big ? big_tile_bn() : tile_bn(t);
+        wide = wide && ls[i]->K % 256 == 0 && ls[i]->K < ((int64_t)1 << 23) &&
+               aligned(ls[i]->scales, 16);
+    const int bm = wide ? wide_tile_bm() : tile_bm(t);
+    const int bn = wide ? wide_tile_bn() : tile_bn(t);
 
     // longest reduction first, so the long tiles start early
     const ql_linear *ord[QL_MAX_GROUP];
@@ -141,13 +141,13 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
-    if (!big)
+    if (!wide)
         return launch_qgemm(ord[0]->fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
 
-    // fp16 path: one exact, row-shifted fp16 copy per distinct activation
+    // Workspace: one exact, row-shifted fp16 copy per distinct activation
     // tensor (layers reading the same X share it)
     int src[QL_MAX_GROUP];
-    size_t off[QL_MAX_GROUP], bytes = 0;
+    size_t xoff[QL_MAX_GROUP], bytes = 0;
     for (int i = 0; i < n; ++i) {
         src[i] = i;
         for (int j = 0; j < i; ++j)
@@ -156,7 +156,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
                 break;
             }
         if (src[i] == i) {
-            off[i] = bytes;
+            xoff[i] = bytes;
             bytes += round256((size_t)a.d[i].M * a.d[i].K * 2) + round256((size_t)a.d[i].M * 4);
         }
     }
@@ -166,6 +166,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     void *ws = nullptr;
     if (hipMallocFromPoolAsync(&ws, bytes, pool, stream) != hipSuccess)
         return QL_ERR_HIP;
+    uint8_t *const wsb = (uint8_t *)ws;
     hipError_t e = hipSuccess;
     const void *xs[QL_MAX_GROUP];
     const int *es[QL_MAX_GROUP];
@@ -175,9 +176,8 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             es[i] = es[src[i]];
             continue;
         }
-        uint8_t *base = (uint8_t *)ws + off[i];
-        uint16_t *xh = (uint16_t *)base;
-        int *ex = (int *)(base + round256((size_t)a.d[i].M * a.d[i].K * 2));
+        uint16_t *xh = (uint16_t *)(wsb + xoff[i]);
+        int *ex = (int *)(wsb + xoff[i] + round256((size_t)a.d[i].M * a.d[i].K * 2));
         if (e == hipSuccess)
             e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, xh, ex, stream);
         xs[i] = xh;
@@ -188,7 +188,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         a.d[i].xexp = es[i];
     }
     if (e == hipSuccess)
-        e = launch_qgemm_big(ord[0]->fmt, true, a, stream);
+        e = launch_qgemm_wide(ord[0]->fmt, a, stream);
     const hipError_t ef = hipFreeAsync(ws, stream);
     return e == hipSuccess && ef == hipSuccess ? QL_OK : QL_ERR_HIP;
 }

@@ -132,7 +132,22 @@ def test_forward_ragged(gpu, orc, fmt, xdt, N, K):
         assert e <= TOL[xdt], (M, N, K, e)
 
 
-@pytest.mark.parametrize("K", [4096, 16384, 16448])
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_large_m_ragged_tiles(gpu, orc, fmt):
+    """The large-M bf16 path (M > 64, K % 256 == 0) at row and column counts
+    that leave partial 128 x 256 tiles, several K steps (odd and even ring
+    positions) and one-step K."""
+    for (M, N, K) in ((65, 200, 512), (130, 256, 768), (257, 300, 256), (300, 520, 1280),
+                      (129, 17, 1024)):
+        W, X = si.small_case(70 + M + N + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        e = rel_err(Yg, Yr)
+        assert e <= TOL[O.DT_BF16], (M, N, K, e)
+
+
+@pytest.mark.parametrize("K", [4096, 16384, 16640])
 def test_forward_long_rows(gpu, orc, K):
     """Large-M bf16 path at reduction lengths that exercise every row width
     of the activation pre-pass (held in registers up to K = 16384, two reads
