@@ -60,15 +60,19 @@ struct Geo {
     static constexpr int XBYTES = BM * 64 * 2;                 // activations per stage
     static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : 32;  // code bytes per row per stage
     static constexpr int CBYTES = BN * CROW;
-    static constexpr int SBYTES = BN * 4;                      // both scales of a step, per row
-    static constexpr int STAGE = XBYTES + CBYTES + SBYTES;
+    static constexpr int STAGE = XBYTES + CBYTES;
+    // scales travel apart: one 16-byte chunk (8 blocks = 4 steps) per weight
+    // row every 4 steps, into a 2-slot ring; a per-step load would cost one
+    // memory request per row for 4 bytes
+    static constexpr int SGROUP = 4, SSLOT = BN * 16;
     static constexpr int XLOADS = XBYTES / 16 / 256;
     static constexpr int CLOADS = CBYTES / 16 / 256;
-    static constexpr int LOADS = XLOADS + CLOADS + 1;          // direct-to-LDS loads per stage
+    static constexpr int LOADS = XLOADS + CLOADS;  // direct-to-LDS loads per step (+1 every 4)
+    static constexpr int LDS = NST * STAGE + 2 * SSLOT;
     static_assert(XBYTES % (16 * 256) == 0 && CBYTES % (16 * 256) == 0,
                   "every thread issues the same number of 16-byte loads per stage");
-    static_assert(BN == 256, "one scale dword per weight row per thread");
-    static_assert(2 * NST * STAGE <= 160 * 1024, "two workgroups per CU");
+    static_assert(BN == 256, "one scale chunk per weight row per thread");
+    static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
 };
 
 __device__ inline constexpr int vmcnt_imm(int v)
@@ -99,14 +103,6 @@ __device__ inline uint64_t sbase(const void *p)
 __device__ inline void dma16(const void *base, uint32_t off, uint32_t lds)
 {
     asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(off), "s"(sbase(base)), "s"(__builtin_amdgcn_readfirstlane(lds))
-                 : "memory");
-}
-
-__device__ inline void dma4(const void *base, uint32_t off, uint32_t lds)
-{
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
                  :
                  : "v"(off), "s"(sbase(base)), "s"(__builtin_amdgcn_readfirstlane(lds))
                  : "memory");
@@ -174,11 +170,13 @@ struct Ctx {
     const uint8_t *xbase, *cbase, *sbase;
     // per-lane byte offsets from those bases, fixed for the whole K loop
     uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff;
+    uint8_t *sring;  // the scale ring (2 slots of BN rows x 16 bytes)
     int wave, l16, lg;
     int f[NSUB];  // weight row (wave * 64 + j * 16 + l16) enters as W * 2^f[j]
 };
 
-// Issue the direct-to-LDS loads of step s into one ring stage.
+// Issue the direct-to-LDS loads of step s into one ring stage (and, every
+// SGROUP steps, the scales of steps s .. s + 3 into their ring slot).
 template <int FMT>
 __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
 {
@@ -186,14 +184,17 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
     const uint32_t base = lds_addr(stage);
     const uint8_t *xb = c.xbase + s * 128;  // 64 fp16 per row per step
     const uint8_t *cb = c.cbase + s * G::CROW;
-    const uint8_t *sb = c.sbase + s * 4;
 #pragma unroll
     for (int r = 0; r < G::XLOADS; ++r)
         dma16(xb, c.xoff[r], base + (r * 256 + c.wave * 64) * 16);
 #pragma unroll
     for (int r = 0; r < G::CLOADS; ++r)
         dma16(cb, c.coff[r], base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
-    dma4(sb, c.soff, base + G::XBYTES + G::CBYTES + c.wave * 256);
+    if (s % G::SGROUP == 0) {
+        const int g = s / G::SGROUP;
+        dma16(c.sbase + g * 16, c.soff,
+              lds_addr(c.sring + (g & 1) * G::SSLOT) + c.wave * 64 * 16);
+    }
 }
 
 // fp16 pair {s * 2^f, s * 2^f} for the scale in the low half of v
@@ -204,15 +205,16 @@ __device__ inline half2v scaled_pair(uint32_t v, int f)
 }
 
 template <int FMT>
-__device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage,
+__device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, int s,
                                      f32x4 (&acc)[MSUB][NSUB])
 {
     using G = Geo<FMT>;
+    // scales of blocks 2s, 2s+1: dword s % 4 of the row's chunk in slot (s / 4) & 1
+    const uint8_t *ss = c.sring + ((s / G::SGROUP) & 1) * G::SSLOT + (s % G::SGROUP) * 4;
     uint32_t sc[NSUB];
 #pragma unroll
     for (int j = 0; j < NSUB; ++j)
-        sc[j] = *reinterpret_cast<const uint32_t *>(stage + G::XBYTES + G::CBYTES +
-                                                    (c.wave * 64 + j * 16 + c.l16) * 4);
+        sc[j] = *reinterpret_cast<const uint32_t *>(ss + (c.wave * 64 + j * 16 + c.l16) * 16);
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi) {
         u32x4 B[NSUB];
@@ -248,7 +250,7 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
 {
     using G = Geo<FMT>;
     constexpr int NST = G::NST, PD = NST - 1;  // prefetch distance in steps
-    __shared__ __align__(16) uint8_t ring[NST * G::STAGE];
+    __shared__ __align__(16) uint8_t ring[G::LDS];
 
     // workgroup p belongs to the layer whose tile range holds p, so every
     // layer (long reductions first) is spread over all 8 XCDs; within the
@@ -310,8 +312,9 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         const int n = min(n0 + row, N - 1) - n0;
         c.coff[r] = (uint32_t)(n * crow_bytes + ch * 16);
     }
-    // scales: one dword (blocks 2s, 2s+1) of weight row tid per step
+    // scales: one 16-byte chunk of weight row tid per 4 steps
     c.soff = (uint32_t)((min(n0 + tid, N - 1) - n0) * nb * 2);
+    c.sring = ring + NST * G::STAGE;
 
     const int ns = nb >> 1;  // steps of 64 k
 #pragma unroll
@@ -358,7 +361,11 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
     int slot = 0;
 #pragma unroll 1
     for (int s = 0; s < ns; ++s) {
-        if (PD == 2 && s + 1 < ns)
+        // stage s+1's loads (one more when it starts a scale group) may
+        // remain in flight
+        if (PD == 2 && s + 1 < ns && (s + 1) % G::SGROUP == 0)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS + 1));
+        else if (PD == 2 && s + 1 < ns)
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS));
         else
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
@@ -366,7 +373,7 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         const int fill = slot + PD >= NST ? slot + PD - NST : slot + PD;
         if (s + PD < ns)
             issue_stage<FMT>(c, ring + fill * G::STAGE, s + PD);
-        compute_stage<FMT>(c, ring + slot * G::STAGE, acc);
+        compute_stage<FMT>(c, ring + slot * G::STAGE, s, acc);
         slot = slot + 1 == NST ? 0 : slot + 1;
     }
 
