@@ -57,4 +57,10 @@ hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
 int skinny_max_m();
 hipError_t launch_qgemm_skinny(int fmt, const LinDesc &d, hipStream_t stream);
 
+// Weight-streaming kernel for M <= stream_max_m() (bf16 activations): whole
+// cache lines via direct-to-LDS loads; K % 256 == 0 and 16-byte aligned
+// scales.
+int stream_max_m();
+hipError_t launch_qgemm_stream(int fmt, const LinDesc &d, hipStream_t stream);
+
 }  // namespace qlk

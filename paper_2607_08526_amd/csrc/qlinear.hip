@@ -97,7 +97,10 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             d.M = (int)ls[i]->M;
             d.N = (int)ls[i]->N;
             d.K = (int)ls[i]->K;
-            if (launch_qgemm_skinny(ls[i]->fmt, d, stream) != hipSuccess)
+            const bool stream_ok = d.M <= stream_max_m() && d.K % 256 == 0 &&
+                                   aligned(d.scales, 16);
+            if ((stream_ok ? launch_qgemm_stream(ls[i]->fmt, d, stream)
+                           : launch_qgemm_skinny(ls[i]->fmt, d, stream)) != hipSuccess)
                 return QL_ERR_HIP;
         }
         return QL_OK;

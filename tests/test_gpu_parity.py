@@ -147,6 +147,24 @@ def test_forward_large_m_ragged_tiles(gpu, orc, fmt):
         assert e <= TOL[O.DT_BF16], (M, N, K, e)
 
 
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_streaming_ragged(gpu, orc, fmt):
+    """The weight-streaming path (M <= 16, K % 256 == 0): row counts around
+    its 8- and 16-row workgroups and the narrow/wide switch, K lengths that
+    leave some wavefronts short or empty and that cross the 32-block scale
+    runs, every M up to 16."""
+    cases = [(1, 1, 256), (2, 7, 512), (3, 9, 768), (4, 16, 2304), (5, 17, 256),
+             (8, 100, 1280), (15, 300, 2048), (16, 4100, 512), (16, 4111, 1024),
+             (1, 5000, 8448), (9, 4096, 256)]
+    for M, N, K in cases:
+        W, X = si.small_case(80 + M + N + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        e = rel_err(Yg, Yr)
+        assert e <= TOL[O.DT_BF16], (M, N, K, e)
+
+
 @pytest.mark.parametrize("K", [4096, 16384, 16640])
 def test_forward_long_rows(gpu, orc, K):
     """Large-M bf16 path at reduction lengths that exercise every row width
