@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-sweeps", action="store_true", help="time the step only")
+    ap.add_argument("--sweeps-only", action="store_true",
+                    help="run the skinny-M sweep and the int8 block only (no step, no JSON line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle's timed sample")
@@ -363,6 +365,11 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         del a, b
+
+    if args.sweeps_only:
+        print(json.dumps({"skinny": skinny_sweep(torch, ql, si),
+                          "block_int8": block_int8(torch, ql, si)}), flush=True)
+        return
 
     step = Step(torch, ql, si, keep_host_block0=not args.no_cpu_baseline)
     total_ms, launch_ms, wall = time_step(torch, step, args.steps, args.warmup)

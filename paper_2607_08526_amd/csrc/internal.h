@@ -19,6 +19,14 @@ struct LinDesc {
     int tiles_m, tiles_n;
     int tile_begin;  // first logical tile of this layer in a grouped launch
     const int *xexp; // fp16 path: per-row power-of-two shift of X (see xprep.hip)
+    // fp16 path, split reduction: each output tile is computed as ksplit
+    // (<= wide_max_split()) parts of psteps 64-k steps each; parts store
+    // fp32 partial tiles in part[tiles][ksplit][BM * BN] and count arrivals
+    // in cnt[tiles_m * tiles_n] (zero before the launch); the last part to
+    // arrive sums them in part order.  ksplit == 1: no workspace.
+    int ksplit, psteps;
+    float *part;
+    int *cnt;
 };
 
 struct GroupArgs {
@@ -46,11 +54,14 @@ hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
 // 16-byte aligned scales.
 int wide_tile_bm();
 int wide_tile_bn();
+int wide_max_split();
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
-// bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M].
-hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
-                        hipStream_t stream);
+// bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M];
+// also sets zero[0 .. nzero) to 0 (the split counters of the launch that
+// follows on the same stream).
+hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp, int *zero,
+                        int nzero, hipStream_t stream);
 
 // Few-row kernel (bf16 activations, M <= skinny_max_m()): one layer per
 // launch, workgroups of 16 weight rows with K split over their wavefronts.

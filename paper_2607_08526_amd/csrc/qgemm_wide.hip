@@ -53,6 +53,7 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
 constexpr int MSUB = 8, NSUB = 4, BM = 16 * MSUB, BN = 64 * NSUB, GROUP_M = 4;
+constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
 
 template <int FMT>
 struct Geo {
@@ -155,6 +156,34 @@ __device__ inline u32x4 deq_q4(uint32_t c, half2v sp)
     r[2] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C060C02u) & 0x000F000Fu) | 0x64006400u, bias, sp);
     r[3] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C070C03u) & 0x000F000Fu) | 0x64006400u, bias, sp);
     return r;
+}
+
+// 16-byte store / load at device coherence (write-through to, and read
+// from, the level shared by all XCDs)
+__device__ inline void st_coherent(float *p, f32x4 v)
+{
+    asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+
+__device__ inline f32x4 ld_coherent(const float *p)
+{
+    f32x4 v;
+    asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+    return v;
+}
+
+// wait for every load issued above; the values pass through the statement so
+// that no use can be scheduled before it
+template <int A, int B>
+__device__ inline void wait_loads(f32x4 (&v)[A][B])
+{
+    static_assert(A * B == 12, "operand list below");
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]),
+                   "+v"(v[1][0]), "+v"(v[1][1]), "+v"(v[1][2]), "+v"(v[1][3]),
+                   "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3])
+                 :
+                 : "memory");
 }
 
 __device__ inline int logical_tile(int p, int G)
@@ -265,12 +294,15 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         if (t < args.n && p < args.d[t].tile_begin && end == args.total_tiles)
             end = args.d[t].tile_begin;
     }
+    // the ksplit parts of one output tile are adjacent (same XCD)
     const int local = logical_tile(p - d.tile_begin, end - d.tile_begin);
+    const int S = d.ksplit;
+    const int tile = local / S, part = local - tile * S;
     const int per_group = GROUP_M * d.tiles_n;
-    const int gid = local / per_group;
+    const int gid = tile / per_group;
     const int first_m = gid * GROUP_M;
     const int gsz = min(d.tiles_m - first_m, GROUP_M);
-    const int within = local - gid * per_group;
+    const int within = tile - gid * per_group;
     const int tm = first_m + within % gsz;
     const int tn = within / gsz;
 
@@ -316,7 +348,13 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
     c.soff = (uint32_t)((min(n0 + tid, N - 1) - n0) * nb * 2);
     c.sring = ring + NST * G::STAGE;
 
-    const int ns = nb >> 1;  // steps of 64 k
+    // this part's steps of 64 k: [s0, s0 + ns); s0 is a multiple of the
+    // scale group (psteps % 4 == 0, checked by the host)
+    const int s0 = part * d.psteps;
+    const int ns = min(nb >> 1, s0 + d.psteps) - s0;
+    c.xbase += s0 * 128;
+    c.cbase += s0 * G::CROW;
+    c.sbase += s0 / G::SGROUP * 16;
 #pragma unroll
     for (int q = 0; q < PD; ++q)
         if (q < ns)
@@ -377,6 +415,72 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         slot = slot + 1 == NST ? 0 : slot + 1;
     }
 
+    // back to the scale of X * W^T (exact power-of-two factors)
+#pragma unroll
+    for (int i = 0; i < MSUB; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = min(m0 + i * 16 + c.lg * 4 + r, M - 1);
+            const int e = d.xexp[m];
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j)
+                acc[i][j][r] = __builtin_amdgcn_ldexpf(acc[i][j][r], e - c.f[j]);
+        }
+
+    if (S > 1) {
+        // Split reduction: publish this part's partial tile, count the
+        // arrival; the last part to arrive adds all partials in part order
+        // (the same sum whichever part finishes last).  A partial tile is
+        // stored thread-major (each thread's 16-byte accumulator groups,
+        // consecutive across the wavefront) with device-coherent
+        // write-through stores and read back with device-coherent loads (the
+        // parts of a tile may run on different XCDs, whose L2s are not
+        // coherent); the stores are complete (s_waitcnt vmcnt(0)) before the
+        // arrival is counted.  A release/acquire fence pair would instead
+        // write back and invalidate each XCD's whole L2.
+        float *const tp = d.part + (int64_t)tile * S * (BM * BN);
+        float *const mine = tp + (int64_t)part * (BM * BN);
+#pragma unroll
+        for (int i = 0; i < MSUB; ++i)
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j)
+                st_coherent(mine + ((i * NSUB + j) * 256 + tid) * 4, acc[i][j]);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();  // the tile's stores are complete; the ring is no longer read
+        int *const flag = reinterpret_cast<int *>(ring);
+        if (tid == 0)
+            *flag = __hip_atomic_fetch_add(d.cnt + tile, 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        if (*flag != S - 1)
+            return;
+#pragma unroll
+        for (int i = 0; i < MSUB; ++i) {
+            // the other parts' groups of row block i, all in flight at once
+            f32x4 v[MAXSPLIT - 1][NSUB];
+#pragma unroll
+            for (int q = 0; q < MAXSPLIT - 1; ++q) {
+                const int qq = q < part ? q : q + 1;
+#pragma unroll
+                for (int j = 0; j < NSUB; ++j)
+                    if (qq < S)
+                        v[q][j] = ld_coherent(tp + (int64_t)qq * (BM * BN) +
+                                              ((i * NSUB + j) * 256 + tid) * 4);
+            }
+            wait_loads(v);
+#pragma unroll
+            for (int j = 0; j < NSUB; ++j) {
+                f32x4 y = part == 0 ? acc[i][j] : v[0][j];
+#pragma unroll
+                for (int q = 1; q < MAXSPLIT; ++q)
+                    if (q < S)
+                        y += q == part ? acc[i][j] : v[q < part ? q : q - 1][j];
+                acc[i][j] = y;
+            }
+        }
+        // fall through: the summed tile is stored like an unsplit one
+    }
+
 #pragma unroll
     for (int i = 0; i < MSUB; ++i)
 #pragma unroll
@@ -384,12 +488,11 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
             const int m = m0 + i * 16 + c.lg * 4 + r;
             if (m >= M)
                 continue;
-            const int e = d.xexp[m];
 #pragma unroll
             for (int j = 0; j < NSUB; ++j) {
                 const int n = n0 + c.wave * 64 + j * 16 + c.l16;
                 if (n < N)
-                    d.Y[(int64_t)m * N + n] = __builtin_amdgcn_ldexpf(acc[i][j][r], e - c.f[j]);
+                    d.Y[(int64_t)m * N + n] = acc[i][j][r];
             }
         }
 }
@@ -398,6 +501,7 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
 
 int wide_tile_bm() { return BM; }
 int wide_tile_bn() { return BN; }
+int wide_max_split() { return MAXSPLIT; }
 
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
 {

@@ -2,7 +2,10 @@
 // argument checks, tile-shape choice and launch.  Every check happens before
 // anything is enqueued; no entry point throws or aborts.
 #include <algorithm>
+#include <functional>
 #include <mutex>
+#include <queue>
+#include <vector>
 
 #include "internal.h"
 
@@ -65,6 +68,139 @@ hipMemPool_t workspace_pool()
 }
 
 size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+int device_cus()
+{
+    constexpr int MAXDEV = 64;
+    static int cus[MAXDEV] = {};
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV)
+        return 256;
+    if (!cus[dev])
+        cus[dev] = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) ==
+                               hipSuccess && v > 0 ? v : 256;
+    return cus[dev];
+}
+
+// Split plan of a grouped fp16-path launch: how many parts each layer's
+// output tiles are cut into along K.  Tiles of different reduction lengths
+// (FFN-down's K = 4d next to K = d) or too few tiles for the GPU leave most
+// workgroup slots idle at the end of the launch; cutting the long
+// reductions into parts evens that out at the price of a partial-tile round
+// trip per part.  The plan is the one with the shortest estimated makespan
+// under the hardware's dispatch: workgroup p runs on XCD p % 8, each XCD
+// takes a contiguous range of every layer's parts (in layer order) and
+// starts them in order on its first free slot (two workgroups per CU).
+struct SplitPlan {
+    int S[QL_MAX_GROUP], psteps[QL_MAX_GROUP];
+};
+
+constexpr int XCDS = 8;
+constexpr double TILE_OVH = 3.0;   // prologue + epilogue, in 64-k steps
+constexpr double SPLIT_OVH = 2.0;  // partial store / reload per part
+
+double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
+{
+    double worst = 0.0;
+    for (int x = 0; x < XCDS; ++x) {
+        // slot free times, earliest first
+        std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+        for (int k = 0; k < slots; ++k)
+            free_at.push(0.0);
+        for (int i = 0; i < n; ++i) {
+            const int64_t parts = (int64_t)d[i].tiles_m * d[i].tiles_n * pl.S[i];
+            const int64_t q = parts / XCDS, r = parts % XCDS;
+            const int64_t mine = q + (x < r ? 1 : 0);
+            const double len = pl.psteps[i] + TILE_OVH + (pl.S[i] > 1 ? SPLIT_OVH : 0.0);
+            for (int64_t t = 0; t < mine; ++t) {
+                const double end = free_at.top() + len;
+                free_at.pop();
+                free_at.push(end);
+                worst = std::max(worst, end);
+            }
+        }
+    }
+    return worst;
+}
+
+SplitPlan plan_splits(const LinDesc *d, int n)
+{
+    const int slots = std::max(1, 2 * device_cus() / XCDS);
+    SplitPlan best{};
+    double best_t = 0.0;
+    int best_parts = 0;
+    // candidate part lengths: every layer's step count halved repeatedly
+    std::vector<int> cand;
+    for (int i = 0; i < n; ++i)
+        for (int L = d[i].K / 64; L >= 8; L /= 2)
+            cand.push_back(L);
+    cand.push_back(1 << 30);  // no split
+    for (const int L : cand) {
+        SplitPlan pl{};
+        int total_parts = 0;
+        for (int i = 0; i < n; ++i) {
+            const int ns = d[i].K / 64;
+            // parts of a multiple of 4 steps (whole scale chunks), >= 8 steps
+            int ps = ns;
+            if (L < ns) {
+                ps = std::max(8, (L + 3) & ~3);
+                ps = std::min(ps, ns);
+            }
+            pl.psteps[i] = ps;
+            pl.S[i] = (ns + ps - 1) / ps;
+            if (pl.S[i] > wide_max_split()) {
+                const int S = wide_max_split();
+                pl.psteps[i] = ((ns + S - 1) / S + 3) & ~3;
+                pl.S[i] = (ns + pl.psteps[i] - 1) / pl.psteps[i];
+            }
+            total_parts += pl.S[i];
+        }
+        const double t = makespan(d, n, pl, slots);
+        if (best_parts == 0 || t < best_t * 0.98 ||
+            (t <= best_t * 1.02 && total_parts < best_parts)) {
+            best = pl;
+            best_t = t;
+            best_parts = total_parts;
+        }
+    }
+    return best;
+}
+
+// Recently used plans, keyed by the group's shapes (the search above costs
+// tens of microseconds of host time).
+SplitPlan cached_plan(const LinDesc *d, int n)
+{
+    struct Entry {
+        int n, cus;
+        int64_t shape[QL_MAX_GROUP][3];
+        SplitPlan pl;
+    };
+    constexpr int SLOTS = 16;
+    static std::mutex mu;
+    static Entry cache[SLOTS];
+    static int used = 0, next = 0;
+    Entry key{};
+    key.n = n;
+    key.cus = device_cus();
+    for (int i = 0; i < n; ++i) {
+        key.shape[i][0] = d[i].M;
+        key.shape[i][1] = d[i].N;
+        key.shape[i][2] = d[i].K;
+    }
+    {
+        std::lock_guard<std::mutex> g(mu);
+        for (int e = 0; e < used; ++e)
+            if (cache[e].n == n && cache[e].cus == key.cus &&
+                std::equal(&cache[e].shape[0][0], &cache[e].shape[0][0] + 3 * n, &key.shape[0][0]))
+                return cache[e].pl;
+    }
+    key.pl = plan_splits(d, n);
+    std::lock_guard<std::mutex> g(mu);
+    cache[next] = key;
+    next = (next + 1) % SLOTS;
+    used = std::min(used + 1, SLOTS);
+    return key.pl;
+}
 
 TileCfg choose_tile(int64_t M, bool xf32)
 {
@@ -137,8 +273,20 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         d.K = (int)ord[i]->K;
         d.tiles_m = (int)((ord[i]->M + bm - 1) / bm);
         d.tiles_n = (int)((ord[i]->N + bn - 1) / bn);
+        d.ksplit = 1;
+        d.psteps = (int)(ord[i]->K / 64);
+    }
+    SplitPlan pl{};
+    if (wide)
+        pl = cached_plan(a.d, n);
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        if (wide) {
+            d.ksplit = pl.S[i];
+            d.psteps = pl.psteps[i];
+        }
         d.tile_begin = (int)total;
-        total += (int64_t)d.tiles_m * d.tiles_n;
+        total += (int64_t)d.tiles_m * d.tiles_n * d.ksplit;
     }
     if (total >= I31)
         return QL_ERR_UNSUPPORTED;
@@ -163,6 +311,23 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             bytes += round256((size_t)a.d[i].M * a.d[i].K * 2) + round256((size_t)a.d[i].M * 4);
         }
     }
+    // split layers: partial tiles [S][M][N] fp32, then all arrival counters
+    size_t poff[QL_MAX_GROUP], coff[QL_MAX_GROUP];
+    int ncnt = 0;
+    for (int i = 0; i < n; ++i) {
+        if (a.d[i].ksplit == 1)
+            continue;
+        poff[i] = bytes;
+        bytes += round256((size_t)a.d[i].tiles_m * a.d[i].tiles_n * a.d[i].ksplit * bm * bn * 4);
+    }
+    const size_t cnt_off = bytes;
+    for (int i = 0; i < n; ++i) {
+        if (a.d[i].ksplit == 1)
+            continue;
+        coff[i] = cnt_off + (size_t)ncnt * 4;
+        ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
+    }
+    bytes += round256((size_t)ncnt * 4);
     hipMemPool_t pool = workspace_pool();
     if (!pool)
         return QL_ERR_HIP;
@@ -171,6 +336,12 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         return QL_ERR_HIP;
     uint8_t *const wsb = (uint8_t *)ws;
     hipError_t e = hipSuccess;
+    for (int i = 0; i < n; ++i)
+        if (a.d[i].ksplit > 1) {
+            a.d[i].part = (float *)(wsb + poff[i]);
+            a.d[i].cnt = (int *)(wsb + coff[i]);
+        }
+    bool zeroed = false;
     const void *xs[QL_MAX_GROUP];
     const int *es[QL_MAX_GROUP];
     for (int i = 0; i < n; ++i) {
@@ -181,8 +352,11 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         }
         uint16_t *xh = (uint16_t *)(wsb + xoff[i]);
         int *ex = (int *)(wsb + xoff[i] + round256((size_t)a.d[i].M * a.d[i].K * 2));
+        // the first pre-pass also clears the split counters
         if (e == hipSuccess)
-            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, xh, ex, stream);
+            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, xh, ex, (int *)(wsb + cnt_off),
+                             zeroed ? 0 : ncnt, stream);
+        zeroed = true;
         xs[i] = xh;
         es[i] = ex;
     }

@@ -61,9 +61,13 @@ __device__ inline u32x4 to_f16(u32x4 v, int e)
 template <int R>
 __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__ X, int K,
                                                     uint16_t *__restrict__ Xh,
-                                                    int *__restrict__ rexp)
+                                                    int *__restrict__ rexp,
+                                                    int *__restrict__ zero, int nzero)
 {
     const int m = blockIdx.x;
+    if (m == 0)
+        for (int i = threadIdx.x; i < nzero; i += 256)
+            zero[i] = 0;
     const u32x4 *row = reinterpret_cast<const u32x4 *>(X + (int64_t)m * K);
     u32x4 *out = reinterpret_cast<u32x4 *>(Xh + (int64_t)m * K);
     const int n16 = K / 8;
@@ -101,22 +105,22 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
 
 }  // namespace
 
-hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp,
-                        hipStream_t stream)
+hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp, int *zero,
+                        int nzero, hipStream_t stream)
 {
     const uint16_t *x = reinterpret_cast<const uint16_t *>(X);
     const int n16 = K / 8;
     const dim3 grid((unsigned)M), block(256);
     if (n16 <= 256)
-        hipLaunchKernelGGL(xprep_kernel<1>, grid, block, 0, stream, x, K, Xh, rexp);
+        hipLaunchKernelGGL(xprep_kernel<1>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
     else if (n16 <= 512)
-        hipLaunchKernelGGL(xprep_kernel<2>, grid, block, 0, stream, x, K, Xh, rexp);
+        hipLaunchKernelGGL(xprep_kernel<2>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
     else if (n16 <= 1024)
-        hipLaunchKernelGGL(xprep_kernel<4>, grid, block, 0, stream, x, K, Xh, rexp);
+        hipLaunchKernelGGL(xprep_kernel<4>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
     else if (n16 <= 2048)
-        hipLaunchKernelGGL(xprep_kernel<8>, grid, block, 0, stream, x, K, Xh, rexp);
+        hipLaunchKernelGGL(xprep_kernel<8>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
     else
-        hipLaunchKernelGGL(xprep_kernel<0>, grid, block, 0, stream, x, K, Xh, rexp);
+        hipLaunchKernelGGL(xprep_kernel<0>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
     return hipGetLastError();
 }
 

@@ -245,6 +245,40 @@ def test_forward_stored_extreme_codes_exact(gpu, orc, fmt):
         assert np.array_equal(Yg.astype(np.int64), Xi.astype(np.int64) @ C.T)
 
 
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_split_reduction(gpu, orc, fmt):
+    """Large-M shapes with few output tiles and long reductions, which the
+    fp16 path cuts into K parts summed by the last part to arrive: uneven
+    last parts (K / 64 not a multiple of the part length), ragged tiles, a
+    grouped call mixing reduction lengths; results repeat bit for bit."""
+    torch, ql = gpu
+    for (M, N, K) in ((300, 520, 4096), (129, 260, 8448), (2048, 64, 2304)):
+        W, X = si.small_case(90 + M + N + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        assert rel_err(Yg, Yr) <= TOL[O.DT_BF16], (M, N, K)
+        assert np.array_equal(Yg, forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N))
+    # one grouped launch: short and long reductions over two activations
+    M = 384
+    _, xa = si.small_case(95, M, 1, 512)
+    _, xb = si.small_case(96, M, 1, 4096)
+    shapes = [(700, 512), (256, 4096), (1000, 512)]
+    entries, refs = [], []
+    for i, (N, K) in enumerate(shapes):
+        W, _ = si.small_case(97 + i, 1, N, K)
+        cd, sd = ql.quantize(fmt, dev_w(torch, W))
+        cr, sr = orc.quantize(fmt, W)
+        X = xa if K == 512 else xb
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        entries.append((fmt, dev_x(torch, X, O.DT_BF16), cd, sd, N, Y))
+        refs.append(orc.forward(fmt, X, O.DT_BF16, cr, sr, N))
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    for e, Yr in zip(entries, refs):
+        assert rel_err(e[5].cpu().numpy(), Yr) <= TOL[O.DT_BF16]
+
+
 def test_forward_deterministic(gpu, orc):
     torch, ql = gpu
     W, X = si.small_case(5, 300, 520, 1024, O.DT_BF16)
