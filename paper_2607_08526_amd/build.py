@@ -24,17 +24,21 @@ DEVICE_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-fno-gpu-flush-denormals-to-zero", "-fno-fast-math",
-    # MFMA results straight into VGPRs: the per-block scale FMA reads them
-    # without v_accvgpr_read copies
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-command-line-argument",
     f"-I{INCLUDE}",
 ]
+# MFMA results straight into VGPRs: the per-block scale FMAs of these kernels
+# read them without v_accvgpr_read copies.  The large-M fp16 kernel keeps its
+# 256 accumulators per lane in AGPRs instead.
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+SOURCE_FLAGS = {"qgemm.hip": VGPR_FORM, "qgemm_skinny.hip": VGPR_FORM,
+                "qgemm_stream.hip": VGPR_FORM}
 
 
 def _compile(src):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *DEVICE_FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

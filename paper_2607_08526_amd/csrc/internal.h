@@ -55,6 +55,7 @@ hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
 int wide_tile_bm();
 int wide_tile_bn();
 int wide_max_split();
+int wide_wgs_per_cu();  // resident workgroups per CU (LDS and register budget)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
 // bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M];

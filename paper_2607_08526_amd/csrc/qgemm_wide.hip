@@ -8,7 +8,7 @@
 //   X'[m][k] = X[m][k] * 2^-e[m]                       (fp16, exact; xprep.hip)
 //   W'[n][k] = fp16(c[n][k] * fp16(s[n][b] * 2^f[n]))   (one rounding)
 //
-// with the whole K accumulated in fp32 by v_mfma_f32_16x16x32_f16.  f[n] is
+// with the whole K accumulated in fp32 by v_mfma_f32_32x32x16_f16.  f[n] is
 // chosen per weight row from the row's largest scale so that every |W'| is
 // below 2^15: c is made exact in fp16 by a magic-number add (the fp16 bit
 // pattern 0x6400 | u is 1024 + u) and one packed fp16 multiply by the scaled
@@ -16,12 +16,27 @@
 // the accumulators, which is what made the exact per-block form
 // (qgemm.hip: an fp32 FMA per output element per block) bound by VALU issue.
 //
+// Matrix instruction.  On gfx950 the 32 x 32 x 16 fp16 MFMA sustains about
+// twice the flop rate of the 16 x 16 x 32 one (each takes the same issue
+// time, the larger one does twice the work), so the tile is built from it.
+// Its operand layout: lane l holds A[l % 32][8 (l / 32) + e] and
+// B[8 (l / 32) + e][l % 32] for e = 0..7, and accumulator register r of lane
+// l is D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+//
+// k order.  The sum over k does not care which k a given MFMA slot holds, as
+// long as A and B agree.  Within a 64-k step, slot e of lane group g = l / 32
+// in the step's 16-k chunk q holds k = 32 g + 8 q + e.  Then every lane's k
+// over the whole step is one contiguous run of 32 = one scale block: its
+// weight codes for the step are one 16-byte (q4) or 32-byte (int8) LDS read,
+// it needs one scale per weight row per step, and each activation fragment
+// is one 16-byte chunk of the row.
+//
 // Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 256 of Y.  Each
-// wavefront owns a 128 x 64 strip (8 x 4 MFMA subtiles): every dequantized
-// weight fragment feeds 8 MFMAs and every activation fragment 4.  The wide N
-// extent halves the activation traffic per flop against a square tile: the
-// fp16 activations (2 bytes per element, re-read once per column tile) are
-// the larger operand stream next to 4-bit codes.
+// wavefront owns a 128 x 64 strip (4 x 2 MFMA tiles of 32 x 32): every
+// dequantized weight fragment feeds 4 MFMAs and every activation fragment 2.
+// The wide N extent halves the activation traffic per flop against a square
+// tile: the fp16 activations (2 bytes per element, re-read once per column
+// tile) are the larger operand stream next to 4-bit codes.
 //
 // Memory pipeline: activations, codes and scales move from global memory to
 // LDS with the gfx950 direct-to-LDS loads (no VGPRs, no VALU), through a ring
@@ -34,32 +49,43 @@
 // kernel waits for each stage explicitly (s_waitcnt vmcnt, then s_barrier; a
 // __syncthreads() would also drain the ring).  Nothing else here uses M0.
 //
-// LDS layouts are XOR-swizzled at 16-byte granularity so that fragment reads
-// hit distinct banks.  A direct-to-LDS load writes lane t's data to slot
-// base + t, so the swizzle is applied by choosing which global chunk each
-// lane fetches.
+// LDS layouts are XOR-swizzled at 16-byte granularity so that the fragment
+// reads of 8 (32 banks) or 16 (64 banks) consecutive lanes hit distinct
+// banks.  A direct-to-LDS load writes lane t's data to slot base + t, so the
+// swizzle is applied by choosing which global chunk each lane fetches.
 //
 // Tile order: within a layer, groups of 4 row tiles walked row-tile fastest;
 // each of the 8 XCDs takes a contiguous range of one layer's tiles (L2
-// reuse), and every layer of a grouped launch is spread over all XCDs.
+// reuse), and every layer of a grouped launch is spread over all XCDs.  Long
+// reductions may be cut into K parts (ksplit, see the split reduction at the
+// end of the kernel).
 #include "internal.h"
 
 namespace qlk {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
-constexpr int MSUB = 8, NSUB = 4, BM = 16 * MSUB, BN = 64 * NSUB, GROUP_M = 4;
+// MSUB = 8: 256 x 256 tiles, one workgroup (one wavefront per SIMD, 256
+// accumulators per lane) per CU; MSUB = 4: 128 x 256 tiles, two per CU.
+#ifndef QL_WIDE_MSUB
+#define QL_WIDE_MSUB 4
+#endif
+constexpr int MSUB = QL_WIDE_MSUB, NSUB = 2, BM = 32 * MSUB, BN = 4 * 32 * NSUB, GROUP_M = 4;
+constexpr int WGS_PER_CU = MSUB == 8 ? 1 : 2;
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
 
 template <int FMT>
 struct Geo {
-    static constexpr int NST = FMT == QL_FMT_INT8 ? 2 : 3;     // ring depth (LDS budget)
+    // ring depth (LDS budget)
+    static constexpr int NST = WGS_PER_CU == 1 || FMT == QL_FMT_Q4 ? 3 : 2;
     static constexpr int XBYTES = BM * 64 * 2;                 // activations per stage
     static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : 32;  // code bytes per row per stage
+    static constexpr int CCH = CROW / 16;                      // 16-byte chunks per code row
     static constexpr int CBYTES = BN * CROW;
     static constexpr int STAGE = XBYTES + CBYTES;
     // scales travel apart: one 16-byte chunk (8 blocks = 4 steps) per weight
@@ -73,7 +99,7 @@ struct Geo {
     static_assert(XBYTES % (16 * 256) == 0 && CBYTES % (16 * 256) == 0,
                   "every thread issues the same number of 16-byte loads per stage");
     static_assert(BN == 256, "one scale chunk per weight row per thread");
-    static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
+    static_assert(WGS_PER_CU * LDS <= 160 * 1024, "resident workgroups per CU");
 };
 
 __device__ inline constexpr int vmcnt_imm(int v)
@@ -83,10 +109,14 @@ __device__ inline constexpr int vmcnt_imm(int v)
     return (v & 15) | (((v >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
 }
 
-// activation chunk swizzle: the 16 rows one MFMA operand read touches land
-// on distinct banks whether the LDS serves 8 lanes of a 16-byte read per
-// clock from 32 banks or 16 lanes from 64 banks
-__device__ inline int xswz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+// 16-byte chunk swizzles (physical chunk = logical ^ swz(row)); each keeps
+// the reads described above free of bank conflicts for 32 or 64 banks
+__device__ inline int xswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+template <int FMT>
+__device__ inline int cswz(int row)
+{
+    return FMT == QL_FMT_INT8 ? ((row >> 1) ^ (row >> 3)) & 3 : ((row >> 2) ^ (row >> 3)) & 1;
+}
 
 // Direct-to-LDS loads from (wave-uniform base + per-lane 32-bit offset):
 // lane t's data lands at LDS address lds + t * size.
@@ -115,9 +145,9 @@ __device__ inline uint32_t lds_addr(const void *p)
     return (uint32_t)(uintptr_t)p;
 }
 
-__device__ inline f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c)
+__device__ inline f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c)
 {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, a),
                                                   __builtin_bit_cast(half8, b), c, 0, 0, 0);
 }
 
@@ -159,10 +189,13 @@ __device__ inline u32x4 deq_q4(uint32_t c, half2v sp)
 }
 
 // 16-byte store / load at device coherence (write-through to, and read
-// from, the level shared by all XCDs)
+// from, the level shared by all XCDs).  A store of more than 8 bytes keeps
+// reading its data registers for a cycle after issue; the compiler's hazard
+// check does not look inside inline asm, so the wait state that keeps the
+// next VALU write from those registers back is part of the statement.
 __device__ inline void st_coherent(float *p, f32x4 v)
 {
-    asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+    asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" : : "v"(p), "v"(v) : "memory");
 }
 
 __device__ inline f32x4 ld_coherent(const float *p)
@@ -200,8 +233,8 @@ struct Ctx {
     // per-lane byte offsets from those bases, fixed for the whole K loop
     uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff;
     uint8_t *sring;  // the scale ring (2 slots of BN rows x 16 bytes)
-    int wave, l16, lg;
-    int f[NSUB];  // weight row (wave * 64 + j * 16 + l16) enters as W * 2^f[j]
+    int wave, l32, g;
+    int f[NSUB];  // weight row (wave * 64 + j * 32 + l32) enters as W * 2^f[j]
 };
 
 // Issue the direct-to-LDS loads of step s into one ring stage (and, every
@@ -226,56 +259,108 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
     }
 }
 
-// fp16 pair {s * 2^f, s * 2^f} for the scale in the low half of v
-__device__ inline half2v scaled_pair(uint32_t v, int f)
+// fp16 pair {s * 2^f, s * 2^f} for the scale bits b
+__device__ inline half2v scaled_pair(uint32_t b, int f)
 {
-    const _Float16 s = __builtin_amdgcn_ldexph(__builtin_bit_cast(_Float16, (uint16_t)v), f);
+    const _Float16 s = __builtin_amdgcn_ldexph(__builtin_bit_cast(_Float16, (uint16_t)b), f);
     return half2v{s, s};
 }
 
+// Word w (two fp16 weights) of weight fragment (chunk q) from the lane's raw
+// codes of the step; the same conversion as deq_q4 / deq_int8, one word at a
+// time so that it can be spread between MFMAs.
+template <int FMT>
+__device__ inline uint32_t deq_word(const uint32_t *raw, int q, int w, half2v sp)
+{
+    if constexpr (FMT == QL_FMT_INT8) {
+        const uint32_t x = raw[2 * q + (w >> 1)] ^ 0x80808080u;
+        const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
+        return h2mul_add(__builtin_amdgcn_perm(0x64646464u, x, (w & 1) ? 0x04030402u : 0x04010400u),
+                         bias, sp);
+    } else {
+        const uint32_t x = raw[q] ^ 0x88888888u, y = x >> 4;
+        constexpr uint32_t sel[4] = {0x0C040C00u, 0x0C050C01u, 0x0C060C02u, 0x0C070C03u};
+        const half2v bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
+        return h2mul_add((__builtin_amdgcn_perm(y, x, sel[w]) & 0x000F000Fu) | 0x64006400u, bias,
+                         sp);
+    }
+}
+
+// One 64-k step.  Per weight fragment j the lane reads its 32 codes (one
+// block) and its block's scale once.  Per 16-k chunk q the wavefront issues
+// 4 x 2 MFMAs; behind each MFMA, in a group the compiler may not reorder,
+// go one word of the next chunk's weight dequantization and (every other
+// MFMA) one of the next chunk's activation fragment reads, so that the
+// matrix core runs while the VALU and LDS prepare the next operands.
 template <int FMT>
 __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, int s,
-                                     f32x4 (&acc)[MSUB][NSUB])
+                                     f32x16 (&acc)[MSUB][NSUB])
 {
     using G = Geo<FMT>;
-    // scales of blocks 2s, 2s+1: dword s % 4 of the row's chunk in slot (s / 4) & 1
-    const uint8_t *ss = c.sring + ((s / G::SGROUP) & 1) * G::SSLOT + (s % G::SGROUP) * 4;
-    uint32_t sc[NSUB];
+    // scale of block 2s + g: half g of dword s % 4 of the row's chunk, slot (s / 4) & 1
+    const uint8_t *ss =
+        c.sring + ((s / G::SGROUP) & 1) * G::SSLOT + (s % G::SGROUP) * 4 + c.g * 2;
+    half2v sp[NSUB];
+    uint32_t raw[NSUB][G::CCH / 2 * 4];
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j) {
+        const int row = c.wave * 64 + j * 32 + c.l32;
+        sp[j] = scaled_pair(*reinterpret_cast<const uint16_t *>(ss + row * 16), c.f[j]);
+#pragma unroll
+        for (int h = 0; h < G::CCH / 2; ++h) {
+            const int lc = c.g * (G::CCH / 2) + h;
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(
+                stage + G::XBYTES + (row * G::CCH + (lc ^ cswz<FMT>(row))) * 16);
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                raw[j][h * 4 + w] = v[w];
+        }
+    }
+    auto read_a = [&](int q, int i) {
+        const int row = i * 32 + c.l32;
+        const int lc = c.g * 4 + q;
+        return *reinterpret_cast<const u32x4 *>(stage + (row * 8 + (lc ^ xswz(row))) * 16);
+    };
+    u32x4 a[MSUB], B[NSUB];
+#pragma unroll
+    for (int i = 0; i < MSUB; ++i)
+        a[i] = read_a(0, i);
 #pragma unroll
     for (int j = 0; j < NSUB; ++j)
-        sc[j] = *reinterpret_cast<const uint32_t *>(ss + (c.wave * 64 + j * 16 + c.l16) * 16);
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
-        u32x4 B[NSUB];
+        for (int w = 0; w < 4; ++w)
+            B[j][w] = deq_word<FMT>(raw[j], 0, w, sp[j]);
 #pragma unroll
-        for (int j = 0; j < NSUB; ++j) {
-            const int row = c.wave * 64 + j * 16 + c.l16;
-            const half2v sp = scaled_pair(sc[j] >> (16 * bi), c.f[j]);
-            if (FMT == QL_FMT_INT8) {
-                const int ch = (bi * 2 + (c.lg >> 1)) ^ ((row >> 2) & 3);
-                const uint2 v = *reinterpret_cast<const uint2 *>(
-                    stage + G::XBYTES + row * 64 + ch * 16 + (c.lg & 1) * 8);
-                B[j] = deq_int8(v.x, v.y, sp);
-            } else {
-                const int ch = bi ^ ((row >> 3) & 1);
-                const uint32_t v = *reinterpret_cast<const uint32_t *>(
-                    stage + G::XBYTES + row * 32 + ch * 16 + c.lg * 4);
-                B[j] = deq_q4(v, sp);
+    for (int q = 0; q < 4; ++q) {
+        u32x4 an[MSUB], Bn[NSUB];
+#pragma unroll
+        for (int k = 0; k < MSUB * NSUB; ++k) {
+            const int i = k / NSUB, j = k % NSUB;
+            acc[i][j] = mfma32(a[i], B[j], acc[i][j]);
+            if (q < 3) {
+                // MSUB reads and 4 NSUB words per MSUB * NSUB MFMAs
+                if (k % NSUB == 0)
+                    an[k / NSUB] = read_a(q + 1, k / NSUB);
+                if ((k + 1) * 4 % MSUB == 0) {
+                    const int wd = (k + 1) * 4 / MSUB - 1, jn = wd / 4, w = wd % 4;
+                    Bn[jn][w] = deq_word<FMT>(raw[jn], q + 1, w, sp[jn]);
+                }
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
+        if (q < 3) {
 #pragma unroll
-        for (int i = 0; i < MSUB; ++i) {
-            const int slot = bi * 512 + (i * 16 + c.l16) * 4 + (c.lg ^ xswz(c.l16));
-            const u32x4 a = *reinterpret_cast<const u32x4 *>(stage + slot * 16);
+            for (int i = 0; i < MSUB; ++i)
+                a[i] = an[i];
 #pragma unroll
             for (int j = 0; j < NSUB; ++j)
-                acc[i][j] = mfma_f16(a, B[j], acc[i][j]);
+                B[j] = Bn[j];
         }
     }
 }
 
 template <int FMT>
-__global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args)
+__global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
     constexpr int NST = G::NST, PD = NST - 1;  // prefetch distance in steps
@@ -313,36 +398,30 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
 
     Ctx<FMT> c;
     c.wave = tid >> 6;
-    c.l16 = tid & 15;
-    c.lg = (tid & 63) >> 4;
+    c.l32 = tid & 31;
+    c.g = (tid & 63) >> 5;
     c.xbase = reinterpret_cast<const uint8_t *>(d.X) + (int64_t)m0 * K * 2;
     c.cbase = d.codes + (int64_t)n0 * crow_bytes;
     c.sbase = reinterpret_cast<const uint8_t *>(d.scales) + (int64_t)n0 * nb * 2;
-    // activations: stage slot = bi*512 + row*4 + (g ^ swz(row)); rows past M
+    // activations: stage slot = row * 8 + (chunk ^ xswz(row)); rows past M
     // repeat the last row (their outputs are never stored)
 #pragma unroll
     for (int r = 0; r < G::XLOADS; ++r) {
         const int slot = r * 256 + tid;
-        const int bi = slot >> 9, rem = slot & 511, row = rem >> 2;
-        const int g = (rem & 3) ^ xswz(row);
+        const int row = slot >> 3;
+        const int lc = (slot & 7) ^ xswz(row);
         const int m = min(m0 + row, M - 1) - m0;
-        c.xoff[r] = (uint32_t)(m * K * 2 + bi * 64 + g * 16);
+        c.xoff[r] = (uint32_t)(m * K * 2 + lc * 16);
     }
-    // codes: stage slot = row*(CROW/16) + (chunk ^ swz(row)); rows past N
+    // codes: stage slot = row * CCH + (chunk ^ cswz(row)); rows past N
     // repeat the last row
 #pragma unroll
     for (int r = 0; r < G::CLOADS; ++r) {
         const int slot = r * 256 + tid;
-        int row, ch;
-        if (FMT == QL_FMT_INT8) {
-            row = slot >> 2;
-            ch = (slot & 3) ^ ((row >> 2) & 3);
-        } else {
-            row = slot >> 1;
-            ch = (slot & 1) ^ ((row >> 3) & 1);
-        }
+        const int row = slot / G::CCH;
+        const int lc = (slot % G::CCH) ^ cswz<FMT>(row);
         const int n = min(n0 + row, N - 1) - n0;
-        c.coff[r] = (uint32_t)(n * crow_bytes + ch * 16);
+        c.coff[r] = (uint32_t)(n * crow_bytes + lc * 16);
     }
     // scales: one 16-byte chunk of weight row tid per 4 steps
     c.soff = (uint32_t)((min(n0 + tid, N - 1) - n0) * nb * 2);
@@ -361,22 +440,21 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
             issue_stage<FMT>(c, ring + q * G::STAGE, q);
 
     // Row shifts, behind the first stages so their latency overlaps: lane
-    // (l16, lg) scans a quarter of the scales of each of its NSUB weight rows
-    // (16-byte chunks lg, lg + 4, ...; K % 256 == 0 and 16-byte aligned
-    // scales, checked by the host); the four quarters are then combined.
-    // fp16 bit patterns of non-negative values order as integers.
+    // (l32, g) scans half of the scales of each of its NSUB weight rows
+    // (16-byte chunks g, g + 2, ...; K % 256 == 0 and 16-byte aligned scales,
+    // checked by the host); the two halves are then combined.  fp16 bit
+    // patterns of non-negative values order as integers.
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
-        const int n = min(n0 + c.wave * 64 + j * 16 + c.l16, N - 1);
+        const int n = min(n0 + c.wave * 64 + j * 32 + c.l32, N - 1);
         const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
         uint32_t mx = 0;
-        for (int q = c.lg; q < nb / 8; q += 4) {
+        for (int q = c.g; q < nb / 8; q += 2) {
             const u32x4 v = srow[q];
 #pragma unroll
             for (int t = 0; t < 4; ++t)
                 mx = max(mx, max(v[t] & 0x7FFFu, (v[t] >> 16) & 0x7FFFu));
         }
-        mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16));
         mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
         const float smax = (float)__builtin_bit_cast(_Float16, (uint16_t)mx);
         int E = 0;
@@ -384,12 +462,14 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         c.f[j] = mx ? 15 - E : 0;  // Q * smax * 2^f in [2^14, 2^15)
     }
 
-    f32x4 acc[MSUB][NSUB];
+    f32x16 acc[MSUB][NSUB];
 #pragma unroll
     for (int i = 0; i < MSUB; ++i)
 #pragma unroll
         for (int j = 0; j < NSUB; ++j)
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][j][r] = 0.f;
 
     // one step: wait for stage s (loads complete in issue order, so allowing
     // the loads of the younger stages already issued to remain outstanding
@@ -415,17 +495,44 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         slot = slot + 1 == NST ? 0 : slot + 1;
     }
 
-    // back to the scale of X * W^T (exact power-of-two factors)
+    // Epilogue.  Register r of tile (i, j) is row i * 32 + 8 (r / 4) + 4 g +
+    // r % 4, column wave * 64 + j * 32 + l32 of the tile; it returns to the
+    // scale of X * W^T by the exact factor 2^(e[m] - f[n]).  Values are taken
+    // from the accumulators as they are stored (no second copy of the tile
+    // in registers).
+    // The tile's row shifts go through LDS (after every wavefront is done
+    // with the ring): 4 consecutive rows per 16-byte read.
+    auto row_of = [&](int i, int r) { return m0 + i * 32 + 8 * (r >> 2) + 4 * c.g + (r & 3); };
+    int *const rowexp = reinterpret_cast<int *>(ring + 256);
+    __syncthreads();
+    for (int t = tid; t < BM; t += 256)
+        rowexp[t] = d.xexp[min(m0 + t, M - 1)];
+    __syncthreads();
+    auto shifts = [&](int i, int (&ex)[16]) {
 #pragma unroll
-    for (int i = 0; i < MSUB; ++i)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = min(m0 + i * 16 + c.lg * 4 + r, M - 1);
-            const int e = d.xexp[m];
-#pragma unroll
-            for (int j = 0; j < NSUB; ++j)
-                acc[i][j][r] = __builtin_amdgcn_ldexpf(acc[i][j][r], e - c.f[j]);
+        for (int b = 0; b < 4; ++b) {
+            const int4 v = *reinterpret_cast<const int4 *>(rowexp + i * 32 + 8 * b + 4 * c.g);
+            ex[4 * b] = v.x;
+            ex[4 * b + 1] = v.y;
+            ex[4 * b + 2] = v.z;
+            ex[4 * b + 3] = v.w;
         }
+    };
+    auto group = [&](int i, int j, int h, const int (&ex)[16]) {
+        return f32x4{__builtin_amdgcn_ldexpf(acc[i][j][4 * h], ex[4 * h] - c.f[j]),
+                     __builtin_amdgcn_ldexpf(acc[i][j][4 * h + 1], ex[4 * h + 1] - c.f[j]),
+                     __builtin_amdgcn_ldexpf(acc[i][j][4 * h + 2], ex[4 * h + 2] - c.f[j]),
+                     __builtin_amdgcn_ldexpf(acc[i][j][4 * h + 3], ex[4 * h + 3] - c.f[j])};
+    };
+    auto store_group = [&](int i, int j, int h, f32x4 y) {
+        const int n = n0 + c.wave * 64 + j * 32 + c.l32;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int m = row_of(i, 4 * h + e);
+            if (m < M && n < N)
+                d.Y[(int64_t)m * N + n] = y[e];
+        }
+    };
 
     if (S > 1) {
         // Split reduction: publish this part's partial tile, count the
@@ -438,15 +545,23 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         // coherent); the stores are complete (s_waitcnt vmcnt(0)) before the
         // arrival is counted.  A release/acquire fence pair would instead
         // write back and invalidate each XCD's whole L2.
+        constexpr int G4 = MSUB * NSUB * 4;  // 16-byte groups per thread
         float *const tp = d.part + (int64_t)tile * S * (BM * BN);
         float *const mine = tp + (int64_t)part * (BM * BN);
 #pragma unroll
-        for (int i = 0; i < MSUB; ++i)
+        for (int i = 0; i < MSUB; ++i) {
+            int ex[16];
+            shifts(i, ex);
 #pragma unroll
             for (int j = 0; j < NSUB; ++j)
-                st_coherent(mine + ((i * NSUB + j) * 256 + tid) * 4, acc[i][j]);
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    st_coherent(mine + (((i * NSUB + j) * 4 + h) * 256 + tid) * 4,
+                                group(i, j, h, ex));
+            __builtin_amdgcn_sched_barrier(0);
+        }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();  // the tile's stores are complete; the ring is no longer read
+        __syncthreads();  // the tile's stores are complete
         int *const flag = reinterpret_cast<int *>(ring);
         if (tid == 0)
             *flag = __hip_atomic_fetch_add(d.cnt + tile, 1, __ATOMIC_RELAXED,
@@ -454,47 +569,54 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
         __syncthreads();
         if (*flag != S - 1)
             return;
+        static_assert(G4 % 4 == 0 && NSUB * 4 % 4 == 0, "groups are summed four at a time");
 #pragma unroll
-        for (int i = 0; i < MSUB; ++i) {
-            // the other parts' groups of row block i, all in flight at once
-            f32x4 v[MAXSPLIT - 1][NSUB];
+        for (int gi = 0; gi < G4; gi += 4) {
+            // groups gi .. gi + 3 (one row block i) of the other parts, all
+            // in flight at once
+            f32x4 v[MAXSPLIT - 1][4];
 #pragma unroll
             for (int q = 0; q < MAXSPLIT - 1; ++q) {
                 const int qq = q < part ? q : q + 1;
 #pragma unroll
-                for (int j = 0; j < NSUB; ++j)
+                for (int u = 0; u < 4; ++u)
                     if (qq < S)
-                        v[q][j] = ld_coherent(tp + (int64_t)qq * (BM * BN) +
-                                              ((i * NSUB + j) * 256 + tid) * 4);
+                        v[q][u] = ld_coherent(tp + (int64_t)qq * (BM * BN) +
+                                              ((gi + u) * 256 + tid) * 4);
             }
             wait_loads(v);
+            const int i = gi / (NSUB * 4);
+            int ex[16];
+            shifts(i, ex);
 #pragma unroll
-            for (int j = 0; j < NSUB; ++j) {
-                f32x4 y = part == 0 ? acc[i][j] : v[0][j];
+            for (int u = 0; u < 4; ++u) {
+                const int gg = gi + u, j = (gg / 4) % NSUB, h = gg % 4;
+                const f32x4 own = group(i, j, h, ex);
+                f32x4 y = part == 0 ? own : v[0][u];
 #pragma unroll
                 for (int q = 1; q < MAXSPLIT; ++q)
                     if (q < S)
-                        y += q == part ? acc[i][j] : v[q < part ? q : q - 1][j];
-                acc[i][j] = y;
+                        y += q == part ? own : v[q < part ? q : q - 1][u];
+                store_group(i, j, h, y);
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        // fall through: the summed tile is stored like an unsplit one
+        return;
     }
 
 #pragma unroll
-    for (int i = 0; i < MSUB; ++i)
+    for (int i = 0; i < MSUB; ++i) {
+        int ex[16];
+        shifts(i, ex);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = m0 + i * 16 + c.lg * 4 + r;
-            if (m >= M)
-                continue;
+        for (int j = 0; j < NSUB; ++j)
 #pragma unroll
-            for (int j = 0; j < NSUB; ++j) {
-                const int n = n0 + c.wave * 64 + j * 16 + c.l16;
-                if (n < N)
-                    d.Y[(int64_t)m * N + n] = acc[i][j][r];
-            }
-        }
+            for (int h = 0; h < 4; ++h)
+                store_group(i, j, h, group(i, j, h, ex));
+        // one row block at a time: hoisting every block's loads would
+        // need more registers than the accumulators leave
+        __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 }  // namespace
@@ -502,6 +624,7 @@ __global__ __launch_bounds__(256, 2) void qgemm_wide_kernel(const GroupArgs args
 int wide_tile_bm() { return BM; }
 int wide_tile_bn() { return BN; }
 int wide_max_split() { return MAXSPLIT; }
+int wide_wgs_per_cu() { return WGS_PER_CU; }
 
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
 {

@@ -90,7 +90,7 @@ int device_cus()
 // trip per part.  The plan is the one with the shortest estimated makespan
 // under the hardware's dispatch: workgroup p runs on XCD p % 8, each XCD
 // takes a contiguous range of every layer's parts (in layer order) and
-// starts them in order on its first free slot (two workgroups per CU).
+// starts them in order on its first free slot (wide_wgs_per_cu() per CU).
 struct SplitPlan {
     int S[QL_MAX_GROUP], psteps[QL_MAX_GROUP];
 };
@@ -125,7 +125,7 @@ double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
 
 SplitPlan plan_splits(const LinDesc *d, int n)
 {
-    const int slots = std::max(1, 2 * device_cus() / XCDS);
+    const int slots = std::max(1, wide_wgs_per_cu() * device_cus() / XCDS);
     SplitPlan best{};
     double best_t = 0.0;
     int best_parts = 0;
