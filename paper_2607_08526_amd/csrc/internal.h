@@ -72,6 +72,11 @@ hipError_t launch_qgemm_skinny(int fmt, const LinDesc &d, hipStream_t stream);
 // Weight-streaming kernel for M <= stream_max_m() (bf16 activations): whole
 // cache lines via direct-to-LDS loads; K % 256 == 0 and 16-byte aligned
 // scales.
+// Wavefront-reduction GEMV for M <= 4 (bf16 activations): codes and scales
+// in registers, activations staged in LDS; gemv_ok() states its shape limits.
+bool gemv_ok(const LinDesc &d);
+hipError_t launch_qgemv(int fmt, const LinDesc &d, hipStream_t stream);
+
 int stream_max_m();
 hipError_t launch_qgemm_stream(int fmt, const LinDesc &d, hipStream_t stream);
 

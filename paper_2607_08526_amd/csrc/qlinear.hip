@@ -235,8 +235,10 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             d.K = (int)ls[i]->K;
             const bool stream_ok = d.M <= stream_max_m() && d.K % 256 == 0 &&
                                    aligned(d.scales, 16);
-            if ((stream_ok ? launch_qgemm_stream(ls[i]->fmt, d, stream)
-                           : launch_qgemm_skinny(ls[i]->fmt, d, stream)) != hipSuccess)
+            const hipError_t e = gemv_ok(d)   ? launch_qgemv(ls[i]->fmt, d, stream)
+                                 : stream_ok ? launch_qgemm_stream(ls[i]->fmt, d, stream)
+                                             : launch_qgemm_skinny(ls[i]->fmt, d, stream);
+            if (e != hipSuccess)
                 return QL_ERR_HIP;
         }
         return QL_OK;
