@@ -243,14 +243,52 @@ def graph_time(torch, fn, reps=20, warm=5):
     return ts[len(ts) // 2], ts[0], ts[-1]
 
 
+class ReadCeiling:
+    """Time per call of a plain streaming read of a given number of bytes
+    (libqlbench.so, built beside the library): the practical ceiling for a
+    kernel that must stream one weight matrix, launch overhead included."""
+
+    def __init__(self, torch):
+        import ctypes
+        from paper_2607_08526_amd import build as B
+        self.torch = torch
+        self.lib = ctypes.CDLL(B.BENCH_LIB)
+        self.lib.qlbench_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        self.lib.qlbench_read.restype = ctypes.c_int
+        self.sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+
+    def us_per_call(self, nbytes):
+        import ctypes
+        torch = self.torch
+        nbytes = (nbytes + 15) // 16 * 16
+        R = max(1, -(-ROT_BYTES // nbytes))
+        bufs = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(R)]
+        for b in bufs:
+            b.fill_(1)
+
+        def fn():
+            s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+            for b in bufs:
+                if self.lib.qlbench_read(ctypes.c_void_p(b.data_ptr()), nbytes,
+                                         ctypes.c_void_p(self.sink.data_ptr()), s) != 0:
+                    raise RuntimeError("read-ceiling launch failed")
+
+        med, lo, hi = graph_time(torch, fn)
+        del bufs
+        return med / R * 1e3
+
+
 def skinny_sweep(torch, ql, si):
     out = []
     dev = torch.device("cuda")
+    ceiling = ReadCeiling(torch)
     for v, fmt, N, K in si.skinny_variants():
         W = si.skinny_weight(v, N, K)
         codes, scales = ql.quantize(fmt, torch.from_numpy(W).to(dev))
         wbytes = codes.numel() + 2 * scales.numel()
         R = max(1, -(-ROT_BYTES // wbytes))
+        ceil_us = ceiling.us_per_call(wbytes)
         copies = [(codes.clone(), scales.clone()) for _ in range(R)]
         for M in si.SKINNY_M:
             X = torch.from_numpy(si.skinny_activations(M, K).view("int16")).to(dev)
@@ -272,6 +310,8 @@ def skinny_sweep(torch, ql, si):
                 "hbm_frac": round(algo_bytes / t / 1e9 / HBM_PEAK_GBPS, 4),
                 "TFLOPs": round(flops / t / 1e12, 3),
                 "rotation_copies": R,
+                "read_ceiling_us": round(ceil_us, 3),
+                "frac_of_read_ceiling": round(ceil_us / (t * 1e6), 4),
             })
             log(f"skinny {out[-1]}")
         del copies

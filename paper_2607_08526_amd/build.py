@@ -45,8 +45,24 @@ def _compile(src):
     return obj
 
 
+BENCH_SRC = os.path.join(HERE, "bench_csrc", "read_ceiling.hip")
+BENCH_LIB = os.path.join(HERE, "libqlbench.so")
+
+
+def build_bench_helper():
+    """The benchmark's read-ceiling kernel (libqlbench.so, not the product)."""
+    tmp = BENCH_LIB + ".tmp"
+    cmd = [HIPCC, *DEVICE_FLAGS, "-shared", BENCH_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for the bench helper:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, BENCH_LIB)
+    return BENCH_LIB
+
+
 def build(verbose=True):
-    """Compile every HIP source for gfx950 and link libqlinear.so; returns its path."""
+    """Compile every HIP source for gfx950 and link libqlinear.so (and the
+    benchmark's helper library); returns the library's path."""
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
@@ -56,8 +72,9 @@ def build(verbose=True):
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    build_bench_helper()
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {BENCH_LIB}")
     return LIB
 
 

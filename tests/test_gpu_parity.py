@@ -165,6 +165,22 @@ def test_forward_streaming_ragged(gpu, orc, fmt):
         assert e <= TOL[O.DT_BF16], (M, N, K, e)
 
 
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_gemv_shapes(gpu, orc, fmt):
+    """The wavefront-reduction GEMV (M <= 4, K % 256 == 0, K <= 8192): every
+    M, lanes with one to four blocks and with a ragged last block round
+    (K / 32 not a multiple of 64), row counts that leave wavefronts of the
+    last workgroup without rows, the largest staged activation (4 x 8192)."""
+    for (M, N, K) in ((1, 1, 256), (2, 13, 2048), (3, 4097, 2304), (4, 1000, 4352),
+                      (1, 8191, 8192), (4, 300, 8192), (2, 64, 6144), (3, 5, 7936)):
+        W, X = si.small_case(40 + M + N + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        e = rel_err(Yg, Yr)
+        assert e <= TOL[O.DT_BF16], (M, N, K, e)
+
+
 @pytest.mark.parametrize("K", [4096, 16384, 16640])
 def test_forward_long_rows(gpu, orc, K):
     """Large-M bf16 path at reduction lengths that exercise every row width
