@@ -1,4 +1,4 @@
-// Quantized linear forward for very few activation rows (bf16, M <= 16):
+// Quantized linear forward for few activation rows (bf16, M <= 32):
 // a weight-streaming kernel, bound by HBM bandwidth.
 //
 //   Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k]
@@ -111,7 +111,8 @@ struct SGeo {
     static constexpr int NCI = (CODE + 1023) / 1024;            // code loads per chunk
     static constexpr int NXI = MX * XROW / 1024;                // activation loads per chunk
     static constexpr int N = NCI + NXI;                         // loads per chunk (+1 every 8)
-    static constexpr int R = MX <= 4 ? 6 : 3;                   // ring depth (chunks)
+    static constexpr int R = MX <= 4 ? 6 : MX <= 8 ? 4 : 3;     // ring depth (chunks)
+    static constexpr int NF = MX / 16 > 1 ? MX / 16 : 1;        // 16-row activation fragments
     static constexpr int SLOT = RW * 64;                        // scales of 32 blocks
     static constexpr int WAVE = R * STAGE + 2 * SLOT;           // LDS bytes per wavefront
     static_assert((MX * XROW) % 1024 == 0, "whole activation loads");
@@ -205,9 +206,14 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
 
     const uint32_t negoff = FMT == QL_FMT_INT8 ? 0xC300C300u : 0xC308C308u;  // -128 / -136
     const u32x4 bneg = {negoff, negoff, negoff, negoff};
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[G::NF];
+#pragma unroll
+    for (int f = 0; f < G::NF; ++f)
+        acc[f] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int j = l16 % RW;  // weight row of this lane's MFMA column
-    const int mx = l16 % MX; // activation row of this lane's A fragment (rows >= M unused)
+    // activation row of this lane's A fragment f: f * 16 + mx (rows >= M are
+    // never stored; with MX < 16 the fragment's other rows repeat these)
+    const int mx = l16 % (MX < 16 ? MX : 16);
 
 #pragma unroll
     for (int c = 0; c < G::R - 1; ++c)
@@ -236,16 +242,21 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
                                                                        lg * 4);
                 B = cvt_q4_off(v);
             }
-            // activation fragment: row mx, bf16 [32 t + 8 lg, +8) = piece 4t + lg
-            const u32x4 a = *reinterpret_cast<const u32x4 *>(
-                st + G::CODE + mx * G::XROW + ((4 * t + lg) ^ (mx & 15)) * 16);
             // scale of block 4c + t (within the 32-block run of this chunk)
             const int bs = (c % 8) * 4 + t;  // 0..31
             const int spiece = (bs >> 3) ^ ((j >> 2) & 3);
             const uint16_t sbits = *reinterpret_cast<const uint16_t *>(
                 ss + j * 64 + spiece * 16 + (bs & 7) * 2);
             const float s = (float)__builtin_bit_cast(_Float16, sbits);
-            acc += s * mfma(a, B, mfma(a, bneg, f32x4{0.f, 0.f, 0.f, 0.f}));
+#pragma unroll
+            for (int f = 0; f < G::NF; ++f) {
+                // activation fragment f: row f * 16 + mx, bf16 [32 t + 8 lg, +8) =
+                // piece 4t + lg
+                const int row = f * 16 + mx;
+                const u32x4 a = *reinterpret_cast<const u32x4 *>(
+                    st + G::CODE + row * G::XROW + ((4 * t + lg) ^ (row & 15)) * 16);
+                acc[f] += s * mfma(a, B, mfma(a, bneg, f32x4{0.f, 0.f, 0.f, 0.f}));
+            }
         }
     }
 
@@ -253,38 +264,49 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
     // memory is reused once every wavefront is done with it)
     __syncthreads();
     f32x4 *red = reinterpret_cast<f32x4 *>(lds);
-    red[wave * 64 + lane] = acc;
+#pragma unroll
+    for (int f = 0; f < G::NF; ++f)
+        red[(f * KW + wave) * 64 + lane] = acc[f];
     __syncthreads();
     if (wave == 0) {
-        f32x4 y = red[lane];
 #pragma unroll
-        for (int w = 1; w < KW; ++w)
-            y += red[w * 64 + lane];
-        const int n = n0 + l16;
+        for (int f = 0; f < G::NF; ++f) {
+            f32x4 y = red[f * KW * 64 + lane];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = lg * 4 + r;
-            if (l16 < RW && m < M && n < N)
-                d.Y[(int64_t)m * N + n] = y[r];
+            for (int w = 1; w < KW; ++w)
+                y += red[(f * KW + w) * 64 + lane];
+            const int n = n0 + l16;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = f * 16 + lg * 4 + r;
+                if (l16 < RW && m < M && n < N)
+                    d.Y[(int64_t)m * N + n] = y[r];
+            }
         }
+    }
+}
+
+template <int FMT, int RW, int MX, int KW>
+hipError_t launch_kw(const LinDesc &d, hipStream_t s)
+{
+    if constexpr (KW * SGeo<FMT, RW, MX>::WAVE > 160 * 1024) {
+        return hipErrorInvalidValue;  // does not fit the LDS; never chosen
+    } else {
+        const dim3 grid((unsigned)((d.N + RW - 1) / RW));
+        hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, KW>), grid, dim3(64 * KW), 0, s, d);
+        return hipGetLastError();
     }
 }
 
 template <int FMT, int RW, int MX>
 hipError_t launch_rw(int kw, const LinDesc &d, hipStream_t s)
 {
-    const dim3 grid((unsigned)((d.N + RW - 1) / RW));
     switch (kw) {
-    case 4:
-        hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, 4>), grid, dim3(256), 0, s, d);
-        break;
-    case 8:
-        hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, 8>), grid, dim3(512), 0, s, d);
-        break;
-    default:
-        return hipErrorInvalidValue;
+    case 2: return launch_kw<FMT, RW, MX, 2>(d, s);
+    case 4: return launch_kw<FMT, RW, MX, 4>(d, s);
+    case 8: return launch_kw<FMT, RW, MX, 8>(d, s);
+    default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 template <int FMT>
@@ -299,12 +321,18 @@ hipError_t launch_fmt(const LinDesc &d, hipStream_t s)
     const int kw = (groups * 4 < 2048 && nb >= 8 * 16) ? 8 : 4;
     if (d.M <= 4)
         return narrow ? launch_rw<FMT, 8, 4>(kw, d, s) : launch_rw<FMT, 16, 4>(kw, d, s);
-    return narrow ? launch_rw<FMT, 8, 16>(kw, d, s) : launch_rw<FMT, 16, 16>(kw, d, s);
+    if (d.M <= 8)
+        return narrow ? launch_rw<FMT, 8, 8>(kw, d, s) : launch_rw<FMT, 16, 8>(kw, d, s);
+    if (d.M <= 16)
+        return narrow ? launch_rw<FMT, 8, 16>(kw, d, s) : launch_rw<FMT, 16, 16>(kw, d, s);
+    // 32 activation rows: two wavefronts per workgroup keep two workgroups
+    // per CU within the LDS; few row groups take four (one per CU)
+    return narrow ? launch_rw<FMT, 8, 32>(4, d, s) : launch_rw<FMT, 16, 32>(2, d, s);
 }
 
 }  // namespace
 
-int stream_max_m() { return 16; }
+int stream_max_m() { return 32; }
 
 hipError_t launch_qgemm_stream(int fmt, const LinDesc &d, hipStream_t stream)
 {
