@@ -75,8 +75,12 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 #ifndef QL_WIDE_MSUB
 #define QL_WIDE_MSUB 4
 #endif
-constexpr int MSUB = QL_WIDE_MSUB, NSUB = 2, BM = 32 * MSUB, BN = 4 * 32 * NSUB, GROUP_M = 4;
-constexpr int WGS_PER_CU = MSUB == 8 ? 1 : 2;
+#ifndef QL_WIDE_WAVES
+#define QL_WIDE_WAVES 4
+#endif
+constexpr int WAVES = QL_WIDE_WAVES, THREADS = 64 * WAVES;
+constexpr int MSUB = QL_WIDE_MSUB, NSUB = 2, BM = 32 * MSUB, BN = WAVES * 32 * NSUB, GROUP_M = 4;
+constexpr int WGS_PER_CU = MSUB == 8 || WAVES == 8 ? 1 : 2;
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
 
 template <int FMT>
@@ -92,13 +96,13 @@ struct Geo {
     // row every 4 steps, into a 2-slot ring; a per-step load would cost one
     // memory request per row for 4 bytes
     static constexpr int SGROUP = 4, SSLOT = BN * 16;
-    static constexpr int XLOADS = XBYTES / 16 / 256;
-    static constexpr int CLOADS = CBYTES / 16 / 256;
+    static constexpr int XLOADS = XBYTES / 16 / THREADS;
+    static constexpr int CLOADS = CBYTES / 16 / THREADS;
     static constexpr int LOADS = XLOADS + CLOADS;  // direct-to-LDS loads per step (+1 every 4)
     static constexpr int LDS = NST * STAGE + 2 * SSLOT;
-    static_assert(XBYTES % (16 * 256) == 0 && CBYTES % (16 * 256) == 0,
+    static_assert(XBYTES % (16 * THREADS) == 0 && CBYTES % (16 * THREADS) == 0,
                   "every thread issues the same number of 16-byte loads per stage");
-    static_assert(BN == 256, "one scale chunk per weight row per thread");
+    static_assert(BN == THREADS, "one scale chunk per weight row per thread");
     static_assert(WGS_PER_CU * LDS <= 160 * 1024, "resident workgroups per CU");
 };
 
@@ -248,10 +252,10 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
     const uint8_t *cb = c.cbase + s * G::CROW;
 #pragma unroll
     for (int r = 0; r < G::XLOADS; ++r)
-        dma16(xb, c.xoff[r], base + (r * 256 + c.wave * 64) * 16);
+        dma16(xb, c.xoff[r], base + (r * THREADS + c.wave * 64) * 16);
 #pragma unroll
     for (int r = 0; r < G::CLOADS; ++r)
-        dma16(cb, c.coff[r], base + G::XBYTES + (r * 256 + c.wave * 64) * 16);
+        dma16(cb, c.coff[r], base + G::XBYTES + (r * THREADS + c.wave * 64) * 16);
     if (s % G::SGROUP == 0) {
         const int g = s / G::SGROUP;
         dma16(c.sbase + g * 16, c.soff,
@@ -360,7 +364,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, in
 }
 
 template <int FMT>
-__global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const GroupArgs args)
+__global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
     constexpr int NST = G::NST, PD = NST - 1;  // prefetch distance in steps
@@ -407,7 +411,7 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
     // repeat the last row (their outputs are never stored)
 #pragma unroll
     for (int r = 0; r < G::XLOADS; ++r) {
-        const int slot = r * 256 + tid;
+        const int slot = r * THREADS + tid;
         const int row = slot >> 3;
         const int lc = (slot & 7) ^ xswz(row);
         const int m = min(m0 + row, M - 1) - m0;
@@ -417,7 +421,7 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
     // repeat the last row
 #pragma unroll
     for (int r = 0; r < G::CLOADS; ++r) {
-        const int slot = r * 256 + tid;
+        const int slot = r * THREADS + tid;
         const int row = slot / G::CCH;
         const int lc = (slot % G::CCH) ^ cswz<FMT>(row);
         const int n = min(n0 + row, N - 1) - n0;
@@ -505,7 +509,7 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
     auto row_of = [&](int i, int r) { return m0 + i * 32 + 8 * (r >> 2) + 4 * c.g + (r & 3); };
     int *const rowexp = reinterpret_cast<int *>(ring + 256);
     __syncthreads();
-    for (int t = tid; t < BM; t += 256)
+    for (int t = tid; t < BM; t += THREADS)
         rowexp[t] = d.xexp[min(m0 + t, M - 1)];
     __syncthreads();
     auto shifts = [&](int i, int (&ex)[16]) {
@@ -524,13 +528,41 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
                      __builtin_amdgcn_ldexpf(acc[i][j][4 * h + 2], ex[4 * h + 2] - c.f[j]),
                      __builtin_amdgcn_ldexpf(acc[i][j][4 * h + 3], ex[4 * h + 3] - c.f[j])};
     };
-    auto store_group = [&](int i, int j, int h, f32x4 y) {
-        const int n = n0 + c.wave * 64 + j * 32 + c.l32;
+    // Y stores: each 32 x 32 tile (the four groups h of (i, j)) goes through
+    // a wavefront-private 4 KB LDS patch, written in the MFMA layout and
+    // read back as rows, so that every lane stores 16 contiguous bytes and
+    // each store instruction covers 8 whole 128-byte row segments (the
+    // register layout would give 4-byte stores).  A wavefront reads only
+    // what it wrote, in order, so no barrier is needed.
+    float *const patch = reinterpret_cast<float *>(ring + 1024) + c.wave * 1024;
+    auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int m = row_of(i, 4 * h + e);
-            if (m < M && n < N)
-                d.Y[(int64_t)m * N + n] = y[e];
+        for (int h = 0; h < 4; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
+        const int lane = tid & 63;
+        const int cq = lane & 7;          // 4-column group of the row
+        const int n = n0 + c.wave * 64 + j * 32 + 4 * cq;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int rl = 8 * t + (lane >> 3);  // row within the 32-row tile
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + rl * 32 + 4 * cq);
+            const int m = m0 + i * 32 + rl;
+            if (m >= M)
+                continue;
+            float *const dst = d.Y + (int64_t)m * N + n;
+            if (n + 3 < N && (N & 3) == 0 && ((uintptr_t)d.Y & 15) == 0) {
+                // streaming store: Y is not read again here, and letting it
+                // allocate would evict the activation and code lines that
+                // other tiles still re-read
+                __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < N)
+                        dst[e] = v[e];
+            }
         }
     };
 
@@ -556,7 +588,7 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
             for (int j = 0; j < NSUB; ++j)
 #pragma unroll
                 for (int h = 0; h < 4; ++h)
-                    st_coherent(mine + (((i * NSUB + j) * 4 + h) * 256 + tid) * 4,
+                    st_coherent(mine + (((i * NSUB + j) * 4 + h) * THREADS + tid) * 4,
                                 group(i, j, h, ex));
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -582,23 +614,24 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
                 for (int u = 0; u < 4; ++u)
                     if (qq < S)
                         v[q][u] = ld_coherent(tp + (int64_t)qq * (BM * BN) +
-                                              ((gi + u) * 256 + tid) * 4);
+                                              ((gi + u) * THREADS + tid) * 4);
             }
             wait_loads(v);
             const int i = gi / (NSUB * 4);
             int ex[16];
             shifts(i, ex);
+            const int j = (gi / 4) % NSUB;
+            f32x4 y[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int gg = gi + u, j = (gg / 4) % NSUB, h = gg % 4;
-                const f32x4 own = group(i, j, h, ex);
-                f32x4 y = part == 0 ? own : v[0][u];
+                const f32x4 own = group(i, j, u, ex);
+                y[u] = part == 0 ? own : v[0][u];
 #pragma unroll
                 for (int q = 1; q < MAXSPLIT; ++q)
                     if (q < S)
-                        y += q == part ? own : v[q < part ? q : q - 1][u];
-                store_group(i, j, h, y);
+                        y[u] += q == part ? own : (q < part ? v[q][u] : v[q - 1][u]);
             }
+            store_tile(i, j, y);
             __builtin_amdgcn_sched_barrier(0);
         }
         return;
@@ -609,10 +642,13 @@ __global__ __launch_bounds__(256, WGS_PER_CU) void qgemm_wide_kernel(const Group
         int ex[16];
         shifts(i, ex);
 #pragma unroll
-        for (int j = 0; j < NSUB; ++j)
+        for (int j = 0; j < NSUB; ++j) {
+            f32x4 y[4];
 #pragma unroll
             for (int h = 0; h < 4; ++h)
-                store_group(i, j, h, group(i, j, h, ex));
+                y[h] = group(i, j, h, ex);
+            store_tile(i, j, y);
+        }
         // one row block at a time: hoisting every block's loads would
         // need more registers than the accumulators leave
         __builtin_amdgcn_sched_barrier(0);
@@ -628,7 +664,7 @@ int wide_wgs_per_cu() { return WGS_PER_CU; }
 
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
 {
-    dim3 grid((unsigned)args.total_tiles), block(256);
+    dim3 grid((unsigned)args.total_tiles), block(THREADS);
     if (fmt == QL_FMT_INT8)
         hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_INT8>, grid, block, 0, stream, args);
     else
