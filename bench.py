@@ -216,17 +216,24 @@ def time_step(torch, step, steps, warmup):
     return total_ms, launch_ms, wall
 
 
+_GRAPH_STREAM = []
+
+
 def graph_time(torch, fn, reps=20, warm=5):
     """Capture fn() (a sequence of launches) in a HIP graph, replay it and
-    return the median replay time in ms."""
-    s = torch.cuda.Stream()
+    return the median replay time in ms.  fn() runs once before the capture
+    on the stream it is captured on (one stream for every call), so the
+    library's per-stream workspace already has its size when captured."""
+    if not _GRAPH_STREAM:
+        _GRAPH_STREAM.append(torch.cuda.Stream())
+    s = _GRAPH_STREAM[0]
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         fn()
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
+    with torch.cuda.graph(g, stream=s):
         fn()
     for _ in range(warm):
         g.replay()

@@ -55,12 +55,21 @@
  *     synchronization, as in HIP itself.
  *   - The library keeps no pointer after a call returns.
  *   - Workspace: the fp16 path (above) needs M * K * 2 + M * 4 bytes per
- *     distinct activation tensor of a call.  It is taken stream-ordered from
- *     a memory pool the library owns (one per device, created on first use)
- *     and returned to it, in stream order, right after the launch; the pool
- *     keeps what it has grown to, so steady-state calls do not reach the
- *     driver.  No other forward path uses device memory beyond its
- *     arguments.  Allocation failure returns QL_ERR_HIP.
+ *     distinct activation tensor of a call, plus fp32 partial results when
+ *     it splits a layer's reduction.  The library keeps one workspace per
+ *     (device, stream), taken from a stream-ordered memory pool it owns; it
+ *     grows when a call outside graph capture needs more (the old buffer
+ *     goes back to the pool in stream order), so steady-state calls
+ *     allocate nothing.  Consequences: calls on one stream share it, which
+ *     their stream order makes safe; a graph captured on a stream keeps
+ *     that stream's buffer (it is then never released before the process
+ *     ends), so replays of the graph must not overlap calls on the capture
+ *     stream or replays of other graphs captured on it.  A call under
+ *     capture that needs more than its stream's buffer allocates for itself
+ *     from the pool (allocation and free nodes in the graph) instead.  A
+ *     destroyed stream's handle value, if reused, inherits its buffer.  No
+ *     other forward path uses device memory beyond its arguments.
+ *     Allocation failure returns QL_ERR_HIP.
  */
 #ifndef QLINEAR_H
 #define QLINEAR_H
@@ -111,7 +120,7 @@ int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K,
 
 /* Y[M][N] (fp32) = X[M][K] * dequant(codes, scales)^T, the forward pass of
  * one quantized linear layer.  Asynchronous on `stream`; does not
- * synchronize, and allocates nothing outside the workspace pool described
+ * synchronize, and allocates nothing outside the workspace described
  * above.  M == 0 is a successful no-op.  Y must not alias
  * X, codes or scales.  Sizes: M, N < 2^31, K < 2^31. */
 int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K,

@@ -20,10 +20,13 @@ struct LinDesc {
     int tile_begin;  // first logical tile of this layer in a grouped launch
     const int *xexp; // fp16 path: per-row power-of-two shift of X (see xprep.hip)
     // fp16 path, split reduction: each output tile is computed as ksplit
-    // (<= wide_max_split()) parts of psteps 64-k steps each; parts store
-    // fp32 partial tiles in part[tiles][ksplit][BM * BN] and count arrivals
-    // in cnt[tiles_m * tiles_n] (zero before the launch); the last part to
-    // arrive sums them in part order.  ksplit == 1: no workspace.
+    // parts of psteps 64-k steps each.  cnt != nullptr (ksplit <=
+    // wide_max_split()): parts store fp32 partial tiles in
+    // part[tiles][ksplit][BM * BN] and count arrivals in
+    // cnt[tiles_m * tiles_n] (zero before the launch); the last part to
+    // arrive sums them in part order.  cnt == nullptr: parts store plain
+    // partial outputs part[ksplit][M][N] and launch_split_sum adds them
+    // after the launch.  ksplit == 1: no workspace.
     int ksplit, psteps;
     float *part;
     int *cnt;
@@ -57,6 +60,10 @@ int wide_tile_bn();
 int wide_max_split();
 int wide_wgs_per_cu();  // resident workgroups per CU (LDS and register budget)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
+
+// Y[M][N] = sum over s < S of P[s][M][N], added in order s = 0, 1, ...
+hipError_t launch_split_sum(const float *P, int S, int64_t M, int64_t N, float *Y,
+                            hipStream_t stream);
 
 // bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M];
 // also sets zero[0 .. nzero) to 0 (the split counters of the launch that

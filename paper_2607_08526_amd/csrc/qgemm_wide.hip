@@ -59,6 +59,8 @@
 // reuse), and every layer of a grouped launch is spread over all XCDs.  Long
 // reductions may be cut into K parts (ksplit, see the split reduction at the
 // end of the kernel).
+#include <algorithm>
+
 #include "internal.h"
 
 namespace qlk {
@@ -209,16 +211,22 @@ __device__ inline f32x4 ld_coherent(const float *p)
     return v;
 }
 
-// wait for every load issued above; the values pass through the statement so
-// that no use can be scheduled before it
-template <int A, int B>
-__device__ inline void wait_loads(f32x4 (&v)[A][B])
+// wait for every load issued above; the values pass through the statements
+// so that no use can be scheduled before the wait
+__device__ inline void wait_loads(f32x4 (&v)[4][8])
 {
-    static_assert(A * B == 12, "operand list below");
     asm volatile("s_waitcnt vmcnt(0)"
                  : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]),
+                   "+v"(v[0][4]), "+v"(v[0][5]), "+v"(v[0][6]), "+v"(v[0][7]),
                    "+v"(v[1][0]), "+v"(v[1][1]), "+v"(v[1][2]), "+v"(v[1][3]),
-                   "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3])
+                   "+v"(v[1][4]), "+v"(v[1][5]), "+v"(v[1][6]), "+v"(v[1][7])
+                 :
+                 : "memory");
+    asm volatile(""
+                 : "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3]),
+                   "+v"(v[2][4]), "+v"(v[2][5]), "+v"(v[2][6]), "+v"(v[2][7]),
+                   "+v"(v[3][0]), "+v"(v[3][1]), "+v"(v[3][2]), "+v"(v[3][3]),
+                   "+v"(v[3][4]), "+v"(v[3][5]), "+v"(v[3][6]), "+v"(v[3][7])
                  :
                  : "memory");
 }
@@ -453,6 +461,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
         const int n = min(n0 + c.wave * 64 + j * 32 + c.l32, N - 1);
         const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
         uint32_t mx = 0;
+#pragma unroll 4
         for (int q = c.g; q < nb / 8; q += 2) {
             const u32x4 v = srow[q];
 #pragma unroll
@@ -535,6 +544,9 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     // register layout would give 4-byte stores).  A wavefront reads only
     // what it wrote, in order, so no barrier is needed.
     float *const patch = reinterpret_cast<float *>(ring + 1024) + c.wave * 1024;
+    // destination: Y, or this part's plain partial output when the parts
+    // are summed by a separate launch (split_sum_kernel)
+    float *const Yd = S > 1 && !d.cnt ? d.part + (int64_t)part * M * N : d.Y;
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
 #pragma unroll
         for (int h = 0; h < 4; ++h)
@@ -551,8 +563,8 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
             const int m = m0 + i * 32 + rl;
             if (m >= M)
                 continue;
-            float *const dst = d.Y + (int64_t)m * N + n;
-            if (n + 3 < N && (N & 3) == 0 && ((uintptr_t)d.Y & 15) == 0) {
+            float *const dst = Yd + (int64_t)m * N + n;
+            if (n + 3 < N && (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0) {
                 // streaming store: Y is not read again here, and letting it
                 // allocate would evict the activation and code lines that
                 // other tiles still re-read
@@ -566,7 +578,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
         }
     };
 
-    if (S > 1) {
+    if (S > 1 && d.cnt) {
         // Split reduction: publish this part's partial tile, count the
         // arrival; the last part to arrive adds all partials in part order
         // (the same sum whichever part finishes last).  A partial tile is
@@ -601,37 +613,33 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
         __syncthreads();
         if (*flag != S - 1)
             return;
-        static_assert(G4 % 4 == 0 && NSUB * 4 % 4 == 0, "groups are summed four at a time");
+        // Every part, this one included, has stored its partial tile: the
+        // sum is read back from memory, two 32 x 32 tiles (8 groups of every
+        // part, up to 32 loads) per round trip, and added in part order.
+        static_assert(G4 % 8 == 0 && MAXSPLIT == 4, "two tiles of four parts per batch");
 #pragma unroll
-        for (int gi = 0; gi < G4; gi += 4) {
-            // groups gi .. gi + 3 (one row block i) of the other parts, all
-            // in flight at once
-            f32x4 v[MAXSPLIT - 1][4];
+        for (int gb = 0; gb < G4; gb += 8) {
+            f32x4 v[MAXSPLIT][8];
 #pragma unroll
-            for (int q = 0; q < MAXSPLIT - 1; ++q) {
-                const int qq = q < part ? q : q + 1;
+            for (int q = 0; q < MAXSPLIT; ++q)
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (qq < S)
-                        v[q][u] = ld_coherent(tp + (int64_t)qq * (BM * BN) +
-                                              ((gi + u) * THREADS + tid) * 4);
-            }
+                for (int u = 0; u < 8; ++u)
+                    if (q < S)
+                        v[q][u] = ld_coherent(tp + (int64_t)q * (BM * BN) +
+                                              ((gb + u) * THREADS + tid) * 4);
             wait_loads(v);
-            const int i = gi / (NSUB * 4);
-            int ex[16];
-            shifts(i, ex);
-            const int j = (gi / 4) % NSUB;
-            f32x4 y[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const f32x4 own = group(i, j, u, ex);
-                y[u] = part == 0 ? own : v[0][u];
+            for (int u = 0; u < 8; ++u)
 #pragma unroll
                 for (int q = 1; q < MAXSPLIT; ++q)
                     if (q < S)
-                        y[u] += q == part ? own : (q < part ? v[q][u] : v[q - 1][u]);
+                        v[0][u] += v[q][u];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int gi = gb + 4 * t;
+                const f32x4 y[4] = {v[0][4 * t], v[0][4 * t + 1], v[0][4 * t + 2], v[0][4 * t + 3]};
+                store_tile(gi / (NSUB * 4), (gi / 4) % NSUB, y);
             }
-            store_tile(i, j, y);
             __builtin_amdgcn_sched_barrier(0);
         }
         return;
@@ -655,7 +663,44 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     }
 }
 
+// Sum of the S plain partial outputs P[s][M][N] of a split launch, in part
+// order (the same sum as the in-kernel reduction): Y = ((P0 + P1) + P2) ...
+// V4: 16-byte groups (N % 4 == 0, Y 16-byte aligned), else single floats.
+template <bool V4>
+__global__ __launch_bounds__(256) void split_sum_kernel(const float *__restrict__ P, int S,
+                                                        int64_t count, float *__restrict__ Y)
+{
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) {
+        if constexpr (V4) {
+            const f32x4 *p = reinterpret_cast<const f32x4 *>(P) + i;
+            f32x4 y = p[0];
+            for (int q = 1; q < S; ++q)
+                y += p[q * count];
+            __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(Y) + i);
+        } else {
+            float y = P[i];
+            for (int q = 1; q < S; ++q)
+                y += P[i + q * count];
+            Y[i] = y;
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_split_sum(const float *P, int S, int64_t M, int64_t N, float *Y,
+                            hipStream_t stream)
+{
+    const bool v4 = N % 4 == 0 && ((uintptr_t)Y & 15) == 0;
+    const int64_t count = v4 ? M * N / 4 : M * N;
+    const unsigned grid = (unsigned)std::min<int64_t>((count + 255) / 256, 4096);
+    if (v4)
+        hipLaunchKernelGGL(split_sum_kernel<true>, dim3(grid), dim3(256), 0, stream, P, S, count, Y);
+    else
+        hipLaunchKernelGGL(split_sum_kernel<false>, dim3(grid), dim3(256), 0, stream, P, S, count, Y);
+    return hipGetLastError();
+}
 
 int wide_tile_bm() { return BM; }
 int wide_tile_bn() { return BN; }

@@ -36,10 +36,8 @@ int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const vo
     return QL_OK;
 }
 
-// Stream-ordered pool (one per device) for the fp16 copies of the
-// activations that the large-M bf16 path works from.  The pool keeps what it
-// has grown to, so steady-state calls reuse memory without touching the
-// driver; allocations are freed in stream order right after their launch.
+// Stream-ordered pool (one per device) that the per-stream workspaces below
+// come from.  The pool keeps what it has grown to.
 hipMemPool_t workspace_pool()
 {
     constexpr int MAXDEV = 64;
@@ -69,6 +67,76 @@ hipMemPool_t workspace_pool()
 
 size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// Workspace of the large-M bf16 path (fp16 activation copies, split
+// partials).  Calls on one stream run in order, so one buffer per (device,
+// stream) serves them all; taking it costs nothing on the device, where a
+// stream-ordered allocation and free per call cost microseconds (and, in a
+// captured graph, allocation nodes that cost more).  The buffer grows, in
+// stream order, when a call outside graph capture needs more; the old one is
+// returned to the pool unless a graph was captured with it, in which case it
+// stays allocated for the life of the process (replays still use it).  A
+// call under capture that needs more than the stream's buffer takes a
+// stream-ordered allocation for itself (freed after its launch) instead.
+struct Workspace {
+    uint8_t *ptr;
+    bool own_alloc;  // allocated for this call: free after the launch
+};
+
+bool take_workspace(size_t bytes, hipStream_t stream, Workspace &w)
+{
+    struct Entry {
+        int dev;
+        hipStream_t stream;
+        void *ptr;
+        size_t bytes;
+        bool captured;  // a graph holds this buffer
+    };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return false;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess)
+        return false;
+    const bool capturing = cs != hipStreamCaptureStatusNone;
+    hipMemPool_t pool = workspace_pool();
+    if (!pool)
+        return false;
+    std::lock_guard<std::mutex> g(mu);
+    Entry *e = nullptr;
+    for (Entry &c : cache)
+        if (c.dev == dev && c.stream == stream)
+            e = &c;
+    if (!e) {
+        cache.push_back(Entry{dev, stream, nullptr, 0, false});
+        e = &cache.back();
+    }
+    if (e->bytes >= bytes) {
+        e->captured |= capturing;
+        w = Workspace{(uint8_t *)e->ptr, false};
+        return true;
+    }
+    void *p = nullptr;
+    if (capturing) {
+        if (hipMallocFromPoolAsync(&p, bytes, pool, stream) != hipSuccess)
+            return false;
+        w = Workspace{(uint8_t *)p, true};
+        return true;
+    }
+    const size_t grow = ((std::max(bytes, e->bytes + e->bytes / 2)) + ((size_t)1 << 21) - 1) &
+                        ~(((size_t)1 << 21) - 1);
+    if (hipMallocFromPoolAsync(&p, grow, pool, stream) != hipSuccess)
+        return false;
+    if (e->ptr && !e->captured && hipFreeAsync(e->ptr, stream) != hipSuccess) {
+        hipFreeAsync(p, stream);
+        return false;
+    }
+    *e = Entry{dev, stream, p, grow, false};
+    w = Workspace{(uint8_t *)p, false};
+    return true;
+}
+
 int device_cus()
 {
     constexpr int MAXDEV = 64;
@@ -91,13 +159,25 @@ int device_cus()
 // under the hardware's dispatch: workgroup p runs on XCD p % 8, each XCD
 // takes a contiguous range of every layer's parts (in layer order) and
 // starts them in order on its first free slot (wide_wgs_per_cu() per CU).
+//
+// A single-layer launch that fits in one wave of workgroup slots has no
+// other work to hide the last parts' in-kernel reduction behind: there the
+// parts may instead store plain partial outputs that one more launch adds
+// up at full-chip bandwidth (ext), which also allows more and shorter parts.
 struct SplitPlan {
     int S[QL_MAX_GROUP], psteps[QL_MAX_GROUP];
+    bool ext;
 };
 
 constexpr int XCDS = 8;
 constexpr double TILE_OVH = 3.0;   // prologue + epilogue, in 64-k steps
 constexpr double SPLIT_OVH = 2.0;  // partial store / reload per part
+// one-wave single-layer launches (times in steps of ~1 us, measured):
+constexpr double PART_STORE = 2.5;       // a part's partial store and arrival
+constexpr double TAIL_PER_PART = 2.2;    // last arriver's reload of one partial tile
+constexpr double EXT_GAP = 2.0;          // the extra launch
+constexpr double EXT_BYTES_PER_STEP = 5.0e6;  // bytes the sum launch moves per step
+constexpr int EXT_MAX_SPLIT = 16;
 
 double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
 {
@@ -161,6 +241,30 @@ SplitPlan plan_splits(const LinDesc *d, int n)
             best = pl;
             best_t = t;
             best_parts = total_parts;
+        }
+    }
+    const int64_t tiles = (int64_t)d[0].tiles_m * d[0].tiles_n;
+    const int64_t wave = (int64_t)slots * XCDS;
+    if (n != 1 || tiles * best.S[0] > wave)
+        return best;
+    // one wave, one layer: the tail of the in-kernel reduction is the last
+    // arrivers' reload of every partial tile, against the ext plans
+    const int ns = d[0].K / 64;
+    best_t = best.psteps[0] + TILE_OVH +
+             (best.S[0] > 1 ? PART_STORE + TAIL_PER_PART * best.S[0] : 0.0);
+    const double out_bytes = (double)d[0].M * d[0].N * 4;
+    for (int S = 2; S <= EXT_MAX_SPLIT; S *= 2) {
+        const int ps = std::max(4, ((ns + S - 1) / S + 3) & ~3);
+        const int Se = (ns + ps - 1) / ps;
+        if (Se < 2 || tiles * Se > wave)
+            continue;
+        const double t = ps + TILE_OVH + PART_STORE + EXT_GAP +
+                         (Se + 1) * out_bytes / EXT_BYTES_PER_STEP;
+        if (t < best_t * 0.95) {
+            best.S[0] = Se;
+            best.psteps[0] = ps;
+            best.ext = true;
+            best_t = t;
         }
     }
     return best;
@@ -313,35 +417,36 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             bytes += round256((size_t)a.d[i].M * a.d[i].K * 2) + round256((size_t)a.d[i].M * 4);
         }
     }
-    // split layers: partial tiles [S][M][N] fp32, then all arrival counters
+    // split layers: fp32 partials (tiles [tiles][S][BM * BN], or plain
+    // outputs [S][M][N] for a plan summed by a separate launch), then the
+    // arrival counters of the in-kernel reductions
     size_t poff[QL_MAX_GROUP], coff[QL_MAX_GROUP];
     int ncnt = 0;
     for (int i = 0; i < n; ++i) {
         if (a.d[i].ksplit == 1)
             continue;
         poff[i] = bytes;
-        bytes += round256((size_t)a.d[i].tiles_m * a.d[i].tiles_n * a.d[i].ksplit * bm * bn * 4);
+        bytes += round256(pl.ext ? (size_t)a.d[i].ksplit * a.d[i].M * a.d[i].N * 4
+                                 : (size_t)a.d[i].tiles_m * a.d[i].tiles_n * a.d[i].ksplit *
+                                       bm * bn * 4);
     }
     const size_t cnt_off = bytes;
     for (int i = 0; i < n; ++i) {
-        if (a.d[i].ksplit == 1)
+        if (a.d[i].ksplit == 1 || pl.ext)
             continue;
         coff[i] = cnt_off + (size_t)ncnt * 4;
         ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
     }
     bytes += round256((size_t)ncnt * 4);
-    hipMemPool_t pool = workspace_pool();
-    if (!pool)
+    Workspace ws{};
+    if (!take_workspace(bytes, stream, ws))
         return QL_ERR_HIP;
-    void *ws = nullptr;
-    if (hipMallocFromPoolAsync(&ws, bytes, pool, stream) != hipSuccess)
-        return QL_ERR_HIP;
-    uint8_t *const wsb = (uint8_t *)ws;
+    uint8_t *const wsb = ws.ptr;
     hipError_t e = hipSuccess;
     for (int i = 0; i < n; ++i)
         if (a.d[i].ksplit > 1) {
             a.d[i].part = (float *)(wsb + poff[i]);
-            a.d[i].cnt = (int *)(wsb + coff[i]);
+            a.d[i].cnt = pl.ext ? nullptr : (int *)(wsb + coff[i]);
         }
     bool zeroed = false;
     const void *xs[QL_MAX_GROUP];
@@ -368,7 +473,11 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     }
     if (e == hipSuccess)
         e = launch_qgemm_wide(ord[0]->fmt, a, stream);
-    const hipError_t ef = hipFreeAsync(ws, stream);
+    for (int i = 0; i < n && pl.ext; ++i)
+        if (e == hipSuccess && a.d[i].ksplit > 1)
+            e = launch_split_sum(a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
+                                 stream);
+    const hipError_t ef = ws.own_alloc ? hipFreeAsync(ws.ptr, stream) : hipSuccess;
     return e == hipSuccess && ef == hipSuccess ? QL_OK : QL_ERR_HIP;
 }
 

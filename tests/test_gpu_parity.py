@@ -267,9 +267,11 @@ def test_forward_stored_extreme_codes_exact(gpu, orc, fmt):
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forward_split_reduction(gpu, orc, fmt):
     """Large-M shapes with few output tiles and long reductions, which the
-    fp16 path cuts into K parts summed by the last part to arrive: uneven
-    last parts (K / 64 not a multiple of the part length), ragged tiles, a
-    grouped call mixing reduction lengths; results repeat bit for bit."""
+    fp16 path cuts into K parts: single layers that fit in one wave of
+    workgroups (parts summed by a separate launch) and a grouped call mixing
+    reduction lengths (parts summed by the last part to arrive); uneven last
+    parts (K / 64 not a multiple of the part length), ragged tiles; results
+    repeat bit for bit."""
     torch, ql = gpu
     for (M, N, K) in ((300, 520, 4096), (129, 260, 8448), (2048, 64, 2304)):
         W, X = si.small_case(90 + M + N + K + fmt, M, N, K)
@@ -321,6 +323,68 @@ def test_forward_on_side_stream(gpu, orc):
     s.synchronize()
     e = rel_err(Y.cpu().numpy(), orc.forward(O.FMT_INT8, X, O.DT_BF16, codes, scales, 130))
     assert e <= TOL[O.DT_BF16]
+
+
+def test_forward_graph_workspace(gpu, orc):
+    """Captured graphs and the per-stream workspace.  A graph captured on a
+    stream whose workspace an eager call has sized keeps that buffer when a
+    later, larger call on the stream grows the workspace; a capture that
+    needs more than its stream's workspace allocates for itself.  Every
+    replay, with eager work and synchronization in between, equals the eager
+    result bit for bit."""
+    torch, ql = gpu
+    fmt = O.FMT_Q4
+    small, large = (300, 520, 1024), (640, 1024, 4096)
+    data = {}
+    for (M, N, K) in (small, large):
+        W, X = si.small_case(300 + M + K, M, N, K)
+        codes, scales = orc.quantize(fmt, W)
+        data[(M, N, K)] = (dev_x(torch, X, O.DT_BF16), torch.from_numpy(codes).cuda(),
+                           torch.from_numpy(scales.view(np.int16)).cuda(),
+                           orc.forward(fmt, X, O.DT_BF16, codes, scales, N))
+    Ys = torch.empty(small[:2], dtype=torch.float32, device="cuda")
+    Yl = torch.empty(large[:2], dtype=torch.float32, device="cuda")
+
+    def run(shape, Y):
+        xd, cd, sd, _ = data[shape]
+        ql.forward(fmt, xd, cd, sd, shape[1], Y)
+
+    s, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        run(small, Ys)
+    s.synchronize()
+    eager_s = Ys.clone()
+    assert rel_err(eager_s.cpu().numpy(), data[small][3]) <= TOL[O.DT_BF16]
+    g1 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g1, stream=s):
+        run(small, Ys)
+    with torch.cuda.stream(s):
+        run(large, Yl)  # grows the workspace of s
+    s.synchronize()
+    eager_l = Yl.clone()
+    assert rel_err(eager_l.cpu().numpy(), data[large][3]) <= TOL[O.DT_BF16]
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=s2):  # nothing sized on s2 yet
+        run(large, Yl)
+    for _ in range(3):
+        Ys.fill_(float("nan"))
+        Yl.fill_(float("nan"))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g1.replay()
+        s.synchronize()
+        assert torch.equal(Ys, eager_s)
+        with torch.cuda.stream(s):
+            run(large, Yl)
+        s.synchronize()
+        assert torch.equal(Yl, eager_l)
+        Yl.fill_(float("nan"))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s2):
+            g2.replay()
+        s2.synchronize()
+        assert torch.equal(Yl, eager_l)
 
 
 # --------------------------------------------------------------------------
