@@ -53,7 +53,7 @@
  *     its own work.  Buffers must stay alive until the stream has passed the
  *     enqueued work.  Asynchronous device faults surface at the caller's next
  *     synchronization, as in HIP itself.
- *   - The library keeps no pointer after a call returns.
+ *   - The library keeps no pointer to caller memory after a call returns.
  *   - Workspace: the fp16 path (above) needs M * K * 2 + M * 4 bytes per
  *     distinct activation tensor of a call, plus fp32 partial results when
  *     it splits a layer's reduction.  The library keeps one workspace per
