@@ -25,11 +25,13 @@
 //
 // k order.  The sum over k does not care which k a given MFMA slot holds, as
 // long as A and B agree.  Within a 64-k step, slot e of lane group g = l / 32
-// in the step's 16-k chunk q holds k = 32 g + 8 q + e.  Then every lane's k
-// over the whole step is one contiguous run of 32 = one scale block: its
-// weight codes for the step are one 16-byte (q4) or 32-byte (int8) LDS read,
-// it needs one scale per weight row per step, and each activation fragment
-// is one 16-byte chunk of the row.
+// in the step's 16-k chunk q holds k = 32 g + 8 q + e (int8), or
+// 32 g + 8 q + Q4_SLOT[e] (q4: the order in which the code conversion
+// produces an 8-k group; the activation copy is stored in that order).  Then
+// every lane's k over the whole step is one contiguous run of 32 = one scale
+// block: its weight codes for the step are one 16-byte (q4) or 32-byte
+// (int8) LDS read, it needs one scale per weight row per step, and each
+// activation fragment is one 16-byte chunk of the row.
 //
 // Tile: 256 threads (4 wavefronts) compute BM x BN = 128 x 256 of Y.  Each
 // wavefront owns a 128 x 64 strip (4 x 2 MFMA tiles of 32 x 32): every
@@ -163,37 +165,6 @@ __device__ inline uint32_t h2mul_add(uint32_t v, half2v bias, half2v sp)
     return __builtin_bit_cast(uint32_t, (__builtin_bit_cast(half2v, v) + bias) * sp);
 }
 
-// 8 int8 codes -> 8 fp16 of c * s', natural order.  byte ^ 0x80 = c + 128 is
-// placed under the fp16 pattern 0x64 (= 1024 + (c + 128)) by v_perm; adding
-// -1152 leaves c exactly.
-__device__ inline u32x4 deq_int8(uint32_t a, uint32_t b, half2v sp)
-{
-    const uint32_t x = a ^ 0x80808080u, y = b ^ 0x80808080u, hi = 0x64646464u;
-    const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
-    u32x4 r;
-    r[0] = h2mul_add(__builtin_amdgcn_perm(hi, x, 0x04010400u), bias, sp);
-    r[1] = h2mul_add(__builtin_amdgcn_perm(hi, x, 0x04030402u), bias, sp);
-    r[2] = h2mul_add(__builtin_amdgcn_perm(hi, y, 0x04010400u), bias, sp);
-    r[3] = h2mul_add(__builtin_amdgcn_perm(hi, y, 0x04030402u), bias, sp);
-    return r;
-}
-
-// 8 q4 codes (k0 in bits 0-3) -> 8 fp16 of c * s', natural order: byte j of
-// x holds codes 2j and 2j+1; v_perm puts byte j of x and of x >> 4 in the two
-// 16-bit halves, the AND keeps one nibble (u = c + 8) in each and the OR
-// sets the fp16 pattern 0x6400 | u = 1024 + u; adding -1032 leaves c.
-__device__ inline u32x4 deq_q4(uint32_t c, half2v sp)
-{
-    const uint32_t x = c ^ 0x88888888u, y = x >> 4;
-    const half2v bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
-    u32x4 r;
-    r[0] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C040C00u) & 0x000F000Fu) | 0x64006400u, bias, sp);
-    r[1] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C050C01u) & 0x000F000Fu) | 0x64006400u, bias, sp);
-    r[2] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C060C02u) & 0x000F000Fu) | 0x64006400u, bias, sp);
-    r[3] = h2mul_add((__builtin_amdgcn_perm(y, x, 0x0C070C03u) & 0x000F000Fu) | 0x64006400u, bias, sp);
-    return r;
-}
-
 // 16-byte store / load at device coherence (write-through to, and read
 // from, the level shared by all XCDs).  A store of more than 8 bytes keeps
 // reading its data registers for a cycle after issue; the compiler's hazard
@@ -279,8 +250,18 @@ __device__ inline half2v scaled_pair(uint32_t b, int f)
 }
 
 // Word w (two fp16 weights) of weight fragment (chunk q) from the lane's raw
-// codes of the step; the same conversion as deq_q4 / deq_int8, one word at a
-// time so that it can be spread between MFMAs.
+// codes of the step, one word at a time so that the conversion can be
+// spread between MFMAs.  c is placed under the fp16 exponent pattern 0x64
+// as an unsigned byte u (0x6400 | u = 1024 + u) by a v_perm whose other
+// source is 0x64646464, then (1024 + u + bias) is exact and one packed
+// multiply by s' rounds.
+//   int8: u = c + 128 (byte ^ 0x80), bias -1152; the 8 k of a word pair in
+//         natural order.
+//   q4:   u = c + 8 (nibble ^ 8), low nibbles (even k) and high nibbles (odd
+//         k) separated into bytes first, bias -1032.  A v_perm takes two
+//         bytes of one source, so the words hold (k0, k2), (k4, k6),
+//         (k1, k3), (k5, k7) of each 8-k group: slot e holds k = Q4_SLOT[e],
+//         and the activations are stored in the same order (xprep.hip).
 template <int FMT>
 __device__ inline uint32_t deq_word(const uint32_t *raw, int q, int w, half2v sp)
 {
@@ -290,11 +271,11 @@ __device__ inline uint32_t deq_word(const uint32_t *raw, int q, int w, half2v sp
         return h2mul_add(__builtin_amdgcn_perm(0x64646464u, x, (w & 1) ? 0x04030402u : 0x04010400u),
                          bias, sp);
     } else {
-        const uint32_t x = raw[q] ^ 0x88888888u, y = x >> 4;
-        constexpr uint32_t sel[4] = {0x0C040C00u, 0x0C050C01u, 0x0C060C02u, 0x0C070C03u};
+        const uint32_t c = w < 2 ? raw[q] : raw[q] >> 4;
+        const uint32_t u = (c & 0x0F0F0F0Fu) ^ 0x08080808u;  // one v_bitop3
         const half2v bias = {(_Float16)-1032.0f, (_Float16)-1032.0f};
-        return h2mul_add((__builtin_amdgcn_perm(y, x, sel[w]) & 0x000F000Fu) | 0x64006400u, bias,
-                         sp);
+        return h2mul_add(__builtin_amdgcn_perm(0x64646464u, u, (w & 1) ? 0x04030402u : 0x04010400u),
+                         bias, sp);
     }
 }
 

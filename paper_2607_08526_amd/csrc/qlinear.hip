@@ -461,8 +461,8 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         int *ex = (int *)(wsb + xoff[i] + round256((size_t)a.d[i].M * a.d[i].K * 2));
         // the first pre-pass also clears the split counters
         if (e == hipSuccess)
-            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, xh, ex, (int *)(wsb + cnt_off),
-                             zeroed ? 0 : ncnt, stream);
+            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, ord[0]->fmt == QL_FMT_Q4, xh, ex,
+                             (int *)(wsb + cnt_off), zeroed ? 0 : ncnt, stream);
         zeroed = true;
         xs[i] = xh;
         es[i] = ex;

@@ -9,7 +9,9 @@
 // multiplies its fp32 results back by 2^e[m] exactly.
 //
 // One workgroup per row; rows up to 16384 wide are read once and held in
-// registers between the max-reduction and the convert-and-store.
+// registers between the max-reduction and the convert-and-store.  For the
+// q4 kernel each 8-k group is stored in the slot order of its weight
+// conversion (qgemm_wide.hip).
 #include "internal.h"
 
 namespace qlk {
@@ -44,6 +46,9 @@ __device__ inline int row_shift(uint32_t mx, int *rexp, int m)
     return e;
 }
 
+// 8 bf16 (k0..k7) -> 8 fp16 of X * 2^-e, in natural order, or (SLOTS) in the
+// slot order of the q4 weight conversion: position e holds k = Q4_SLOT[e]
+template <bool SLOTS>
 __device__ inline u32x4 to_f16(u32x4 v, int e)
 {
     half8 h;
@@ -52,13 +57,20 @@ __device__ inline u32x4 to_f16(u32x4 v, int e)
         h[2 * j] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] << 16), -e);
         h[2 * j + 1] = (_Float16)__builtin_amdgcn_ldexpf(__uint_as_float(v[j] & 0xFFFF0000u), -e);
     }
+    if constexpr (SLOTS) {
+        half8 p;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            p[i] = h[Q4_SLOT[i]];
+        h = p;
+    }
     return __builtin_bit_cast(u32x4, h);
 }
 
 // R > 0: the row (K / 8 16-byte chunks <= 256 * R) is read once into
 // registers.  R == 0: any K, a max pass and a convert pass (the second read
 // of the row hits L2).
-template <int R>
+template <int R, bool SLOTS>
 __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__ X, int K,
                                                     uint16_t *__restrict__ Xh,
                                                     int *__restrict__ rexp,
@@ -88,7 +100,7 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
         for (int r = 0; r < R; ++r) {
             const int i = t + r * 256;
             if (i < n16)
-                out[i] = to_f16(v[r], e);
+                out[i] = to_f16<SLOTS>(v[r], e);
         }
     } else {
         for (int i = t; i < n16; i += 256) {
@@ -99,28 +111,38 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
         }
         const int e = row_shift(mx, rexp, m);
         for (int i = t; i < n16; i += 256)
-            out[i] = to_f16(row[i], e);
+            out[i] = to_f16<SLOTS>(row[i], e);
     }
+}
+
+template <bool SLOTS>
+void launch_xprep_t(const uint16_t *x, int M, int K, uint16_t *Xh, int *rexp, int *zero,
+                    int nzero, hipStream_t stream)
+{
+    const int n16 = K / 8;
+    const dim3 grid((unsigned)M), block(256);
+    if (n16 <= 256)
+        hipLaunchKernelGGL((xprep_kernel<1, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+    else if (n16 <= 512)
+        hipLaunchKernelGGL((xprep_kernel<2, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+    else if (n16 <= 1024)
+        hipLaunchKernelGGL((xprep_kernel<4, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+    else if (n16 <= 2048)
+        hipLaunchKernelGGL((xprep_kernel<8, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+    else
+        hipLaunchKernelGGL((xprep_kernel<0, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
 }
 
 }  // namespace
 
-hipError_t launch_xprep(const void *X, int M, int K, uint16_t *Xh, int *rexp, int *zero,
-                        int nzero, hipStream_t stream)
+hipError_t launch_xprep(const void *X, int M, int K, bool q4_slots, uint16_t *Xh, int *rexp,
+                        int *zero, int nzero, hipStream_t stream)
 {
     const uint16_t *x = reinterpret_cast<const uint16_t *>(X);
-    const int n16 = K / 8;
-    const dim3 grid((unsigned)M), block(256);
-    if (n16 <= 256)
-        hipLaunchKernelGGL(xprep_kernel<1>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
-    else if (n16 <= 512)
-        hipLaunchKernelGGL(xprep_kernel<2>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
-    else if (n16 <= 1024)
-        hipLaunchKernelGGL(xprep_kernel<4>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
-    else if (n16 <= 2048)
-        hipLaunchKernelGGL(xprep_kernel<8>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+    if (q4_slots)
+        launch_xprep_t<true>(x, M, K, Xh, rexp, zero, nzero, stream);
     else
-        hipLaunchKernelGGL(xprep_kernel<0>, grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        launch_xprep_t<false>(x, M, K, Xh, rexp, zero, nzero, stream);
     return hipGetLastError();
 }
 
