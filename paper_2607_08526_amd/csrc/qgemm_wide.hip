@@ -83,8 +83,13 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 #define QL_WIDE_WAVES 4
 #endif
 constexpr int WAVES = QL_WIDE_WAVES, THREADS = 64 * WAVES;
-constexpr int MSUB = QL_WIDE_MSUB, NSUB = 2, BM = 32 * MSUB, BN = WAVES * 32 * NSUB, GROUP_M = 4;
-constexpr int WGS_PER_CU = MSUB == 8 || WAVES == 8 ? 1 : 2;
+#ifndef QL_WIDE_NSUB
+#define QL_WIDE_NSUB 2
+#endif
+constexpr int MSUB = QL_WIDE_MSUB, NSUB = QL_WIDE_NSUB, BM = 32 * MSUB, BN = WAVES * 32 * NSUB;
+constexpr int WN = 32 * NSUB;  // columns per wavefront
+constexpr int GROUP_M = 4;
+constexpr int WGS_PER_CU = MSUB * NSUB > 8 || WAVES == 8 ? 1 : 2;
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
 
 template <int FMT>
@@ -102,11 +107,12 @@ struct Geo {
     static constexpr int SGROUP = 4, SSLOT = BN * 16;
     static constexpr int XLOADS = XBYTES / 16 / THREADS;
     static constexpr int CLOADS = CBYTES / 16 / THREADS;
-    static constexpr int LOADS = XLOADS + CLOADS;  // direct-to-LDS loads per step (+1 every 4)
+    static constexpr int SPT = BN / THREADS;        // scale chunks per thread per group
+    static constexpr int LOADS = XLOADS + CLOADS;  // direct-to-LDS loads per step (+SPT every 4)
     static constexpr int LDS = NST * STAGE + 2 * SSLOT;
     static_assert(XBYTES % (16 * THREADS) == 0 && CBYTES % (16 * THREADS) == 0,
                   "every thread issues the same number of 16-byte loads per stage");
-    static_assert(BN == THREADS, "one scale chunk per weight row per thread");
+    static_assert(BN % THREADS == 0, "whole scale chunks per thread");
     static_assert(WGS_PER_CU * LDS <= 160 * 1024, "resident workgroups per CU");
 };
 
@@ -214,10 +220,10 @@ struct Ctx {
     // wave-uniform bases of this tile (advanced per step by the caller)
     const uint8_t *xbase, *cbase, *sbase;
     // per-lane byte offsets from those bases, fixed for the whole K loop
-    uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff;
+    uint32_t xoff[Geo<FMT>::XLOADS], coff[Geo<FMT>::CLOADS], soff[Geo<FMT>::SPT];
     uint8_t *sring;  // the scale ring (2 slots of BN rows x 16 bytes)
     int wave, l32, g;
-    int f[NSUB];  // weight row (wave * 64 + j * 32 + l32) enters as W * 2^f[j]
+    int f[NSUB];  // weight row (wave * WN + j * 32 + l32) enters as W * 2^f[j]
 };
 
 // Issue the direct-to-LDS loads of step s into one ring stage (and, every
@@ -237,8 +243,10 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
         dma16(cb, c.coff[r], base + G::XBYTES + (r * THREADS + c.wave * 64) * 16);
     if (s % G::SGROUP == 0) {
         const int g = s / G::SGROUP;
-        dma16(c.sbase + g * 16, c.soff,
-              lds_addr(c.sring + (g & 1) * G::SSLOT) + c.wave * 64 * 16);
+#pragma unroll
+        for (int h = 0; h < G::SPT; ++h)
+            dma16(c.sbase + g * 16, c.soff[h],
+                  lds_addr(c.sring + (g & 1) * G::SSLOT) + (h * THREADS + c.wave * 64) * 16);
     }
 }
 
@@ -297,7 +305,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, in
     uint32_t raw[NSUB][G::CCH / 2 * 4];
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
-        const int row = c.wave * 64 + j * 32 + c.l32;
+        const int row = c.wave * WN + j * 32 + c.l32;
         sp[j] = scaled_pair(*reinterpret_cast<const uint16_t *>(ss + row * 16), c.f[j]);
 #pragma unroll
         for (int h = 0; h < G::CCH / 2; ++h) {
@@ -416,8 +424,10 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
         const int n = min(n0 + row, N - 1) - n0;
         c.coff[r] = (uint32_t)(n * crow_bytes + lc * 16);
     }
-    // scales: one 16-byte chunk of weight row tid per 4 steps
-    c.soff = (uint32_t)((min(n0 + tid, N - 1) - n0) * nb * 2);
+    // scales: one 16-byte chunk of weight rows h * THREADS + tid per 4 steps
+#pragma unroll
+    for (int h = 0; h < G::SPT; ++h)
+        c.soff[h] = (uint32_t)((min(n0 + h * THREADS + tid, N - 1) - n0) * nb * 2);
     c.sring = ring + NST * G::STAGE;
 
     // this part's steps of 64 k: [s0, s0 + ns); s0 is a multiple of the
@@ -439,7 +449,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     // patterns of non-negative values order as integers.
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
-        const int n = min(n0 + c.wave * 64 + j * 32 + c.l32, N - 1);
+        const int n = min(n0 + c.wave * WN + j * 32 + c.l32, N - 1);
         const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
         uint32_t mx = 0;
 #pragma unroll 4
@@ -476,7 +486,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
         // stage s+1's loads (one more when it starts a scale group) may
         // remain in flight
         if (PD == 2 && s + 1 < ns && (s + 1) % G::SGROUP == 0)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS + 1));
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS + G::SPT));
         else if (PD == 2 && s + 1 < ns)
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS));
         else
@@ -490,7 +500,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     }
 
     // Epilogue.  Register r of tile (i, j) is row i * 32 + 8 (r / 4) + 4 g +
-    // r % 4, column wave * 64 + j * 32 + l32 of the tile; it returns to the
+    // r % 4, column wave * WN + j * 32 + l32 of the tile; it returns to the
     // scale of X * W^T by the exact factor 2^(e[m] - f[n]).  Values are taken
     // from the accumulators as they are stored (no second copy of the tile
     // in registers).
@@ -536,7 +546,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
                 patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
         const int lane = tid & 63;
         const int cq = lane & 7;          // 4-column group of the row
-        const int n = n0 + c.wave * 64 + j * 32 + 4 * cq;
+        const int n = n0 + c.wave * WN + j * 32 + 4 * cq;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int rl = 8 * t + (lane >> 3);  // row within the 32-row tile
