@@ -90,6 +90,14 @@ bool gemv_ok(const LinDesc &d);
 hipError_t launch_qgemv(int fmt, const LinDesc &d, hipStream_t stream);
 
 int stream_max_m();
-hipError_t launch_qgemm_stream(int fmt, const LinDesc &d, hipStream_t stream);
+// mx: activation rows staged (4, 8, 16, 32); rw: weight rows per workgroup;
+// kw: wavefronts per workgroup; S, psteps: K parts of psteps 32-blocks each
+// (S > 1: LinDesc::part receives plain partial outputs [S][M][N])
+struct StreamPlan {
+    int mx, rw, kw, S, psteps;
+};
+StreamPlan stream_plan(int fmt, const LinDesc &d, int cus);
+hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LinDesc &d,
+                               hipStream_t stream);
 
 }  // namespace qlk

@@ -14,10 +14,17 @@
 // to the wavefront (it both issues the loads and consumes them), so no
 // barrier is needed until the final reduction.
 //
-// Decomposition.  A workgroup owns RW weight rows (16; 8 when N is small, the
-// MFMA's other 8 columns then repeat them) and all M rows; its KW wavefronts
-// split the K blocks in 8-block-aligned ranges, and their fp32 partial
-// outputs are summed through LDS in wavefront order (deterministic).
+// Decomposition.  A workgroup owns RW weight rows (8, 16, 32 or 64: NB =
+// RW / 16 MFMA column blocks per wavefront, each activation fragment feeding
+// all of them; with RW = 8 the MFMA's other 8 columns repeat the rows) and
+// all M rows, for one of S parts of the K blocks.  The activation bytes a
+// workgroup streams do not depend on RW, so wider row groups cut the
+// activation re-reads (for 32 rows at K = 8192 they are 8x the codes of an
+// 8-row group); the K parts restore the workgroup count.  Its KW wavefronts
+// split the part's blocks in 8-block-aligned ranges, and their fp32 partial
+// outputs are summed through LDS in wavefront order (deterministic).  With
+// S > 1 each part stores a plain partial output part[S][M][N] that
+// launch_split_sum adds up in part order.
 //
 // Contraction (exact, as in the other few-row path): per 32-wide block one
 // v_mfma_f32_16x16x32_bf16 of the activation fragment against the codes in
@@ -28,6 +35,9 @@
 //
 // Requirements (checked by the host): K % 256 == 0, 16-byte aligned codes,
 // scales and X.
+#include <algorithm>
+#include <cmath>
+
 #include "internal.h"
 
 namespace qlk {
@@ -102,6 +112,9 @@ __device__ inline u32x4 cvt_q4_off(uint32_t c)
 
 template <int FMT, int RW, int MX>
 struct SGeo {
+    static constexpr int NB = RW >= 16 ? RW / 16 : 1;          // MFMA column blocks
+    static constexpr int RL = RW >= 16 ? 16 : RW;               // rows per column block
+    static constexpr int NSL = (RW + 15) / 16;                  // scale loads per 32 blocks
     static constexpr int BPC = 4;                               // blocks per chunk (128 k)
     static constexpr int CB = FMT == QL_FMT_INT8 ? 128 : 64;    // code bytes per row per chunk
     static constexpr int PPR = CB / 16;                         // 16-byte pieces per code row
@@ -110,13 +123,13 @@ struct SGeo {
     static constexpr int STAGE = CODE + MX * XROW;
     static constexpr int NCI = (CODE + 1023) / 1024;            // code loads per chunk
     static constexpr int NXI = MX * XROW / 1024;                // activation loads per chunk
-    static constexpr int N = NCI + NXI;                         // loads per chunk (+1 every 8)
+    static constexpr int N = NCI + NXI;                         // loads per chunk (+NSL every 8)
     static constexpr int R = MX <= 4 ? 6 : MX <= 8 ? 4 : 3;     // ring depth (chunks)
     static constexpr int NF = MX / 16 > 1 ? MX / 16 : 1;        // 16-row activation fragments
     static constexpr int SLOT = RW * 64;                        // scales of 32 blocks
     static constexpr int WAVE = R * STAGE + 2 * SLOT;           // LDS bytes per wavefront
     static_assert((MX * XROW) % 1024 == 0, "whole activation loads");
-    static_assert((R - 1) * N + 1 <= 63, "vmcnt range");
+    static_assert((R - 1) * N + NSL <= 63, "vmcnt range");
 };
 
 // code row j's physical 16-byte piece for logical piece p (bank spread for
@@ -136,16 +149,21 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int l16 = lane & 15, lg = lane >> 4;
     const int M = d.M, N = d.N, K = d.K, nb = K >> 5;
-    const int n0 = (int)blockIdx.x * RW;
+    // consecutive workgroups take the parts of one row group: with the
+    // round-robin XCD dispatch, part p's activation range stays on few XCDs
+    const int S = d.ksplit, part = (int)blockIdx.x % S;
+    const int n0 = (int)blockIdx.x / S * RW;
     const int crow_bytes = FMT == QL_FMT_INT8 ? K : K / 2;
 
     uint8_t *const ring = lds + wave * G::WAVE;
     uint8_t *const sring = ring + G::R * G::STAGE;
 
-    // this wavefront's blocks [bw0, bw1), 8-aligned (whole scale pieces and
+    // this part's blocks [pb0, pb1) (psteps blocks, a multiple of 8), and
+    // this wavefront's share [bw0, bw1), 8-aligned (whole scale pieces and
     // chunks; nb % 8 == 0)
-    const int per = (((nb + KW - 1) / KW) + 7) & ~7;
-    const int bw0 = min(wave * per, nb), bw1 = min(bw0 + per, nb);
+    const int pb0 = min(part * d.psteps, nb), pb1 = min(pb0 + d.psteps, nb);
+    const int per = (((pb1 - pb0 + KW - 1) / KW) + 7) & ~7;
+    const int bw0 = min(pb0 + wave * per, pb1), bw1 = min(bw0 + per, pb1);
     const int nch = (bw1 - bw0) / G::BPC;
 
     // per-lane load offsets (from wave-uniform bases that advance per chunk)
@@ -165,10 +183,9 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
         const int m = o / G::XROW, pp = (o % G::XROW) / 16;  // 16 pieces per row
         xoff[r] = (uint32_t)(min(m, M - 1) * K * 2 + (pp ^ (m & 15)) * 16);
     }
-    // scales: lane -> (row j = lane / 4, piece p = lane % 4) of a 32-block run
-    const int sj = lane >> 2, sp = lane & 3;
-    const bool sact = sj < RW;
-    const int srowi = min(n0 + min(sj, RW - 1), N - 1);
+    // scales: lane -> (row j = 16 h + lane / 4, piece p = lane % 4) of a
+    // 32-block run, h < NSL
+    const int sp = lane & 3;
 
     const uint8_t *const cbase = d.codes + (FMT == QL_FMT_INT8 ? bw0 * 32 : bw0 * 16);
     const uint8_t *const xbase = reinterpret_cast<const uint8_t *>(d.X) + bw0 * 64;
@@ -182,13 +199,20 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
 #pragma unroll
         for (int r = 0; r < G::NXI; ++r)
             dma16(xbase + c * G::XROW, xoff[r], lds_addr(st + G::CODE) + r * 1024);
-        if (c % 8 == 0 && sact) {
+        if (c % 8 == 0) {
             // scales of blocks bw0 + 4c .. + 31 (pieces past the row end
             // repeat its last piece; their values are never read)
             const int g = c / 8;
-            const int b = min(bw0 + 32 * g + 8 * ((sp ^ ((sj >> 2) & 3))), nb - 8);
             const uint8_t *sb = reinterpret_cast<const uint8_t *>(d.scales);
-            dma16(sb, (uint32_t)(srowi * nb * 2 + b * 2), lds_addr(sring + (g & 1) * G::SLOT));
+#pragma unroll
+            for (int h = 0; h < G::NSL; ++h) {
+                const int sj = 16 * h + (lane >> 2);
+                const int srowi = min(n0 + min(sj, RW - 1), N - 1);
+                const int b = min(bw0 + 32 * g + 8 * ((sp ^ ((sj >> 2) & 3))), nb - 8);
+                if (sj < RW)
+                    dma16(sb, (uint32_t)(srowi * nb * 2 + b * 2),
+                          lds_addr(sring + (g & 1) * G::SLOT) + h * 1024);
+            }
         }
     };
 
@@ -206,11 +230,13 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
 
     const uint32_t negoff = FMT == QL_FMT_INT8 ? 0xC300C300u : 0xC308C308u;  // -128 / -136
     const u32x4 bneg = {negoff, negoff, negoff, negoff};
-    f32x4 acc[G::NF];
+    f32x4 acc[G::NF][G::NB];
 #pragma unroll
     for (int f = 0; f < G::NF; ++f)
-        acc[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int j = l16 % RW;  // weight row of this lane's MFMA column
+#pragma unroll
+        for (int nbi = 0; nbi < G::NB; ++nbi)
+            acc[f][nbi] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int jl = l16 % G::RL;  // weight row of this lane's MFMA column, block 0
     // activation row of this lane's A fragment f: f * 16 + mx (rows >= M are
     // never stored; with MX < 16 the fragment's other rows repeat these)
     const int mx = l16 % (MX < 16 ? MX : 16);
@@ -228,60 +254,70 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
         const uint8_t *ss = sring + ((c / 8) & 1) * G::SLOT;
 #pragma unroll
         for (int t = 0; t < G::BPC; ++t) {
-            u32x4 B;
-            if (FMT == QL_FMT_INT8) {
-                // bytes [32 t + 8 lg, +8) of row j: logical piece 2t + lg/2
-                const int pp = cswz<FMT>(j, 2 * t + (lg >> 1));
-                const uint2 v = *reinterpret_cast<const uint2 *>(st + j * G::CB + pp * 16 +
-                                                                 (lg & 1) * 8);
-                B = cvt_int8_off(v.x, v.y);
-            } else {
-                // bytes [16 t + 4 lg, +4) of row j: logical piece t
-                const int pp = cswz<FMT>(j, t);
-                const uint32_t v = *reinterpret_cast<const uint32_t *>(st + j * G::CB + pp * 16 +
-                                                                       lg * 4);
-                B = cvt_q4_off(v);
-            }
+            u32x4 B[G::NB];
+            float sc[G::NB];
             // scale of block 4c + t (within the 32-block run of this chunk)
             const int bs = (c % 8) * 4 + t;  // 0..31
-            const int spiece = (bs >> 3) ^ ((j >> 2) & 3);
-            const uint16_t sbits = *reinterpret_cast<const uint16_t *>(
-                ss + j * 64 + spiece * 16 + (bs & 7) * 2);
-            const float s = (float)__builtin_bit_cast(_Float16, sbits);
+#pragma unroll
+            for (int nbi = 0; nbi < G::NB; ++nbi) {
+                const int j = nbi * 16 + jl;
+                if (FMT == QL_FMT_INT8) {
+                    // bytes [32 t + 8 lg, +8) of row j: logical piece 2t + lg/2
+                    const int pp = cswz<FMT>(j, 2 * t + (lg >> 1));
+                    const uint2 v = *reinterpret_cast<const uint2 *>(st + j * G::CB + pp * 16 +
+                                                                     (lg & 1) * 8);
+                    B[nbi] = cvt_int8_off(v.x, v.y);
+                } else {
+                    // bytes [16 t + 4 lg, +4) of row j: logical piece t
+                    const int pp = cswz<FMT>(j, t);
+                    const uint32_t v = *reinterpret_cast<const uint32_t *>(
+                        st + j * G::CB + pp * 16 + lg * 4);
+                    B[nbi] = cvt_q4_off(v);
+                }
+                const int spiece = (bs >> 3) ^ ((j >> 2) & 3);
+                const uint16_t sbits = *reinterpret_cast<const uint16_t *>(
+                    ss + j * 64 + spiece * 16 + (bs & 7) * 2);
+                sc[nbi] = (float)__builtin_bit_cast(_Float16, sbits);
+            }
 #pragma unroll
             for (int f = 0; f < G::NF; ++f) {
                 // activation fragment f: row f * 16 + mx, bf16 [32 t + 8 lg, +8) =
-                // piece 4t + lg
+                // piece 4t + lg; its offset term is shared by the column blocks
                 const int row = f * 16 + mx;
                 const u32x4 a = *reinterpret_cast<const u32x4 *>(
                     st + G::CODE + row * G::XROW + ((4 * t + lg) ^ (row & 15)) * 16);
-                acc[f] += s * mfma(a, B, mfma(a, bneg, f32x4{0.f, 0.f, 0.f, 0.f}));
+                const f32x4 off = mfma(a, bneg, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int nbi = 0; nbi < G::NB; ++nbi)
+                    acc[f][nbi] += sc[nbi] * mfma(a, B[nbi], off);
             }
         }
     }
 
     // sum the wavefronts' partial outputs in wavefront order (the ring
     // memory is reused once every wavefront is done with it)
+    static_assert(G::NF * G::NB * KW * 64 * 16 <= KW * G::WAVE, "reduction fits the ring");
     __syncthreads();
     f32x4 *red = reinterpret_cast<f32x4 *>(lds);
 #pragma unroll
     for (int f = 0; f < G::NF; ++f)
-        red[(f * KW + wave) * 64 + lane] = acc[f];
+#pragma unroll
+        for (int nbi = 0; nbi < G::NB; ++nbi)
+            red[((f * G::NB + nbi) * KW + wave) * 64 + lane] = acc[f][nbi];
     __syncthreads();
-    if (wave == 0) {
+    float *const Yd = S > 1 ? d.part + (int64_t)part * M * N : d.Y;
+    // wavefront w sums (and stores) fragments (f, nbi) = w, w + KW, ...
+    for (int q = wave; q < G::NF * G::NB; q += KW) {
+        const int f = q / G::NB, nbi = q % G::NB;
+        f32x4 y = red[(q * KW) * 64 + lane];
+        for (int w = 1; w < KW; ++w)
+            y += red[(q * KW + w) * 64 + lane];
+        const int n = n0 + nbi * 16 + l16;
 #pragma unroll
-        for (int f = 0; f < G::NF; ++f) {
-            f32x4 y = red[f * KW * 64 + lane];
-#pragma unroll
-            for (int w = 1; w < KW; ++w)
-                y += red[(f * KW + w) * 64 + lane];
-            const int n = n0 + l16;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = f * 16 + lg * 4 + r;
-                if (l16 < RW && m < M && n < N)
-                    d.Y[(int64_t)m * N + n] = y[r];
-            }
+        for (int r = 0; r < 4; ++r) {
+            const int m = f * 16 + lg * 4 + r;
+            if (l16 < G::RL && m < M && n < N)
+                Yd[(int64_t)m * N + n] = y[r];
         }
     }
 }
@@ -292,7 +328,7 @@ hipError_t launch_kw(const LinDesc &d, hipStream_t s)
     if constexpr (KW * SGeo<FMT, RW, MX>::WAVE > 160 * 1024) {
         return hipErrorInvalidValue;  // does not fit the LDS; never chosen
     } else {
-        const dim3 grid((unsigned)((d.N + RW - 1) / RW));
+        const dim3 grid((unsigned)((d.N + RW - 1) / RW * d.ksplit));
         hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, KW>), grid, dim3(64 * KW), 0, s, d);
         return hipGetLastError();
     }
@@ -309,35 +345,113 @@ hipError_t launch_rw(int kw, const LinDesc &d, hipStream_t s)
     }
 }
 
-template <int FMT>
-hipError_t launch_fmt(const LinDesc &d, hipStream_t s)
+template <int FMT, int MX>
+hipError_t launch_mx(int rw, int kw, const LinDesc &d, hipStream_t s)
 {
-    // rows per workgroup: 16, or 8 when that would leave fewer workgroups
-    // than CUs; wavefronts per workgroup: enough for ~2048 in the grid,
-    // each with at least 16 blocks
-    const int nb = d.K / 32;
-    const bool narrow = (d.N + 15) / 16 < 256;
-    const int groups = narrow ? (d.N + 7) / 8 : (d.N + 15) / 16;
-    const int kw = (groups * 4 < 2048 && nb >= 8 * 16) ? 8 : 4;
-    if (d.M <= 4)
-        return narrow ? launch_rw<FMT, 8, 4>(kw, d, s) : launch_rw<FMT, 16, 4>(kw, d, s);
-    if (d.M <= 8)
-        return narrow ? launch_rw<FMT, 8, 8>(kw, d, s) : launch_rw<FMT, 16, 8>(kw, d, s);
-    if (d.M <= 16)
-        return narrow ? launch_rw<FMT, 8, 16>(kw, d, s) : launch_rw<FMT, 16, 16>(kw, d, s);
-    // 32 activation rows: two wavefronts per workgroup keep two workgroups
-    // per CU within the LDS; few row groups take four (one per CU)
-    return narrow ? launch_rw<FMT, 8, 32>(4, d, s) : launch_rw<FMT, 16, 32>(2, d, s);
+    switch (rw) {
+    case 8: return launch_rw<FMT, 8, MX>(kw, d, s);
+    case 16: return launch_rw<FMT, 16, MX>(kw, d, s);
+    case 32: return launch_rw<FMT, 32, MX>(kw, d, s);
+    case 64: return launch_rw<FMT, 64, MX>(kw, d, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int FMT>
+hipError_t launch_fmt(const StreamPlan &p, const LinDesc &d, hipStream_t s)
+{
+    switch (p.mx) {
+    case 4: return launch_mx<FMT, 4>(p.rw, p.kw, d, s);
+    case 8: return launch_mx<FMT, 8>(p.rw, p.kw, d, s);
+    case 16: return launch_mx<FMT, 16>(p.rw, p.kw, d, s);
+    case 32: return launch_mx<FMT, 32>(p.rw, p.kw, d, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int FMT, int RW, int MX>
+constexpr int wave_lds() { return SGeo<FMT, RW, MX>::WAVE; }
+
+template <int FMT, int MX>
+int geo(int rw, int &stage, int &ring)
+{
+    switch (rw) {
+    case 8: stage = SGeo<FMT, 8, MX>::STAGE; ring = SGeo<FMT, 8, MX>::R; return wave_lds<FMT, 8, MX>();
+    case 16: stage = SGeo<FMT, 16, MX>::STAGE; ring = SGeo<FMT, 16, MX>::R; return wave_lds<FMT, 16, MX>();
+    case 32: stage = SGeo<FMT, 32, MX>::STAGE; ring = SGeo<FMT, 32, MX>::R; return wave_lds<FMT, 32, MX>();
+    default: stage = SGeo<FMT, 64, MX>::STAGE; ring = SGeo<FMT, 64, MX>::R; return wave_lds<FMT, 64, MX>();
+    }
+}
+
+// LDS bytes per wavefront, stage bytes and ring depth of a configuration
+int stream_geo(int fmt, int mx, int rw, int &stage, int &ring)
+{
+    const bool i8 = fmt == QL_FMT_INT8;
+    switch (mx) {
+    case 4: return i8 ? geo<QL_FMT_INT8, 4>(rw, stage, ring) : geo<QL_FMT_Q4, 4>(rw, stage, ring);
+    case 8: return i8 ? geo<QL_FMT_INT8, 8>(rw, stage, ring) : geo<QL_FMT_Q4, 8>(rw, stage, ring);
+    case 16: return i8 ? geo<QL_FMT_INT8, 16>(rw, stage, ring) : geo<QL_FMT_Q4, 16>(rw, stage, ring);
+    default: return i8 ? geo<QL_FMT_INT8, 32>(rw, stage, ring) : geo<QL_FMT_Q4, 32>(rw, stage, ring);
+    }
 }
 
 }  // namespace
 
 int stream_max_m() { return 32; }
 
-hipError_t launch_qgemm_stream(int fmt, const LinDesc &d, hipStream_t stream)
+// Choice of rows per workgroup, wavefronts and K parts.  Each wavefront
+// keeps R - 1 chunks of loads in flight, so a workgroup streams its bytes
+// (activations MX * Kp * 2, codes RW * Kp * cb for its part's Kp) in about
+// bytes / (KW (R - 1) STAGE) memory round trips; the launch takes as many
+// workgroup rounds as the grid needs over the CUs, and a split adds the
+// partial round trip and the sum launch.  The plan minimizes that estimate.
+StreamPlan stream_plan(int fmt, const LinDesc &d, int cus)
 {
-    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(d, stream)
-                              : launch_fmt<QL_FMT_Q4>(d, stream);
+    constexpr double RT = 2.0;           // us per memory round trip under load
+    constexpr double SUM_LAUNCH = 3.0;   // us: split_sum launch and its gap
+    constexpr double SUM_RATE = 4.0e6;   // bytes per us the sum launch moves
+    constexpr double PART_COST = 0.3;    // us per part (fitted to a sweep of configurations)
+    const int mx = d.M <= 4 ? 4 : d.M <= 8 ? 8 : d.M <= 16 ? 16 : 32;
+    const int nb = d.K / 32;
+    const double cb = fmt == QL_FMT_INT8 ? 1.0 : 0.5;
+    StreamPlan best{mx, 16, 4, 1, nb};
+    double best_t = 1e30;
+    for (int rw : {8, 16, 32, 64}) {
+        int stage = 0, ring = 0;
+        const int wave = stream_geo(fmt, mx, rw, stage, ring);
+        for (int kw : {2, 4, 8}) {
+            if (kw * wave > 160 * 1024)
+                continue;
+            const int per_cu = std::min(160 * 1024 / (kw * wave), 2048 / (64 * kw));
+            for (int S : {1, 2, 4, 8, 16}) {
+                // parts of whole 8-block groups, at least 8 blocks per wavefront
+                const int pb = ((nb + S - 1) / S + 7) & ~7;
+                const int Se = (nb + pb - 1) / pb;
+                if (Se != S || pb < 8 * kw)
+                    continue;
+                const int64_t wgs = (int64_t)((d.N + rw - 1) / rw) * S;
+                const double bytes = (double)pb * 32 * (mx * 2 + rw * cb);
+                const double trips = std::ceil(bytes / ((double)kw * (ring - 1) * stage)) + 1;
+                const double rounds = std::ceil((double)wgs / ((double)cus * per_cu));
+                double t = rounds * trips * RT;
+                if (S > 1)
+                    t += RT + SUM_LAUNCH + (double)(S + 1) * d.M * d.N * 4 / SUM_RATE +
+                         PART_COST * S;
+                if (t < best_t * 0.97) {
+                    best_t = t;
+                    best = StreamPlan{mx, rw, kw, S, pb};
+                }
+            }
+        }
+    }
+    return best;
+}
+
+hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LinDesc &d,
+                               hipStream_t stream)
+{
+    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(p, d, stream)
+                              : launch_fmt<QL_FMT_Q4>(p, d, stream);
 }
 
 }  // namespace qlk

@@ -339,9 +339,29 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
             d.K = (int)ls[i]->K;
             const bool stream_ok = d.M <= stream_max_m() && d.K % 256 == 0 &&
                                    aligned(d.scales, 16);
-            const hipError_t e = gemv_ok(d)   ? launch_qgemv(ls[i]->fmt, d, stream)
-                                 : stream_ok ? launch_qgemm_stream(ls[i]->fmt, d, stream)
-                                             : launch_qgemm_skinny(ls[i]->fmt, d, stream);
+            hipError_t e = hipSuccess;
+            if (gemv_ok(d)) {
+                e = launch_qgemv(ls[i]->fmt, d, stream);
+            } else if (stream_ok) {
+                const StreamPlan p = stream_plan(ls[i]->fmt, d, device_cus());
+                d.ksplit = p.S;
+                d.psteps = p.psteps;
+                Workspace ws{};
+                if (p.S > 1) {
+                    if (!take_workspace(round256((size_t)p.S * d.M * d.N * 4), stream, ws))
+                        return QL_ERR_HIP;
+                    d.part = (float *)ws.ptr;
+                }
+                e = launch_qgemm_stream(ls[i]->fmt, p, d, stream);
+                if (e == hipSuccess && p.S > 1)
+                    e = launch_split_sum(d.part, p.S, d.M, d.N, d.Y, stream);
+                if (ws.own_alloc) {
+                    const hipError_t ef = hipFreeAsync(ws.ptr, stream);
+                    e = e == hipSuccess ? ef : e;
+                }
+            } else {
+                e = launch_qgemm_skinny(ls[i]->fmt, d, stream);
+            }
             if (e != hipSuccess)
                 return QL_ERR_HIP;
         }

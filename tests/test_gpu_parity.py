@@ -150,15 +150,17 @@ def test_forward_large_m_ragged_tiles(gpu, orc, fmt):
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forward_streaming_ragged(gpu, orc, fmt):
     """The weight-streaming path (M <= 32, K % 256 == 0; M <= 4 goes to the
-    GEMV when it fits): row counts around its 8- and 16-row workgroups and
-    the narrow/wide switch, K lengths that leave some wavefronts short or
-    empty and that cross the 32-block scale runs, activation stages of 8, 16
-    and 32 rows."""
+    GEMV when it fits): row counts around its 8- to 64-row workgroups,
+    K lengths that leave some wavefronts or K parts short or empty and that
+    cross the 32-block scale runs, activation stages of 8, 16 and 32 rows,
+    and long reductions cut into K parts summed by a second launch (results
+    repeat bit for bit)."""
     cases = [(1, 1, 256), (2, 7, 512), (3, 9, 768), (4, 16, 2304), (5, 17, 256),
              (8, 100, 1280), (15, 300, 2048), (16, 4100, 512), (16, 4111, 1024),
              (1, 5000, 8448), (9, 4096, 256), (6, 4097, 768), (17, 300, 2048),
              (24, 4100, 1024), (32, 513, 2304), (31, 2048, 8192), (20, 7, 256),
-             (32, 4096, 256)]
+             (32, 4096, 256), (32, 100, 8192), (12, 777, 4352), (29, 65, 12288),
+             (8, 2049, 8192)]
     for M, N, K in cases:
         W, X = si.small_case(80 + M + N + K + fmt, M, N, K)
         codes, scales = quantize_both(gpu, orc, fmt, W)
@@ -166,6 +168,8 @@ def test_forward_streaming_ragged(gpu, orc, fmt):
         Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
         e = rel_err(Yg, Yr)
         assert e <= TOL[O.DT_BF16], (M, N, K, e)
+        if K >= 4096:
+            assert np.array_equal(Yg, forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N))
 
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
