@@ -70,11 +70,24 @@ hipError_t launch_split_sum(const float *P, int S, int64_t M, int64_t N, float *
 // copy is written to match).
 constexpr int Q4_SLOT[8] = {0, 2, 4, 6, 1, 3, 5, 7};
 
-// bf16 X [M][K] -> fp16 Xh [M][K] with per-row power-of-two shifts rexp[M],
-// each 8-k group in Q4_SLOT order if q4_slots; also sets zero[0 .. nzero)
-// to 0 (the split counters of the launch that follows on the same stream).
-hipError_t launch_xprep(const void *X, int M, int K, bool q4_slots, uint16_t *Xh, int *rexp,
-                        int *zero, int nzero, hipStream_t stream);
+// One activation tensor for the pre-pass: bf16 X [M][K] -> fp16 Xh [M][K]
+// with per-row power-of-two shifts rexp[M].
+struct XprepJob {
+    const void *X;
+    int M, K;
+    uint16_t *Xh;
+    int *rexp;
+};
+struct XprepArgs {
+    XprepJob j[QL_MAX_GROUP];
+    int row_begin[QL_MAX_GROUP];
+    int n;
+};
+// All n (<= QL_MAX_GROUP) jobs in one launch, each 8-k group in Q4_SLOT
+// order if q4_slots; also sets zero[0 .. nzero) to 0 (the split counters of
+// the launch that follows on the same stream).
+hipError_t launch_xprep(const XprepJob *jobs, int n, bool q4_slots, int *zero, int nzero,
+                        hipStream_t stream);
 
 // Few-row kernel (bf16 activations, M <= skinny_max_m()): one layer per
 // launch, workgroups of 16 weight rows with K split over their wavefronts.

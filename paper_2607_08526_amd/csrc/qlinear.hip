@@ -414,7 +414,10 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         d.tile_begin = (int)total;
         total += (int64_t)d.tiles_m * d.tiles_n * d.ksplit;
     }
-    if (total >= I31)
+    int64_t rows = 0;  // pre-pass grid bound (one workgroup per activation row)
+    for (int i = 0; i < n; ++i)
+        rows += a.d[i].M;
+    if (total >= I31 || rows >= I31)
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
@@ -462,13 +465,15 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     if (!take_workspace(bytes, stream, ws))
         return QL_ERR_HIP;
     uint8_t *const wsb = ws.ptr;
-    hipError_t e = hipSuccess;
     for (int i = 0; i < n; ++i)
         if (a.d[i].ksplit > 1) {
             a.d[i].part = (float *)(wsb + poff[i]);
             a.d[i].cnt = pl.ext ? nullptr : (int *)(wsb + coff[i]);
         }
-    bool zeroed = false;
+    // one pre-pass launch over every distinct activation tensor; it also
+    // clears the split counters
+    XprepJob jobs[QL_MAX_GROUP];
+    int njobs = 0;
     const void *xs[QL_MAX_GROUP];
     const int *es[QL_MAX_GROUP];
     for (int i = 0; i < n; ++i) {
@@ -479,14 +484,12 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         }
         uint16_t *xh = (uint16_t *)(wsb + xoff[i]);
         int *ex = (int *)(wsb + xoff[i] + round256((size_t)a.d[i].M * a.d[i].K * 2));
-        // the first pre-pass also clears the split counters
-        if (e == hipSuccess)
-            e = launch_xprep(a.d[i].X, a.d[i].M, a.d[i].K, ord[0]->fmt == QL_FMT_Q4, xh, ex,
-                             (int *)(wsb + cnt_off), zeroed ? 0 : ncnt, stream);
-        zeroed = true;
+        jobs[njobs++] = XprepJob{a.d[i].X, a.d[i].M, a.d[i].K, xh, ex};
         xs[i] = xh;
         es[i] = ex;
     }
+    hipError_t e = launch_xprep(jobs, njobs, ord[0]->fmt == QL_FMT_Q4, (int *)(wsb + cnt_off),
+                                ncnt, stream);
     for (int i = 0; i < n; ++i) {
         a.d[i].X = xs[i];
         a.d[i].xexp = es[i];

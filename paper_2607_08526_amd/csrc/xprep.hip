@@ -8,8 +8,9 @@
 // rounded, by at most 2^-25 of the shifted scale.  The forward kernel
 // multiplies its fp32 results back by 2^e[m] exactly.
 //
-// One workgroup per row; rows up to 16384 wide are read once and held in
-// registers between the max-reduction and the convert-and-store.  For the
+// One workgroup per row, the rows of every activation tensor of a call in
+// one launch; rows up to 16384 wide are read once and held in registers
+// between the max-reduction and the convert-and-store.  For the
 // q4 kernel each 8-k group is stored in the slot order of its weight
 // conversion (qgemm_wide.hip).
 #include "internal.h"
@@ -69,19 +70,26 @@ __device__ inline u32x4 to_f16(u32x4 v, int e)
 
 // R > 0: the row (K / 8 16-byte chunks <= 256 * R) is read once into
 // registers.  R == 0: any K, a max pass and a convert pass (the second read
-// of the row hits L2).
+// of the row hits L2).  Workgroup b converts row b - row_begin[i] of job i
+// (all activation tensors of a call in one launch).
 template <int R, bool SLOTS>
-__global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__ X, int K,
-                                                    uint16_t *__restrict__ Xh,
-                                                    int *__restrict__ rexp,
-                                                    int *__restrict__ zero, int nzero)
+__global__ __launch_bounds__(256) void xprep_kernel(const XprepArgs a, int *__restrict__ zero,
+                                                    int nzero)
 {
-    const int m = blockIdx.x;
-    if (m == 0)
+    const int b = blockIdx.x;
+    if (b == 0)
         for (int i = threadIdx.x; i < nzero; i += 256)
             zero[i] = 0;
+    int ji = 0;
+#pragma unroll
+    for (int i = 1; i < QL_MAX_GROUP; ++i)
+        if (i < a.n && b >= a.row_begin[i])
+            ji = i;
+    const XprepJob &jb = a.j[ji];
+    const int m = b - a.row_begin[ji], K = jb.K;
+    const uint16_t *X = reinterpret_cast<const uint16_t *>(jb.X);
     const u32x4 *row = reinterpret_cast<const u32x4 *>(X + (int64_t)m * K);
-    u32x4 *out = reinterpret_cast<u32x4 *>(Xh + (int64_t)m * K);
+    u32x4 *out = reinterpret_cast<u32x4 *>(jb.Xh + (int64_t)m * K);
     const int n16 = K / 8;
     const int t = threadIdx.x;
     uint32_t mx = 0;
@@ -95,7 +103,7 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
             for (int j = 0; j < 4; ++j)
                 mx = max(mx, bf16_absmax2(v[r][j]));
         }
-        const int e = row_shift(mx, rexp, m);
+        const int e = row_shift(mx, jb.rexp, m);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int i = t + r * 256;
@@ -109,40 +117,48 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t *__restrict__
             for (int j = 0; j < 4; ++j)
                 mx = max(mx, bf16_absmax2(v[j]));
         }
-        const int e = row_shift(mx, rexp, m);
+        const int e = row_shift(mx, jb.rexp, m);
         for (int i = t; i < n16; i += 256)
             out[i] = to_f16<SLOTS>(row[i], e);
     }
 }
 
 template <bool SLOTS>
-void launch_xprep_t(const uint16_t *x, int M, int K, uint16_t *Xh, int *rexp, int *zero,
-                    int nzero, hipStream_t stream)
+void launch_xprep_t(const XprepArgs &a, int rows, int maxK, int *zero, int nzero,
+                    hipStream_t stream)
 {
-    const int n16 = K / 8;
-    const dim3 grid((unsigned)M), block(256);
+    const int n16 = maxK / 8;
+    const dim3 grid((unsigned)rows), block(256);
     if (n16 <= 256)
-        hipLaunchKernelGGL((xprep_kernel<1, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        hipLaunchKernelGGL((xprep_kernel<1, SLOTS>), grid, block, 0, stream, a, zero, nzero);
     else if (n16 <= 512)
-        hipLaunchKernelGGL((xprep_kernel<2, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        hipLaunchKernelGGL((xprep_kernel<2, SLOTS>), grid, block, 0, stream, a, zero, nzero);
     else if (n16 <= 1024)
-        hipLaunchKernelGGL((xprep_kernel<4, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        hipLaunchKernelGGL((xprep_kernel<4, SLOTS>), grid, block, 0, stream, a, zero, nzero);
     else if (n16 <= 2048)
-        hipLaunchKernelGGL((xprep_kernel<8, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        hipLaunchKernelGGL((xprep_kernel<8, SLOTS>), grid, block, 0, stream, a, zero, nzero);
     else
-        hipLaunchKernelGGL((xprep_kernel<0, SLOTS>), grid, block, 0, stream, x, K, Xh, rexp, zero, nzero);
+        hipLaunchKernelGGL((xprep_kernel<0, SLOTS>), grid, block, 0, stream, a, zero, nzero);
 }
 
 }  // namespace
 
-hipError_t launch_xprep(const void *X, int M, int K, bool q4_slots, uint16_t *Xh, int *rexp,
-                        int *zero, int nzero, hipStream_t stream)
+hipError_t launch_xprep(const XprepJob *jobs, int n, bool q4_slots, int *zero, int nzero,
+                        hipStream_t stream)
 {
-    const uint16_t *x = reinterpret_cast<const uint16_t *>(X);
+    XprepArgs a{};
+    int rows = 0, maxK = 0;
+    for (int i = 0; i < n; ++i) {
+        a.j[i] = jobs[i];
+        a.row_begin[i] = rows;
+        rows += jobs[i].M;
+        maxK = jobs[i].K > maxK ? jobs[i].K : maxK;
+    }
+    a.n = n;
     if (q4_slots)
-        launch_xprep_t<true>(x, M, K, Xh, rexp, zero, nzero, stream);
+        launch_xprep_t<true>(a, rows, maxK, zero, nzero, stream);
     else
-        launch_xprep_t<false>(x, M, K, Xh, rexp, zero, nzero, stream);
+        launch_xprep_t<false>(a, rows, maxK, zero, nzero, stream);
     return hipGetLastError();
 }
 
