@@ -364,9 +364,14 @@ def cpu_baseline(step, si, target_s):
             orc.forward(O.FMT_Q4, X, O.DT_BF16, codes, scales, N, rows=np.arange(rows))
         return time.perf_counter() - t
 
-    t1 = run(1)
-    rows = int(max(1, min(step.M, target_s / max(t1, 1e-3))))
+    # size the sample from a short run, then once more from the sample
+    # itself (a one-row run overstates the per-row time)
+    t1 = run(8)
+    rows = int(max(1, min(step.M, 8 * target_s / max(t1, 1e-3))))
     t = run(rows)
+    if t < 0.8 * target_s and rows < step.M:
+        rows = int(max(1, min(step.M, rows * target_s / max(t, 1e-3))))
+        t = run(rows)
     flops = rows * sum(2.0 * N * K for _, N, K in lin)
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
             "kind": "oracle",

@@ -537,7 +537,8 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     float *const patch = reinterpret_cast<float *>(ring + 1024) + c.wave * 1024;
     // destination: Y, or this part's plain partial output when the parts
     // are summed by a separate launch (split_sum_kernel)
-    float *const Yd = S > 1 && !d.cnt ? d.part + (int64_t)part * M * N : d.Y;
+    const bool to_part = S > 1 && !d.cnt;
+    float *const Yd = to_part ? d.part + (int64_t)part * M * N : d.Y;
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
 #pragma unroll
         for (int h = 0; h < 4; ++h)
@@ -556,10 +557,14 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
                 continue;
             float *const dst = Yd + (int64_t)m * N + n;
             if (n + 3 < N && (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0) {
-                // streaming store: Y is not read again here, and letting it
+                // streaming store for Y (not read again here: letting it
                 // allocate would evict the activation and code lines that
-                // other tiles still re-read
-                __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
+                // other tiles still re-read); partials, which the sum launch
+                // reads next, stay cacheable
+                if (to_part)
+                    *reinterpret_cast<f32x4 *>(dst) = v;
+                else
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -656,7 +661,27 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
 
 // Sum of the S plain partial outputs P[s][M][N] of a split launch, in part
 // order (the same sum as the in-kernel reduction): Y = ((P0 + P1) + P2) ...
+// Loads go out eight parts at a time so that a thread has eight in flight.
 // V4: 16-byte groups (N % 4 == 0, Y 16-byte aligned), else single floats.
+template <typename T>
+__device__ inline T sum_parts(const T *p, int S, int64_t count)
+{
+    T y = p[0];
+    int q = 1;
+    for (; q + 8 <= S; q += 8) {
+        T v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            v[u] = p[(q + u) * count];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            y += v[u];
+    }
+    for (; q < S; ++q)
+        y += p[q * count];
+    return y;
+}
+
 template <bool V4>
 __global__ __launch_bounds__(256) void split_sum_kernel(const float *__restrict__ P, int S,
                                                         int64_t count, float *__restrict__ Y)
@@ -664,16 +689,10 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float *__restrict_
     const int64_t stride = (int64_t)gridDim.x * 256;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) {
         if constexpr (V4) {
-            const f32x4 *p = reinterpret_cast<const f32x4 *>(P) + i;
-            f32x4 y = p[0];
-            for (int q = 1; q < S; ++q)
-                y += p[q * count];
+            const f32x4 y = sum_parts(reinterpret_cast<const f32x4 *>(P) + i, S, count);
             __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(Y) + i);
         } else {
-            float y = P[i];
-            for (int q = 1; q < S; ++q)
-                y += P[i + q * count];
-            Y[i] = y;
+            Y[i] = sum_parts(P + i, S, count);
         }
     }
 }
