@@ -346,6 +346,61 @@ def block_int8(torch, ql, si):
             "weight_GBps": round(wbytes / t / 1e9, 1)}
 
 
+def paper_widths(torch, ql, si):
+    """The paper's two DiT widths (q4, distinct weights per block) at the
+    tokens of one 10 s clip: one step = every block's grouped call, timed as
+    a HIP graph over R copies of the step's weights (R x footprint >= 512 MB,
+    past the last-level cache)."""
+    import numpy as np
+    import concurrent.futures as cf
+    dev = torch.device("cuda")
+    out = []
+    for w, (name, d, nblk) in enumerate(si.PAPER_WIDTHS):
+        xa, xb = si.paper_activations(w)
+        xa_d = torch.from_numpy(xa.view("int16")).to(dev)
+        xb_d = torch.from_numpy(xb.view("int16")).to(dev)
+        lin = si.block_linears(d)
+        M = xa.shape[0]
+        Ys = [torch.empty((M, N), dtype=torch.float32, device=dev) for _, N, _ in lin]
+        jobs = [(blk, i) for blk in range(nblk) for i in range(len(lin))]
+        with cf.ThreadPoolExecutor(max_workers=8) as pool:
+            Ws = list(pool.map(lambda bi: si.paper_weight(w, *bi), jobs))
+        q, wbytes = [], 0
+        for W in Ws:
+            c, sc = ql.quantize(ql.FMT_Q4, torch.from_numpy(W).to(dev))
+            q.append((c, sc))
+            wbytes += c.numel() + 2 * sc.numel()
+        del Ws
+        R = max(1, -(-512 * 10**6 // wbytes))
+        copies = [q] + [[(c.clone(), sc.clone()) for c, sc in q] for _ in range(R - 1)]
+        groups = []
+        for qq in copies:
+            for blk in range(nblk):
+                ents = []
+                for i, (_, N, K) in enumerate(lin):
+                    c, sc = qq[blk * len(lin) + i]
+                    ents.append((ql.FMT_Q4, xb_d if K == 4 * d else xa_d, c, sc, N, Ys[i]))
+                groups.append(ql.make_group(ents))
+
+        def fn():
+            for g in groups:
+                ql.block_forward(None, group=g)
+
+        med, lo, hi = graph_time(torch, fn, reps=10, warm=3)
+        t = med / R * 1e-3
+        flops = nblk * sum(2.0 * M * N * K for _, N, K in lin)
+        act = nblk * (M * d * 2 * 2 + sum(M * N * 4 for _, N, _ in lin))  # X read, Y written
+        out.append({"name": name, "d": d, "blocks": nblk, "tokens": M, "fmt": "q4",
+                    "ms_per_step": round(t * 1e3, 4), "TFLOPs": round(flops / t / 1e12, 1),
+                    "mfma_frac": round(flops / t / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                    "weight_GBps": round(wbytes / t / 1e9, 1),
+                    "hbm_frac": round((wbytes + act) / t / 1e9 / HBM_PEAK_GBPS, 4),
+                    "copies": R})
+        del groups, copies, q
+        torch.cuda.synchronize()
+    return out
+
+
 def cpu_baseline(step, si, target_s):
     """The fp64 oracle on a bounded sample of the same workload: rows of
     block 0's four linears (all N), after the oracle's own quantization."""
@@ -420,7 +475,8 @@ def main():
 
     if args.sweeps_only:
         print(json.dumps({"skinny": skinny_sweep(torch, ql, si),
-                          "block_int8": block_int8(torch, ql, si)}), flush=True)
+                          "block_int8": block_int8(torch, ql, si),
+                          "paper_widths": paper_widths(torch, ql, si)}), flush=True)
         return
 
     step = Step(torch, ql, si, keep_host_block0=not args.no_cpu_baseline)
@@ -468,6 +524,7 @@ def main():
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)
+        res["paper_widths"] = paper_widths(torch, ql, si)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(step, si, args.cpu_seconds)
     print(json.dumps(res), flush=True)

@@ -21,6 +21,13 @@ Workloads (the DiT shapes the paper's medium model implies: width d, FFN 4d,
   step_q4       24 such blocks, q4; W seeds 100 + 4*block + i, X as above
   skinny        int8/q4 x (N,K) in {(8192,2048),(2048,8192)} x M in
                 {1,8,32,128}, bf16 X; W seed 200 + variant, X seed 300 + M
+  paper widths  the paper's two DiT configurations (small-music: 20 blocks at
+                d = 1024; medium: 24 blocks at d = 1536; Related Work,
+                generative audio models, and Experiments, setup) at the
+                token count of one 10 s clip: ~107 latent frames at ~10.7 Hz
+                (Methodology, the runtime) x 2 guidance branches = 214;
+                W seeds 1000 * (width index + 1) + 4 * block + i, X seed
+                900 + width index
 """
 import numpy as np
 
@@ -39,6 +46,11 @@ N_BLOCKS = 24
 def block_linears(d=D_MODEL):
     return [("qkv", 3 * d, d), ("out", d, d), ("ffn_up", 4 * d, d), ("ffn_down", d, 4 * d)]
 
+
+# (name, d, blocks) of the paper's DiT configurations, and the tokens of a
+# 10 s clip with both guidance branches
+PAPER_WIDTHS = [("small_music", 1024, 20), ("medium", 1536, 24)]
+PAPER_TOKENS = 2 * 107
 
 SKINNY_SHAPES = [(8192, 2048), (2048, 8192)]
 SKINNY_M = [1, 8, 32, 128]
@@ -101,6 +113,17 @@ def block_int8_weight(i, d=D_MODEL):
 
 def step_q4_weight(blk, i, d=D_MODEL):
     return block_weights(i, 100 + 4 * blk, d)
+
+
+def paper_weight(w, blk, i):
+    """Weight i of block blk of paper width w (index into PAPER_WIDTHS)."""
+    d = PAPER_WIDTHS[w][1]
+    return block_weights(i, 1000 * (w + 1) + 4 * blk, d)
+
+
+def paper_activations(w):
+    d = PAPER_WIDTHS[w][1]
+    return block_activations(M=PAPER_TOKENS, d=d, seed=900 + w)
 
 
 def skinny_variants():

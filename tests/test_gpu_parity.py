@@ -461,6 +461,20 @@ def test_step_q4_config_sampled_blocks(gpu, orc, blk):
     assert max(errs) <= TOL[O.DT_BF16]
 
 
+@pytest.mark.parametrize("w", range(len(si.PAPER_WIDTHS)))
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_paper_width_block(gpu, orc, w, fmt):
+    """The last block of each of the paper's DiT widths (d = 1024, 1536) at
+    the token count of one 10 s clip (214 rows: partial 128-row tiles, few
+    tiles per layer), every output row against the oracle."""
+    xa, xb = si.paper_activations(w)
+    blk = si.PAPER_WIDTHS[w][2] - 1
+    weights = [si.paper_weight(w, blk, i) for i in range(4)]
+    errs = run_block(gpu, orc, fmt, weights, xa, xb, np.arange(xa.shape[0]))
+    print(f"paper width {si.PAPER_WIDTHS[w][0]} fmt {fmt} errs", errs)
+    assert max(errs) <= TOL[O.DT_BF16]
+
+
 @pytest.mark.parametrize("v,fmt,N,K", si.skinny_variants())
 def test_skinny_configs(gpu, orc, v, fmt, N, K):
     W = si.skinny_weight(v, N, K)
