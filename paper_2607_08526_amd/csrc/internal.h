@@ -61,9 +61,15 @@ int wide_max_split();
 int wide_wgs_per_cu();  // resident workgroups per CU (LDS and register budget)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
-// Y[M][N] = sum over s < S of P[s][M][N], added in order s = 0, 1, ...
-hipError_t launch_split_sum(const float *P, int S, int64_t M, int64_t N, float *Y,
-                            hipStream_t stream);
+// Y[M][N] = sum over s < S of P[s][M][N], added in order s = 0, 1, ..., for
+// n (<= QL_MAX_GROUP) split layers in one launch
+struct SplitSum {
+    const float *P;
+    int S;
+    int64_t M, N;
+    float *Y;
+};
+hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream);
 
 // Slot order of an 8-k group in the q4 fp16 path: MFMA operand slot e holds
 // k = Q4_SLOT[e] (the order the q4 code conversion yields; the activation

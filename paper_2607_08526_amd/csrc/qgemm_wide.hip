@@ -659,10 +659,21 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     }
 }
 
-// Sum of the S plain partial outputs P[s][M][N] of a split launch, in part
+// Sum of the S plain partial outputs P[s][M][N] of a split layer, in part
 // order (the same sum as the in-kernel reduction): Y = ((P0 + P1) + P2) ...
 // Loads go out eight parts at a time so that a thread has eight in flight.
-// V4: 16-byte groups (N % 4 == 0, Y 16-byte aligned), else single floats.
+struct SumJob {
+    const float *P;
+    float *Y;
+    int S, v4;
+    int64_t count;  // outputs per part, in 16-byte groups if v4
+};
+struct SumArgs {
+    SumJob j[QL_MAX_GROUP];
+    int64_t begin[QL_MAX_GROUP + 1];
+    int n;
+};
+
 template <typename T>
 __device__ inline T sum_parts(const T *p, int S, int64_t count)
 {
@@ -682,33 +693,50 @@ __device__ inline T sum_parts(const T *p, int S, int64_t count)
     return y;
 }
 
-template <bool V4>
-__global__ __launch_bounds__(256) void split_sum_kernel(const float *__restrict__ P, int S,
-                                                        int64_t count, float *__restrict__ Y)
+// One launch for the split layers of a call: flat index space over every
+// job's outputs, 16-byte groups for jobs that allow them (N % 4 == 0, Y
+// 16-byte aligned), single floats otherwise.
+__global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
 {
     const int64_t stride = (int64_t)gridDim.x * 256;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) {
-        if constexpr (V4) {
-            const f32x4 y = sum_parts(reinterpret_cast<const f32x4 *>(P) + i, S, count);
-            __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(Y) + i);
+    for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < a.begin[a.n]; x += stride) {
+        int ji = 0;
+#pragma unroll
+        for (int i = 1; i < QL_MAX_GROUP; ++i)
+            if (i < a.n && x >= a.begin[i])
+                ji = i;
+        const SumJob &jb = a.j[ji];
+        const int64_t i = x - a.begin[ji];
+        if (jb.v4) {
+            const f32x4 y = sum_parts(reinterpret_cast<const f32x4 *>(jb.P) + i, jb.S, jb.count);
+            __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(jb.Y) + i);
         } else {
-            Y[i] = sum_parts(P + i, S, count);
+            jb.Y[i] = sum_parts(jb.P + i, jb.S, jb.count);
         }
     }
 }
 
 }  // namespace
 
-hipError_t launch_split_sum(const float *P, int S, int64_t M, int64_t N, float *Y,
-                            hipStream_t stream)
+hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream)
 {
-    const bool v4 = N % 4 == 0 && ((uintptr_t)Y & 15) == 0;
-    const int64_t count = v4 ? M * N / 4 : M * N;
-    const unsigned grid = (unsigned)std::min<int64_t>((count + 255) / 256, 4096);
-    if (v4)
-        hipLaunchKernelGGL(split_sum_kernel<true>, dim3(grid), dim3(256), 0, stream, P, S, count, Y);
-    else
-        hipLaunchKernelGGL(split_sum_kernel<false>, dim3(grid), dim3(256), 0, stream, P, S, count, Y);
+    SumArgs a{};
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        const SplitSum &q = sums[i];
+        const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & 15) == 0;
+        const int64_t count = v4 ? q.M * q.N / 4 : q.M * q.N;
+        a.j[i] = SumJob{q.P, q.Y, q.S, v4 ? 1 : 0, count};
+        a.begin[i] = total;
+        total += count;
+    }
+    for (int i = n; i <= QL_MAX_GROUP; ++i)
+        a.begin[i] = total;
+    a.n = n;
+    if (total == 0)
+        return hipSuccess;
+    const unsigned grid = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(split_sum_kernel, dim3(grid), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -160,10 +160,10 @@ int device_cus()
 // takes a contiguous range of every layer's parts (in layer order) and
 // starts them in order on its first free slot (wide_wgs_per_cu() per CU).
 //
-// A single-layer launch that fits in one wave of workgroup slots has no
-// other work to hide the last parts' in-kernel reduction behind: there the
-// parts may instead store plain partial outputs that one more launch adds
-// up at full-chip bandwidth (ext), which also allows more and shorter parts.
+// A launch that fits in one wave of workgroup slots has no other work to
+// hide the last parts' in-kernel reduction behind: there the parts may
+// instead store plain partial outputs that one more launch adds up at
+// full-chip bandwidth (ext), which also allows more and shorter parts.
 struct SplitPlan {
     int S[QL_MAX_GROUP], psteps[QL_MAX_GROUP];
     bool ext;
@@ -243,27 +243,52 @@ SplitPlan plan_splits(const LinDesc *d, int n)
             best_parts = total_parts;
         }
     }
-    const int64_t tiles = (int64_t)d[0].tiles_m * d[0].tiles_n;
     const int64_t wave = (int64_t)slots * XCDS;
-    if (n != 1 || tiles * best.S[0] > wave)
+    int64_t parts = 0;
+    for (int i = 0; i < n; ++i)
+        parts += (int64_t)d[i].tiles_m * d[i].tiles_n * best.S[i];
+    if (parts > wave)
         return best;
-    // one wave, one layer: the tail of the in-kernel reduction is the last
-    // arrivers' reload of every partial tile, against the ext plans
-    const int ns = d[0].K / 64;
-    best_t = best.psteps[0] + TILE_OVH +
-             (best.S[0] > 1 ? PART_STORE + TAIL_PER_PART * best.S[0] : 0.0);
-    const double out_bytes = (double)d[0].M * d[0].N * 4;
-    for (int S = 2; S <= EXT_MAX_SPLIT; S *= 2) {
-        const int ps = std::max(4, ((ns + S - 1) / S + 3) & ~3);
-        const int Se = (ns + ps - 1) / ps;
-        if (Se < 2 || tiles * Se > wave)
+    // one wave: the tail of the in-kernel reduction is the last arrivers'
+    // reload of every partial tile, against plans whose parts a separate
+    // launch adds up (every layer cut to one common part length)
+    best_t = 0.0;
+    for (int i = 0; i < n; ++i)
+        best_t = std::max(best_t, best.psteps[i] + TILE_OVH +
+                                      (best.S[i] > 1 ? PART_STORE + TAIL_PER_PART * best.S[i]
+                                                     : 0.0));
+    std::vector<int> lens;
+    for (int i = 0; i < n; ++i)
+        for (int L = d[i].K / 64; L >= 4; L /= 2)
+            lens.push_back(L);
+    for (const int L : lens) {
+        SplitPlan pl{};
+        pl.ext = true;
+        int64_t np = 0;
+        int longest = 0, split = 0;
+        double sum_bytes = 0.0;
+        for (int i = 0; i < n; ++i) {
+            const int ns = d[i].K / 64;
+            int ps = std::min(ns, std::max(4, (L + 3) & ~3));
+            int S = (ns + ps - 1) / ps;
+            if (S > EXT_MAX_SPLIT) {
+                ps = ((ns + EXT_MAX_SPLIT - 1) / EXT_MAX_SPLIT + 3) & ~3;
+                S = (ns + ps - 1) / ps;
+            }
+            pl.S[i] = S;
+            pl.psteps[i] = ps;
+            np += (int64_t)d[i].tiles_m * d[i].tiles_n * S;
+            longest = std::max(longest, ps);
+            if (S > 1) {
+                ++split;
+                sum_bytes += (S + 1) * (double)d[i].M * d[i].N * 4;
+            }
+        }
+        if (!split || np > wave)
             continue;
-        const double t = ps + TILE_OVH + PART_STORE + EXT_GAP +
-                         (Se + 1) * out_bytes / EXT_BYTES_PER_STEP;
+        const double t = longest + TILE_OVH + PART_STORE + EXT_GAP + sum_bytes / EXT_BYTES_PER_STEP;
         if (t < best_t * 0.95) {
-            best.S[0] = Se;
-            best.psteps[0] = ps;
-            best.ext = true;
+            best = pl;
             best_t = t;
         }
     }
@@ -353,8 +378,10 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
                     d.part = (float *)ws.ptr;
                 }
                 e = launch_qgemm_stream(ls[i]->fmt, p, d, stream);
-                if (e == hipSuccess && p.S > 1)
-                    e = launch_split_sum(d.part, p.S, d.M, d.N, d.Y, stream);
+                if (e == hipSuccess && p.S > 1) {
+                    const SplitSum q{d.part, p.S, d.M, d.N, d.Y};
+                    e = launch_split_sum(&q, 1, stream);
+                }
                 if (ws.own_alloc) {
                     const hipError_t ef = hipFreeAsync(ws.ptr, stream);
                     e = e == hipSuccess ? ef : e;
@@ -496,10 +523,14 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     }
     if (e == hipSuccess)
         e = launch_qgemm_wide(ord[0]->fmt, a, stream);
-    for (int i = 0; i < n && pl.ext; ++i)
-        if (e == hipSuccess && a.d[i].ksplit > 1)
-            e = launch_split_sum(a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
-                                 stream);
+    if (pl.ext && e == hipSuccess) {
+        SplitSum sums[QL_MAX_GROUP];
+        int ns = 0;
+        for (int i = 0; i < n; ++i)
+            if (a.d[i].ksplit > 1)
+                sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y};
+        e = launch_split_sum(sums, ns, stream);
+    }
     const hipError_t ef = ws.own_alloc ? hipFreeAsync(ws.ptr, stream) : hipSuccess;
     return e == hipSuccess && ef == hipSuccess ? QL_OK : QL_ERR_HIP;
 }
