@@ -49,6 +49,8 @@ def load(path=None):
         lib.oracle_forward_rows.argtypes = [ctypes.c_int, p, ctypes.c_int, i64, i64, p, p,
                                             i64, p, i64, p]
         lib.oracle_forward_rows.restype = ctypes.c_int
+        lib.oracle_forward_f16_rows.argtypes = [p, ctypes.c_int, i64, i64, p, i64, p, i64, p]
+        lib.oracle_forward_f16_rows.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
@@ -134,6 +136,24 @@ class Oracle:
             Y = np.empty((len(rows), N), dtype=np.float64)
             st = self.lib.oracle_forward_rows(fmt, _ptr(X), xdt, M, K, _ptr(codes),
                                               _ptr(scales), N, _ptr(rows), len(rows), _ptr(Y))
+        if st != OK:
+            raise OracleError(st)
+        return Y
+
+
+    def forward_f16(self, X, xdt, W16, rows=None):
+        """Y (fp64) = X * W^T for fp16 weight bit patterns W16 [N][K] (the
+        unquantized reference), optionally only for the listed rows of X."""
+        X = np.ascontiguousarray(X, dtype=np.float32 if xdt == DT_F32 else np.uint16)
+        W16 = np.ascontiguousarray(W16, dtype=np.uint16)
+        M, K = X.shape
+        N = W16.shape[0]
+        rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = M if rows is None else len(rows_arr)
+        Y = np.empty((nrows, N), dtype=np.float64)
+        st = self.lib.oracle_forward_f16_rows(
+            _ptr(X), xdt, M, K, _ptr(W16), N,
+            None if rows_arr is None else _ptr(rows_arr), nrows, _ptr(Y))
         if st != OK:
             raise OracleError(st)
         return Y

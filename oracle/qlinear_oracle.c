@@ -28,6 +28,9 @@
  *       code 2j+1 in its high nibble, both two's complement.
  *   R5  Y = X * W^T in fp64 from the stored codes and scales:
  *       Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k].
+ *   R6  the unquantized reference (the fp16 weights the paper's table of
+ *       precisions measures q8 / q4 against): Y = X * W^T in fp64 from fp16
+ *       weight bit patterns W[N][K].
  *
  * Exactness of the arithmetic used for R2/R3 (why fp64 is enough):
  *   - absmax / Q: the fp64 quotient differs from the exact one by less than
@@ -275,6 +278,34 @@ int oracle_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K,
                    const uint8_t *codes, const uint16_t *scales, int64_t N, double *Y)
 {
     return oracle_forward_rows(fmt, X, xdt, M, K, codes, scales, N, NULL, M, Y);
+}
+
+/* ---- unquantized reference (R6) --------------------------------------- */
+
+/* Y[i][n] = sum_k X[m][k] * W[n][k] for rows m = rows[i] (rows == NULL:
+ * m = i), W fp16 bit patterns [N][K]; fp64. */
+int oracle_forward_f16_rows(const void *X, int xdt, int64_t M, int64_t K, const uint16_t *W,
+                            int64_t N, const int64_t *rows, int64_t nrows, double *Y)
+{
+    if (xdt != ORC_DT_F32 && xdt != ORC_DT_BF16)
+        return ORC_ERR_INVALID;
+    if (N <= 0 || K <= 0 || M < 0 || nrows < 0)
+        return ORC_ERR_SHAPE;
+    for (int64_t i = 0; i < nrows; ++i) {
+        int64_t m = rows ? rows[i] : i;
+        if (m < 0 || m >= M)
+            return ORC_ERR_SHAPE;
+    }
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < nrows; ++i)
+        for (int64_t n = 0; n < N; ++n) {
+            const int64_t m = rows ? rows[i] : i;
+            double y = 0.0;
+            for (int64_t k = 0; k < K; ++k)
+                y += x_at(X, xdt, K, m, k) * oracle_f16_to_f64(W[n * K + k]);
+            Y[i * N + n] = y;
+        }
+    return ORC_OK;
 }
 
 /* Number of threads the parallel loops above use (reported beside timings). */

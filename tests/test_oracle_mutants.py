@@ -47,6 +47,13 @@ MUTANTS = [
      "code_at(fmt, codes, K, n, k);\n        }", "code_at(fmt, codes, K, n, (k + ORC_BLOCK) % K);\n        }"),
     ("bf16 decode shift",
      "(uint32_t)b << 16", "(uint32_t)b << 15"),
+    ("fp16-weight forward transposed weight index",
+     "oracle_f16_to_f64(W[n * K + k])", "oracle_f16_to_f64(W[k * N + n])"),
+    ("fp16-weight forward shifted activation index",
+     "y += x_at(X, xdt, K, m, k) * oracle_f16_to_f64(W",
+     "y += x_at(X, xdt, K, m, (k + 1) % K) * oracle_f16_to_f64(W"),
+    ("fp16-weight forward ignores the row list",
+     "const int64_t m = rows ? rows[i] : i;", "const int64_t m = i;"),
 ]
 
 
@@ -68,6 +75,9 @@ def pin_cases():
     cases += [(pins.test_f16_decode_all_patterns, ())]
     cases += [(pins.test_f16_encode_exact_values_roundtrip, ())]
     cases += [(pins.test_f16_encode_midpoints_and_neighbours, ())]
+    cases += [(pins.test_forward_f16_integer_bruteforce, (x,)) for x in (0, 1)]
+    cases += [(pins.test_forward_f16_equals_quantized_at_power_of_two_scales, (f,)) for f in F]
+    cases += [(pins.test_forward_f16_subnormal_and_signed_zero_weights, ())]
     return cases
 
 

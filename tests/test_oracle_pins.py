@@ -311,6 +311,72 @@ def test_forward_rows_subset_matches_full(orc):
 
 
 # --------------------------------------------------------------------------
+# unquantized reference: fp16 weights (R6)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("xdt", [O.DT_F32, O.DT_BF16])
+def test_forward_f16_integer_bruteforce(orc, xdt):
+    """Small integers are exact in fp16, bf16 and fp32: the product is an
+    integer matmul, checked against exact integer arithmetic (a transposed
+    or mis-indexed operand fails on the non-square shapes)."""
+    rng = np.random.default_rng(61 + xdt)
+    M, N, K = 5, 7, 96
+    Xi = rng.integers(-100, 101, (M, K))
+    Wi = rng.integers(-2048, 2049, (N, K))
+    W16 = Wi.astype(np.float16).view(np.uint16)
+    X = Xi.astype(np.float32)
+    if xdt == O.DT_BF16:
+        import synth_inputs as si
+        X = si.f32_to_bf16_bits(X)
+    Y = orc.forward_f16(X, xdt, W16)
+    assert np.array_equal(Y, (Xi @ Wi.T).astype(np.float64))
+    rows = np.array([4, 0, 2])
+    assert np.array_equal(orc.forward_f16(X, xdt, W16, rows=rows), Y[rows])
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_forward_f16_equals_quantized_at_power_of_two_scales(orc, fmt):
+    """With power-of-two scales every dequantized weight c * s is exact in
+    fp16, so the unquantized product of those fp16 weights must equal the
+    quantized product (itself pinned above) exactly: both are sums of exact
+    fp64 products well inside 53 bits."""
+    import synth_inputs as si
+    rng = np.random.default_rng(71 + fmt)
+    Q = QMAX[fmt]
+    M, N, K = 6, 9, 256
+    C = rng.integers(-Q - 1, Q + 1, (N, K))
+    e = rng.integers(-8, -5, (N, K // 32))
+    scales = (np.float16(2.0) ** e.astype(np.float16)).astype(np.float16).view(np.uint16)
+    if fmt == O.FMT_INT8:
+        codes = C.astype(np.int8).view(np.uint8)
+    else:
+        u = (C & 0xF).astype(np.uint8)
+        codes = (u[:, 0::2] | (u[:, 1::2] << 4)).astype(np.uint8)
+    Wd = C * np.repeat(2.0 ** e, 32, axis=1)
+    W16 = Wd.astype(np.float16)
+    assert np.array_equal(W16.astype(np.float64), Wd)  # exact in fp16
+    X = si.f32_to_bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+    assert np.array_equal(orc.forward_f16(X, O.DT_BF16, W16.view(np.uint16)),
+                          orc.forward(fmt, X, O.DT_BF16, codes, scales, N))
+
+
+def test_forward_f16_subnormal_and_signed_zero_weights(orc):
+    """fp16 subnormal weights decode exactly (2^-24 steps) and -0 adds
+    nothing."""
+    K = 64
+    W16 = np.zeros((3, K), np.uint16)
+    W16[0, :] = 0x0001            # 2^-24
+    W16[1, :] = 0x83FF            # -(1023 * 2^-24), largest negative subnormal
+    W16[2, :] = 0x8000            # -0
+    X = np.ones((2, K), np.float32)
+    X[1] = 2.0
+    Y = orc.forward_f16(X, O.DT_F32, W16)
+    assert np.array_equal(Y[:, 0], np.array([K, 2 * K]) * 2.0 ** -24)
+    assert np.array_equal(Y[:, 1], -np.array([K, 2 * K]) * 1023 * 2.0 ** -24)
+    assert np.array_equal(Y[:, 2], np.zeros(2))
+
+
+# --------------------------------------------------------------------------
 # error conventions
 # --------------------------------------------------------------------------
 
