@@ -28,9 +28,9 @@
  * contracted with the exact codes and fp32 block partials (error a few fp32
  * roundings).  bf16 activations at larger M take the fp16 path: X is copied
  * exactly to fp16 with a power-of-two shift per row, each weight enters the
- * matrix cores as fp16(c * s * 2^f) with one shift f per 128-row weight tile,
- * so the one extra rounding is that of c * s to 11 significant bits
- * (relative 2^-12 per weight; about 2e-4 of max |Y| at transformer shapes).
+ * matrix cores as fp16(c * s * 2^f) with one shift f per weight row, so the
+ * one extra rounding is that of c * s to 11 significant bits (relative
+ * 2^-12 per weight; about 2e-4 of max |Y| at transformer shapes).
  *
  * Data formats (all buffers are DEVICE memory owned by the caller):
  *   W       fp32 [N][K]
@@ -39,6 +39,14 @@
  *                        low nibble and code 2j+1 in its high nibble, both
  *                        two's complement (the stored codes -128 / -8 are
  *                        accepted by the forward pass, never produced)
+ *           QL_FMT_F16:  fp16 bit patterns, uint16 [N][K] -- unquantized
+ *                        weights, the reference point the paper's table of
+ *                        precisions measures q8 / q4 against (Experiments,
+ *                        runtime benchmarks); forward only, bf16
+ *                        activations, K % 256 == 0 (else
+ *                        QL_ERR_UNSUPPORTED), scales unused (may be NULL);
+ *                        Y = X * W^T on the fp16 path (X shifted to fp16
+ *                        exactly, the weights exact, fp32 accumulation)
  *   scales  fp16 bit patterns, uint16 [N][K/32]
  *   X       QL_DT_BF16: bf16 bit patterns, uint16 [M][K]; QL_DT_F32: fp32
  *   Y       fp32 [M][N]
@@ -93,13 +101,15 @@ typedef enum {
     QL_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
 } ql_status;
 
-typedef enum { QL_FMT_Q4 = 4, QL_FMT_INT8 = 8 } ql_fmt;   /* block fixed at 32 along K */
+typedef enum { QL_FMT_Q4 = 4, QL_FMT_INT8 = 8, QL_FMT_F16 = 16 } ql_fmt;
+                                               /* q4 / int8: block fixed at 32 along K */
 typedef enum { QL_DT_F32 = 0, QL_DT_BF16 = 1 } ql_dtype; /* activation dtype; Y is fp32 */
 
 #define QL_BLOCK 32
 
-/* Bytes of the packed codes of an N x K weight: N*K (int8) or N*K/2 (q4).
- * Returns 0 for an unknown format or a non-positive size. */
+/* Bytes of the packed codes of an N x K weight: N*K (int8), N*K/2 (q4) or
+ * 2*N*K (the fp16 weights of QL_FMT_F16).  Returns 0 for an unknown format
+ * or a non-positive size. */
 size_t qlinear_codes_bytes(int fmt, int64_t N, int64_t K);
 
 /* Bytes of the fp16 scales of an N x K weight: N * (K/32) * 2.

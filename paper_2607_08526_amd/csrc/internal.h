@@ -58,7 +58,7 @@ hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
 int wide_tile_bm();
 int wide_tile_bn();
 int wide_max_split();
-int wide_wgs_per_cu();  // resident workgroups per CU (LDS and register budget)
+int wide_wgs_per_cu(int fmt);  // resident workgroups per CU (LDS and register budget)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
 // Y[M][N] = sum over s < S of P[s][M][N], added in order s = 0, 1, ..., for

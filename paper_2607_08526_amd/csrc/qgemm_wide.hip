@@ -90,30 +90,36 @@ constexpr int MSUB = QL_WIDE_MSUB, NSUB = QL_WIDE_NSUB, BM = 32 * MSUB, BN = WAV
 constexpr int WN = 32 * NSUB;  // columns per wavefront
 constexpr int GROUP_M = 4;
 constexpr int WGS_PER_CU = MSUB * NSUB > 8 || WAVES == 8 ? 1 : 2;
+// fp16 weights (the unquantized reference format) take 128 bytes per row per
+// stage: one workgroup per CU
+template <int FMT>
+constexpr int wgs_per_cu() { return FMT == QL_FMT_F16 ? 1 : WGS_PER_CU; }
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
 
 template <int FMT>
 struct Geo {
     // ring depth (LDS budget)
-    static constexpr int NST = WGS_PER_CU == 1 || FMT == QL_FMT_Q4 ? 3 : 2;
+    static constexpr int NST = wgs_per_cu<FMT>() == 1 || FMT == QL_FMT_Q4 ? 3 : 2;
     static constexpr int XBYTES = BM * 64 * 2;                 // activations per stage
-    static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : 32;  // code bytes per row per stage
+    static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : FMT == QL_FMT_Q4 ? 32 : 128;  // weight
+                                                               // bytes per row per stage
     static constexpr int CCH = CROW / 16;                      // 16-byte chunks per code row
     static constexpr int CBYTES = BN * CROW;
     static constexpr int STAGE = XBYTES + CBYTES;
     // scales travel apart: one 16-byte chunk (8 blocks = 4 steps) per weight
     // row every 4 steps, into a 2-slot ring; a per-step load would cost one
     // memory request per row for 4 bytes
-    static constexpr int SGROUP = 4, SSLOT = BN * 16;
+    static constexpr int SGROUP = 4, SSLOT = FMT == QL_FMT_F16 ? 0 : BN * 16;
     static constexpr int XLOADS = XBYTES / 16 / THREADS;
     static constexpr int CLOADS = CBYTES / 16 / THREADS;
-    static constexpr int SPT = BN / THREADS;        // scale chunks per thread per group
+    static constexpr int SPT = FMT == QL_FMT_F16 ? 0 : BN / THREADS;  // scale chunks per
+                                                                     // thread per group
     static constexpr int LOADS = XLOADS + CLOADS;  // direct-to-LDS loads per step (+SPT every 4)
     static constexpr int LDS = NST * STAGE + 2 * SSLOT;
     static_assert(XBYTES % (16 * THREADS) == 0 && CBYTES % (16 * THREADS) == 0,
                   "every thread issues the same number of 16-byte loads per stage");
     static_assert(BN % THREADS == 0, "whole scale chunks per thread");
-    static_assert(WGS_PER_CU * LDS <= 160 * 1024, "resident workgroups per CU");
+    static_assert(wgs_per_cu<FMT>() * LDS <= 160 * 1024, "resident workgroups per CU");
 };
 
 __device__ inline constexpr int vmcnt_imm(int v)
@@ -129,6 +135,8 @@ __device__ inline int xswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 template <int FMT>
 __device__ inline int cswz(int row)
 {
+    if constexpr (FMT == QL_FMT_F16)
+        return xswz(row);  // 8 chunks per row, as the activations
     return FMT == QL_FMT_INT8 ? ((row >> 1) ^ (row >> 3)) & 3 : ((row >> 2) ^ (row >> 3)) & 1;
 }
 
@@ -273,7 +281,9 @@ __device__ inline half2v scaled_pair(uint32_t b, int f)
 template <int FMT>
 __device__ inline uint32_t deq_word(const uint32_t *raw, int q, int w, half2v sp)
 {
-    if constexpr (FMT == QL_FMT_INT8) {
+    if constexpr (FMT == QL_FMT_F16) {
+        return raw[4 * q + w];  // the weights themselves, natural k order
+    } else if constexpr (FMT == QL_FMT_INT8) {
         const uint32_t x = raw[2 * q + (w >> 1)] ^ 0x80808080u;
         const half2v bias = {(_Float16)-1152.0f, (_Float16)-1152.0f};
         return h2mul_add(__builtin_amdgcn_perm(0x64646464u, x, (w & 1) ? 0x04030402u : 0x04010400u),
@@ -306,7 +316,8 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, in
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
         const int row = c.wave * WN + j * 32 + c.l32;
-        sp[j] = scaled_pair(*reinterpret_cast<const uint16_t *>(ss + row * 16), c.f[j]);
+        if constexpr (FMT != QL_FMT_F16)
+            sp[j] = scaled_pair(*reinterpret_cast<const uint16_t *>(ss + row * 16), c.f[j]);
 #pragma unroll
         for (int h = 0; h < G::CCH / 2; ++h) {
             const int lc = c.g * (G::CCH / 2) + h;
@@ -361,7 +372,7 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, in
 }
 
 template <int FMT>
-__global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const GroupArgs args)
+__global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
     constexpr int NST = G::NST, PD = NST - 1;  // prefetch distance in steps
@@ -395,7 +406,7 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     const int M = d.M, N = d.N, K = d.K, nb = K >> 5;
     const int m0 = tm * BM, n0 = tn * BN;
     const int tid = threadIdx.x;
-    const int crow_bytes = FMT == QL_FMT_INT8 ? K : K / 2;
+    const int crow_bytes = FMT == QL_FMT_INT8 ? K : FMT == QL_FMT_Q4 ? K / 2 : 2 * K;
 
     Ctx<FMT> c;
     c.wave = tid >> 6;
@@ -449,6 +460,10 @@ __global__ __launch_bounds__(THREADS, WGS_PER_CU) void qgemm_wide_kernel(const G
     // patterns of non-negative values order as integers.
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
+        if constexpr (FMT == QL_FMT_F16) {
+            c.f[j] = 0;  // fp16 weights enter as they are
+            continue;
+        }
         const int n = min(n0 + c.wave * WN + j * 32 + c.l32, N - 1);
         const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
         uint32_t mx = 0;
@@ -743,15 +758,20 @@ hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream)
 int wide_tile_bm() { return BM; }
 int wide_tile_bn() { return BN; }
 int wide_max_split() { return MAXSPLIT; }
-int wide_wgs_per_cu() { return WGS_PER_CU; }
+int wide_wgs_per_cu(int fmt)
+{
+    return fmt == QL_FMT_F16 ? wgs_per_cu<QL_FMT_F16>() : WGS_PER_CU;
+}
 
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
 {
     dim3 grid((unsigned)args.total_tiles), block(THREADS);
     if (fmt == QL_FMT_INT8)
         hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_INT8>, grid, block, 0, stream, args);
-    else
+    else if (fmt == QL_FMT_Q4)
         hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_Q4>, grid, block, 0, stream, args);
+    else
+        hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_F16>, grid, block, 0, stream, args);
     return hipGetLastError();
 }
 

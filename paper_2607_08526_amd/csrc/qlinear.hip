@@ -19,19 +19,26 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 bool fmt_ok(int f) { return f == QL_FMT_INT8 || f == QL_FMT_Q4; }
 
+// formats the forward product takes: the quantized ones and fp16 weights
+bool fwd_fmt_ok(int f) { return fmt_ok(f) || f == QL_FMT_F16; }
+
 int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
                  const uint16_t *scales, int64_t N, const float *Y)
 {
-    if (!fmt_ok(fmt) || (xdt != QL_DT_F32 && xdt != QL_DT_BF16))
+    const bool f16 = fmt == QL_FMT_F16;
+    if (!fwd_fmt_ok(fmt) || (xdt != QL_DT_F32 && xdt != QL_DT_BF16))
         return QL_ERR_INVALID;
     if (M < 0 || N <= 0 || K <= 0 || K % QL_BLOCK)
         return QL_ERR_SHAPE;
     if (M >= I31 || N >= I31 || K >= I31)
         return QL_ERR_UNSUPPORTED;
-    if (!codes || !scales || (M > 0 && (!X || !Y)))
+    // fp16 weights: the fp16 path's kernel only (bf16 X, whole 256-k steps)
+    if (f16 && (xdt != QL_DT_BF16 || K % 256 || K >= ((int64_t)1 << 22)))
+        return QL_ERR_UNSUPPORTED;
+    if (!codes || (!f16 && !scales) || (M > 0 && (!X || !Y)))
         return QL_ERR_INVALID;
-    if (!aligned(codes, 16) || !aligned(scales, 2) || (M > 0 && (!aligned(X, 16) ||
-                                                                 !aligned(Y, 4))))
+    if (!aligned(codes, 16) || (!f16 && !aligned(scales, 2)) ||
+        (M > 0 && (!aligned(X, 16) || !aligned(Y, 4))))
         return QL_ERR_ALIGN;
     return QL_OK;
 }
@@ -158,7 +165,7 @@ int device_cus()
 // trip per part.  The plan is the one with the shortest estimated makespan
 // under the hardware's dispatch: workgroup p runs on XCD p % 8, each XCD
 // takes a contiguous range of every layer's parts (in layer order) and
-// starts them in order on its first free slot (wide_wgs_per_cu() per CU).
+// starts them in order on its first free slot (wide_wgs_per_cu(fmt) per CU).
 //
 // A launch that fits in one wave of workgroup slots has no other work to
 // hide the last parts' in-kernel reduction behind: there the parts may
@@ -203,9 +210,9 @@ double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
     return worst;
 }
 
-SplitPlan plan_splits(const LinDesc *d, int n)
+SplitPlan plan_splits(int fmt, const LinDesc *d, int n)
 {
-    const int slots = std::max(1, wide_wgs_per_cu() * device_cus() / XCDS);
+    const int slots = std::max(1, wide_wgs_per_cu(fmt) * device_cus() / XCDS);
     SplitPlan best{};
     double best_t = 0.0;
     int best_parts = 0;
@@ -297,10 +304,10 @@ SplitPlan plan_splits(const LinDesc *d, int n)
 
 // Recently used plans, keyed by the group's shapes (the search above costs
 // tens of microseconds of host time).
-SplitPlan cached_plan(const LinDesc *d, int n)
+SplitPlan cached_plan(int fmt, const LinDesc *d, int n)
 {
     struct Entry {
-        int n, cus;
+        int n, cus, slots;
         int64_t shape[QL_MAX_GROUP][3];
         SplitPlan pl;
     };
@@ -311,6 +318,7 @@ SplitPlan cached_plan(const LinDesc *d, int n)
     Entry key{};
     key.n = n;
     key.cus = device_cus();
+    key.slots = wide_wgs_per_cu(fmt);
     for (int i = 0; i < n; ++i) {
         key.shape[i][0] = d[i].M;
         key.shape[i][1] = d[i].N;
@@ -319,11 +327,11 @@ SplitPlan cached_plan(const LinDesc *d, int n)
     {
         std::lock_guard<std::mutex> g(mu);
         for (int e = 0; e < used; ++e)
-            if (cache[e].n == n && cache[e].cus == key.cus &&
+            if (cache[e].n == n && cache[e].cus == key.cus && cache[e].slots == key.slots &&
                 std::equal(&cache[e].shape[0][0], &cache[e].shape[0][0] + 3 * n, &key.shape[0][0]))
                 return cache[e].pl;
     }
-    key.pl = plan_splits(d, n);
+    key.pl = plan_splits(fmt, d, n);
     std::lock_guard<std::mutex> g(mu);
     cache[next] = key;
     next = (next + 1) % SLOTS;
@@ -351,7 +359,8 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     int64_t maxM = 0;
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->M);
-    if (!xf32 && maxM <= skinny_max_m()) {
+    const bool f16 = ls[0]->fmt == QL_FMT_F16;
+    if (!xf32 && !f16 && maxM <= skinny_max_m()) {
         // few rows: streaming-bound, one launch per layer
         for (int i = 0; i < n; ++i) {
             LinDesc d{};
@@ -404,6 +413,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     for (int i = 0; i < n; ++i)
         wide = wide && ls[i]->K % 256 == 0 && ls[i]->K < ((int64_t)1 << 23) &&
                aligned(ls[i]->scales, 16);
+    wide = wide || f16;  // fp16 weights: this kernel at every M (checked by check_linear)
     const int bm = wide ? wide_tile_bm() : tile_bm(t);
     const int bn = wide ? wide_tile_bn() : tile_bn(t);
 
@@ -431,7 +441,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     }
     SplitPlan pl{};
     if (wide)
-        pl = cached_plan(a.d, n);
+        pl = cached_plan(ord[0]->fmt, a.d, n);
     for (int i = 0; i < n; ++i) {
         LinDesc &d = a.d[i];
         if (wide) {
@@ -541,9 +551,11 @@ extern "C" {
 
 size_t qlinear_codes_bytes(int fmt, int64_t N, int64_t K)
 {
-    if (!fmt_ok(fmt) || N <= 0 || K <= 0)
+    if (!fwd_fmt_ok(fmt) || N <= 0 || K <= 0)
         return 0;
-    return fmt == QL_FMT_INT8 ? (size_t)N * (size_t)K : (size_t)N * (size_t)(K / 2);
+    return fmt == QL_FMT_INT8 ? (size_t)N * (size_t)K
+         : fmt == QL_FMT_Q4   ? (size_t)N * (size_t)(K / 2)
+                              : 2 * (size_t)N * (size_t)K;
 }
 
 size_t qlinear_scales_bytes(int64_t N, int64_t K)
@@ -605,15 +617,16 @@ int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
             return st;
     }
     // partition the non-empty layers by (fmt, xdt); each class is one launch
-    const ql_linear *cls[4][QL_MAX_GROUP];
-    int cnt[4] = {0, 0, 0, 0};
+    const ql_linear *cls[6][QL_MAX_GROUP];
+    int cnt[6] = {0, 0, 0, 0, 0, 0};
     for (int i = 0; i < n_lin; ++i) {
         if (lin[i].M == 0)
             continue;
-        const int c = (lin[i].fmt == QL_FMT_INT8 ? 2 : 0) + (lin[i].xdt == QL_DT_BF16 ? 1 : 0);
+        const int f = lin[i].fmt == QL_FMT_Q4 ? 0 : lin[i].fmt == QL_FMT_INT8 ? 1 : 2;
+        const int c = 2 * f + (lin[i].xdt == QL_DT_BF16 ? 1 : 0);
         cls[c][cnt[c]++] = &lin[i];
     }
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < 6; ++c) {
         const int st = launch_group(cls[c], cnt[c], stream);
         if (st != QL_OK)
             return st;

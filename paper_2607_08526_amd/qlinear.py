@@ -14,6 +14,7 @@ from . import build as _build
 
 FMT_Q4 = 4
 FMT_INT8 = 8
+FMT_F16 = 16  # unquantized fp16 weights (forward only; scales unused)
 DT_F32 = 0
 DT_BF16 = 1
 BLOCK = 32
@@ -150,7 +151,9 @@ def _xdt(X):
 
 
 def forward(fmt, X, codes, scales, N, Y=None, stream=None):
-    """Y [M][N] fp32 = X [M][K] . dequant(codes, scales)^T.  Asynchronous."""
+    """Y [M][N] fp32 = X [M][K] . dequant(codes, scales)^T.  Asynchronous.
+    FMT_F16: codes are the fp16 weights [N][K] (any 2-byte dtype), scales
+    None."""
     M, K = X.shape
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
@@ -166,7 +169,7 @@ def make_group(entries):
     for i, (fmt, X, codes, scales, N, Y) in enumerate(entries):
         M, K = X.shape
         arr[i] = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
-                         scales.data_ptr(), Y.data_ptr())
+                         scales.data_ptr() if scales is not None else 0, Y.data_ptr())
     return arr
 
 

@@ -392,6 +392,70 @@ def test_forward_graph_workspace(gpu, orc):
 
 
 # --------------------------------------------------------------------------
+# unquantized reference: fp16 weights through the same large-M kernel
+# --------------------------------------------------------------------------
+
+def f16_bits(W):
+    return np.ascontiguousarray(W, dtype=np.float32).astype(np.float16).view(np.uint16)
+
+
+def test_forward_f16_weights(gpu, orc):
+    """fp16 weights (QL_FMT_F16) against the oracle's unquantized product:
+    ragged row and column counts, one to several 64-k steps, small M (the
+    same kernel serves every M), a split long reduction; results repeat bit
+    for bit."""
+    torch, ql = gpu
+    for (M, N, K) in ((1, 40, 256), (65, 200, 512), (300, 520, 1280), (129, 17, 1024),
+                      (214, 3072, 1024), (128, 64, 8192)):
+        W, X = si.small_case(500 + M + N + K, M, N, K)
+        W16 = f16_bits(W)
+        wd = torch.from_numpy(W16.view(np.int16)).cuda()
+        Y = ql.forward(ql.FMT_F16, dev_x(torch, X, O.DT_BF16), wd, None, N)
+        torch.cuda.synchronize()
+        Yg = Y.cpu().numpy()
+        Yr = orc.forward_f16(X, O.DT_BF16, W16)
+        e = rel_err(Yg, Yr)
+        assert e <= TOL[O.DT_BF16], (M, N, K, e)
+        Y2 = ql.forward(ql.FMT_F16, dev_x(torch, X, O.DT_BF16), wd, None, N)
+        torch.cuda.synchronize()
+        assert np.array_equal(Yg, Y2.cpu().numpy())
+
+
+def test_forward_f16_block_and_errors(gpu, orc):
+    """A grouped call of one block's four fp16-weight linears (sampled rows
+    against the oracle), and the calls the format does not take."""
+    torch, ql = gpu
+    xa, xb = si.paper_activations(1)
+    d = si.PAPER_WIDTHS[1][1]
+    entries, refs = [], []
+    rows = sample_rows(xa.shape[0], 8, 3)
+    for i, (_, N, K) in enumerate(si.block_linears(d)):
+        W16 = f16_bits(si.paper_weight(1, 0, i))
+        X = xb if K == 4 * d else xa
+        Y = torch.full((X.shape[0], N), float("nan"), dtype=torch.float32, device="cuda")
+        entries.append((ql.FMT_F16, dev_x(torch, X, O.DT_BF16),
+                        torch.from_numpy(W16.view(np.int16)).cuda(), None, N, Y))
+        refs.append(orc.forward_f16(X, O.DT_BF16, W16, rows=rows))
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    for e, Yr in zip(entries, refs):
+        assert rel_err(e[5].cpu().numpy()[rows], Yr) <= TOL[O.DT_BF16]
+    w = torch.zeros((16, 512), dtype=torch.int16, device="cuda")
+    for X, status in ((torch.zeros((4, 512), dtype=torch.float32, device="cuda"), 5),
+                      (torch.zeros((4, 512), dtype=torch.int16, device="cuda"), None)):
+        if status is None:
+            ql.forward(ql.FMT_F16, X, w, None, 16)
+            continue
+        with pytest.raises(ql.QLinearError) as err:
+            ql.forward(ql.FMT_F16, X, w, None, 16)
+        assert err.value.status == status  # fp32 activations: unsupported
+    with pytest.raises(ql.QLinearError) as err:
+        ql.forward(ql.FMT_F16, torch.zeros((4, 96), dtype=torch.int16, device="cuda"),
+                   torch.zeros((16, 96), dtype=torch.int16, device="cuda"), None, 16)
+    assert err.value.status == 5  # K % 256 != 0: unsupported
+
+
+# --------------------------------------------------------------------------
 # the workload configurations
 # --------------------------------------------------------------------------
 
