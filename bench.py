@@ -149,7 +149,7 @@ def summarize_traffic(fetch_dir, write_dir):
 class Step:
     """The 24-block q4 linear stack, quantized and resident on the GPU."""
 
-    def __init__(self, torch, ql, si, keep_host_block0=True):
+    def __init__(self, torch, ql, si, keep_host_block0=True, with_f16=True):
         self.torch, self.ql = torch, ql
         dev = torch.device("cuda")
         xa, xb = si.block_activations()
@@ -160,6 +160,9 @@ class Step:
         M = xa.shape[0]
         self.Y = [torch.empty((M, N), dtype=torch.float32, device=dev) for _, N, _ in lin]
         self.blocks, self.groups = [], []
+        # the same weights as fp16 (the unquantized reference format),
+        # converted on the device as input preparation
+        self.groups_f16, self.keep_f16 = [], []
         self.W0 = []
         self.weight_bytes = 0
         t0 = time.time()
@@ -168,17 +171,25 @@ class Step:
         pool = cf.ThreadPoolExecutor(max_workers=8)
         gen = pool.map(lambda bi: si.step_q4_weight(*bi), jobs)  # drawn in parallel, in order
         for blk in range(si.N_BLOCKS):
-            ents = []
+            ents, ents16 = [], []
             for i, (name, N, K) in enumerate(lin):
                 W = next(gen)
                 if blk == 0 and keep_host_block0:
                     self.W0.append(W)
-                codes, scales = ql.quantize(ql.FMT_Q4, torch.from_numpy(W).to(dev))
+                Wd = torch.from_numpy(W).to(dev)
+                codes, scales = ql.quantize(ql.FMT_Q4, Wd)
                 self.weight_bytes += codes.numel() + 2 * scales.numel()
                 X = self.xb if K == 4 * si.D_MODEL else self.xa
                 ents.append((ql.FMT_Q4, X, codes, scales, N, self.Y[i]))
+                if with_f16:
+                    w16 = Wd.to(torch.float16).view(torch.int16)
+                    self.keep_f16.append(w16)
+                    ents16.append((ql.FMT_F16, X, w16, None, N, self.Y[i]))
+                del Wd
             self.blocks.append(ents)
             self.groups.append(ql.make_group(ents))
+            if with_f16:
+                self.groups_f16.append(ql.make_group(ents16))
         pool.shutdown()
         torch.cuda.synchronize()
         log(f"step weights quantized on the GPU in {time.time() - t0:.1f}s "
@@ -194,6 +205,24 @@ class Step:
             self.ql.block_forward(None, group=g)
             if events is not None:
                 events[b][1].record()
+
+
+def time_f16_step(torch, ql, step, steps, warmup):
+    """The same step with the weights in fp16 (QL_FMT_F16), same timing
+    method as the q4 step's total."""
+    def run():
+        for g in step.groups_f16:
+            ql.block_forward(None, group=g)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        run()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
 
 
 def time_step(torch, step, steps, warmup):
@@ -520,6 +549,15 @@ def main():
             "flops_per_launch": step.flops_per_block,
             "avg_launch_ms": round(avg_launch_ms, 5),
         },
+    }
+    f16_ms = time_f16_step(torch, ql, step, max(3, args.steps // 2), args.warmup)
+    res["fp16_reference"] = {
+        "note": "the same 24-block step with the weights in fp16 (QL_FMT_F16, the "
+                "unquantized reference format) through the same kernel",
+        "ms_per_step": round(f16_ms, 4),
+        "TFLOPs": round(step.flops / (f16_ms * 1e-3) / 1e12, 1),
+        "weight_GBps": round(sum(2 * w.numel() for w in step.keep_f16) / (f16_ms * 1e-3) / 1e9, 1),
+        "q4_step_speedup": round(f16_ms / ms_per_step, 3),
     }
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
