@@ -53,6 +53,7 @@ def test_size_helpers(lib):
     assert lib.qlinear_codes_bytes(INT8, 6144, 2048) == 6144 * 2048
     assert lib.qlinear_codes_bytes(Q4, 6144, 2048) == 6144 * 1024
     assert lib.qlinear_codes_bytes(5, 6144, 2048) == 0
+    assert lib.qlinear_codes_bytes(16, 6144, 2048) == 2 * 6144 * 2048  # fp16 weights
     assert lib.qlinear_scales_bytes(6144, 2048) == 6144 * 64 * 2
     assert lib.qlinear_scales_bytes(6144, 2047) == 0
     assert lib.qlinear_scales_bytes(0, 64) == 0
