@@ -52,9 +52,10 @@ hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
                         hipStream_t stream);
 
 // Large-M kernel of the fp16 path (bf16 activations): 128 x 256 tiles,
-// direct-to-LDS pipeline.  Each LinDesc's X points to the fp16 activations
-// prepared by launch_xprep and xexp to their per-row shifts; K % 256 == 0 and
-// 16-byte aligned scales.
+// direct-to-LDS pipeline; fmt int8, q4 or fp16 weights (QL_FMT_F16: codes
+// are the fp16 weights, no scales).  Each LinDesc's X points to the fp16
+// activations prepared by launch_xprep and xexp to their per-row shifts;
+// K % 256 == 0 and 16-byte aligned scales.
 int wide_tile_bm();
 int wide_tile_bn();
 int wide_max_split();

@@ -56,6 +56,11 @@
 // banks.  A direct-to-LDS load writes lane t's data to slot base + t, so the
 // swizzle is applied by choosing which global chunk each lane fetches.
 //
+// fp16 weights (QL_FMT_F16, the unquantized reference format) go through the
+// same kernel: the weight words are the MFMA operand as they are (no
+// conversion, f = 0, no scales), 128 bytes per row per stage, one workgroup
+// per CU.
+//
 // Tile order: within a layer, groups of 4 row tiles walked row-tile fastest;
 // each of the 8 XCDs takes a contiguous range of one layer's tiles (L2
 // reuse), and every layer of a grouped launch is spread over all XCDs.  Long
@@ -74,8 +79,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
-// MSUB = 8: 256 x 256 tiles, one workgroup (one wavefront per SIMD, 256
-// accumulators per lane) per CU; MSUB = 4: 128 x 256 tiles, two per CU.
+// Tile shape (compile-time): each of WAVES wavefronts owns MSUB x NSUB MFMA
+// tiles of 32 x 32.  The shipped shape is MSUB = 4, NSUB = 2, WAVES = 4:
+// 128 x 256 tiles, two workgroups per CU.  Shapes with 256 accumulators per
+// lane (MSUB * NSUB = 16: one workgroup, one wavefront per SIMD) or 8
+// wavefronts build too; measured on the q4 step they were slower.
 #ifndef QL_WIDE_MSUB
 #define QL_WIDE_MSUB 4
 #endif
