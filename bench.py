@@ -461,7 +461,7 @@ def cpu_baseline(step, si, target_s):
             "kind": "oracle",
             "sample": f"fp64 oracle forward of {rows} of 2048 token rows through block 0's four "
                       f"q4 linears (all outputs), {t:.1f}s; the oracle's own quantization of "
-                      f"those 50.3M weights took {tq:.1f}s (not in the rate)"}
+                      f"those 50.3M weights took {tq:.2f}s (not in the rate)"}
 
 
 def traffic_entry():
