@@ -17,6 +17,8 @@ FMT_INT8 = 8
 DT_F32 = 0
 DT_BF16 = 1
 BLOCK = 32
+ACT_NONE = 0
+ACT_GELU = 1
 
 OK = 0
 ERR_INVALID = 1
@@ -51,6 +53,8 @@ def load(path=None):
         lib.oracle_forward_rows.restype = ctypes.c_int
         lib.oracle_forward_f16_rows.argtypes = [p, ctypes.c_int, i64, i64, p, i64, p, i64, p]
         lib.oracle_forward_f16_rows.restype = ctypes.c_int
+        lib.oracle_epilogue.argtypes = [p, i64, i64, p, p, ctypes.c_int, p]
+        lib.oracle_epilogue.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
@@ -154,6 +158,22 @@ class Oracle:
         st = self.lib.oracle_forward_f16_rows(
             _ptr(X), xdt, M, K, _ptr(W16), N,
             None if rows_arr is None else _ptr(rows_arr), nrows, _ptr(Y))
+        if st != OK:
+            raise OracleError(st)
+        return Y
+
+
+    def epilogue(self, Y, bias=None, act=ACT_NONE, residual=None, rows=None):
+        """act(Y + bias[n]) + residual[m][n] (fp64) on a product Y of the
+        listed rows of X (all rows if None); returns a new array."""
+        Y = np.array(Y, dtype=np.float64, order="C", copy=True)
+        nrows, N = Y.shape
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        r = None if residual is None else np.ascontiguousarray(residual, dtype=np.float32)
+        rw = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        st = self.lib.oracle_epilogue(_ptr(Y), nrows, N, None if rw is None else _ptr(rw),
+                                      None if b is None else _ptr(b), act,
+                                      None if r is None else _ptr(r))
         if st != OK:
             raise OracleError(st)
         return Y

@@ -31,6 +31,10 @@
  *   R6  the unquantized reference (the fp16 weights the paper's table of
  *       precisions measures q8 / q4 against): Y = X * W^T in fp64 from fp16
  *       weight bit patterns W[N][K].
+ *   R7  the epilogue a linear layer of a DiT block may carry (bias, the
+ *       feed-forward's GELU, the residual add): Y = act(P + bias[n]) +
+ *       residual[m][n] on the fp64 product P, act the identity or the GELU
+ *       in its exact form x * Phi(x) = x * (1 + erf(x / sqrt 2)) / 2.
  *
  * Exactness of the arithmetic used for R2/R3 (why fp64 is enough):
  *   - absmax / Q: the fp64 quotient differs from the exact one by less than
@@ -305,6 +309,37 @@ int oracle_forward_f16_rows(const void *X, int xdt, int64_t M, int64_t K, const 
                 y += x_at(X, xdt, K, m, k) * oracle_f16_to_f64(W[n * K + k]);
             Y[i * N + n] = y;
         }
+    return ORC_OK;
+}
+
+/* ---- epilogue (R7) ------------------------------------------------------ */
+
+#define ORC_ACT_NONE 0
+#define ORC_ACT_GELU 1
+
+/* In place on Y[i][n] (fp64, nrows x N) holding the products of rows
+ * m = rows[i] (rows == NULL: m = i): Y = act(Y + bias[n]) + residual[m][n];
+ * bias [N] and residual [M][N] fp32, either may be NULL. */
+int oracle_epilogue(double *Y, int64_t nrows, int64_t N, const int64_t *rows,
+                    const float *bias, int act, const float *residual)
+{
+    if (act != ORC_ACT_NONE && act != ORC_ACT_GELU)
+        return ORC_ERR_INVALID;
+    if (N <= 0 || nrows < 0)
+        return ORC_ERR_SHAPE;
+    for (int64_t i = 0; i < nrows; ++i) {
+        const int64_t src = rows ? rows[i] : i;  /* row of X, and of the residual */
+        for (int64_t n = 0; n < N; ++n) {
+            double v = Y[i * N + n];
+            if (bias)
+                v += (double)bias[n];
+            if (act == ORC_ACT_GELU)
+                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));
+            if (residual)
+                v += (double)residual[src * N + n];
+            Y[i * N + n] = v;
+        }
+    }
     return ORC_OK;
 }
 

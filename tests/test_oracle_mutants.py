@@ -54,6 +54,15 @@ MUTANTS = [
      "y += x_at(X, xdt, K, m, (k + 1) % K) * oracle_f16_to_f64(W"),
     ("fp16-weight forward ignores the row list",
      "const int64_t m = rows ? rows[i] : i;", "const int64_t m = i;"),
+    ("GELU without the 1/sqrt(2)",
+     "erf(v / sqrt(2.0))", "erf(v)"),
+    ("epilogue bias indexed by row",
+     "v += (double)bias[n];", "v += (double)bias[i % N];"),
+    ("epilogue residual before the activation",
+     "            if (act == ORC_ACT_GELU)\n                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));\n            if (residual)\n                v += (double)residual[src * N + n];",
+     "            if (residual)\n                v += (double)residual[src * N + n];\n            if (act == ORC_ACT_GELU)\n                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));"),
+    ("epilogue residual ignores the row list",
+     "v += (double)residual[src * N + n];", "v += (double)residual[i * N + n];"),
 ]
 
 
@@ -78,6 +87,8 @@ def pin_cases():
     cases += [(pins.test_forward_f16_integer_bruteforce, (x,)) for x in (0, 1)]
     cases += [(pins.test_forward_f16_equals_quantized_at_power_of_two_scales, (f,)) for f in F]
     cases += [(pins.test_forward_f16_subnormal_and_signed_zero_weights, ())]
+    cases += [(pins.test_epilogue_gelu_normal_cdf_values, ())]
+    cases += [(pins.test_epilogue_bias_residual_exact_and_order, ())]
     return cases
 
 

@@ -377,6 +377,42 @@ def test_forward_f16_subnormal_and_signed_zero_weights(orc):
 
 
 # --------------------------------------------------------------------------
+# epilogue (R7): act(P + bias) + residual
+# --------------------------------------------------------------------------
+
+def test_epilogue_gelu_normal_cdf_values(orc):
+    """GELU(x) = x * Phi(x) at points where the standard normal CDF is a
+    textbook value: Phi(0) = 1/2, Phi(1) = 0.8413447460685429,
+    Phi(-1) = 0.15865525393145707, Phi(2) = 0.9772498680518208, and
+    GELU(x) -> x (resp. 0) far in the right (left) tail."""
+    x = np.array([[0.0, 1.0, -1.0, 2.0, 40.0, -40.0]])
+    want = np.array([0.0, 0.8413447460685429, -0.15865525393145707,
+                     2 * 0.9772498680518208, 40.0, 0.0])
+    got = orc.epilogue(x, act=O.ACT_GELU)[0]
+    assert np.allclose(got, want, rtol=2e-16, atol=1e-300)
+
+
+def test_epilogue_bias_residual_exact_and_order(orc):
+    """Bias indexed by output column, residual by the product's source row
+    (a row subset), act between them: with act = GELU the result is
+    GELU(P + b) + r, not GELU(P + b + r) and not GELU(P) + b + r."""
+    rng = np.random.default_rng(81)
+    M, N = 6, 5
+    P = rng.integers(-50, 51, (M, N)).astype(np.float64)
+    b = rng.integers(-50, 51, N).astype(np.float32)
+    r = rng.integers(-50, 51, (M, N)).astype(np.float32)
+    assert np.array_equal(orc.epilogue(P, bias=b, residual=r), P + b + r)
+    rows = np.array([4, 1])
+    assert np.array_equal(orc.epilogue(P[rows], bias=b, residual=r, rows=rows),
+                          (P + b + r)[rows])
+    # order: 1 + (-1) = 0 through GELU gives 0; then + residual
+    P1 = np.array([[1.0]])
+    got = orc.epilogue(P1, bias=np.float32([-1.0]), act=O.ACT_GELU,
+                       residual=np.float32([[3.0]]))
+    assert got[0, 0] == 3.0
+
+
+# --------------------------------------------------------------------------
 # error conventions
 # --------------------------------------------------------------------------
 
