@@ -160,6 +160,46 @@ typedef struct {
  * entry is checked as in qlinear_forward. */
 int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream);
 
+/* Epilogue of a linear layer: the rest of the DiT block's linear around the
+ * product (bias, the feed-forward's GELU, the residual adds of the stream
+ * the paper steers: Methodology, taste steering), applied by the kernel
+ * that stores each output element:
+ *
+ *     Y[m][n] = act(P[m][n] + bias[n]) + residual[m][n]
+ *
+ * with P the product of qlinear_forward, in fp32.  act: QL_ACT_NONE, or
+ * QL_ACT_GELU in its exact form x * (1 + erf(x / sqrt 2)) / 2.  bias fp32
+ * [N] and residual fp32 [M][N] may each be NULL (4-byte aligned).  ydt:
+ * QL_DT_F32 (Y fp32 [M][N]) or QL_DT_BF16 (Y bf16 bit patterns [M][N],
+ * rounded to nearest even from the fp32 result; 2-byte aligned Y).
+ * residual may be Y itself when ydt is QL_DT_F32 (an in-place residual
+ * add); no other aliasing. */
+typedef enum { QL_ACT_NONE = 0, QL_ACT_GELU = 1 } ql_act;
+
+typedef struct {
+    const float *bias;      /* [N] or NULL */
+    int act;                /* ql_act */
+    const float *residual;  /* [M][N] or NULL */
+    int ydt;                /* ql_dtype of Y */
+} ql_epilogue;
+
+/* qlinear_forward with an epilogue (ep == NULL: none, fp32 Y).  Y is fp32 or
+ * bf16 as ep->ydt says.  Errors as in qlinear_forward, plus QL_ERR_INVALID
+ * for an unknown act or ydt and QL_ERR_ALIGN for misaligned bias/residual. */
+int qlinear_forward_ep(int fmt, const void *X, int xdt, int64_t M, int64_t K,
+                       const void *codes, const uint16_t *scales, int64_t N,
+                       void *Y, const ql_epilogue *ep, hipStream_t stream);
+
+/* One layer of qlinear_block_forward_ep: lin.Y points to fp32 or bf16
+ * outputs as ep.ydt says. */
+typedef struct {
+    ql_linear lin;
+    ql_epilogue ep;
+} ql_linear_ep;
+
+/* qlinear_block_forward with an epilogue per layer. */
+int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *qlinear_status_string(int status);
 

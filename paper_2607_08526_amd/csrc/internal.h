@@ -9,12 +9,22 @@
 
 namespace qlk {
 
+// A layer's epilogue as the kernels see it (see epilogue.h): Y[m][n] =
+// act(P + bias[n]) + resid[m][n], stored as fp32 or (ybf16) bf16.
+struct Epilogue {
+    const float *bias;   // [N] or nullptr
+    const float *resid;  // [M][N] or nullptr
+    int act;             // QL_ACT_NONE / QL_ACT_GELU
+    int ybf16;           // Y holds bf16 bit patterns
+};
+
 // Activations and packed codes of one linear layer as the kernels see it.
 struct LinDesc {
     const void *X;
     const uint8_t *codes;
     const uint16_t *scales;
-    float *Y;
+    float *Y;  // fp32 [M][N], or bf16 bit patterns if ep.ybf16
+    Epilogue ep;
     int M, N, K;
     int tiles_m, tiles_n;
     int tile_begin;  // first logical tile of this layer in a grouped launch
@@ -69,6 +79,7 @@ struct SplitSum {
     int S;
     int64_t M, N;
     float *Y;
+    Epilogue ep;  // applied to the sum
 };
 hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream);
 

@@ -37,6 +37,7 @@
 // L2.
 #include <type_traits>
 
+#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -384,7 +385,7 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
             for (int r = 0; r < 4; ++r) {
                 const int m = m0 + i * 16 + lg * 4 + r;
                 if (m < M && n < N)
-                    d.Y[(int64_t)m * N + n] = acc[i][j][r];
+                    epi_store(d.ep, d.Y, (int64_t)m * N + n, n, acc[i][j][r]);
             }
         }
 }

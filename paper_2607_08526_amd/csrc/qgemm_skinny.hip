@@ -28,6 +28,7 @@
 // (sign-extended, then converted to fp32 and truncated to bf16).
 #include <type_traits>
 
+#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(64 * KW) void qgemm_skinny_kernel(const LinDesc d)
             for (int r = 0; r < 4; ++r) {
                 const int m = i * 16 + lg * 4 + r;
                 if (m < M && n < N)
-                    d.Y[(int64_t)m * N + n] = y[r];
+                    epi_store(d.ep, d.Y, (int64_t)m * N + n, n, y[r]);
             }
         }
     }

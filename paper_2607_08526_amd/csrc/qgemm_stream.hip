@@ -38,6 +38,7 @@
 #include <algorithm>
 #include <cmath>
 
+#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -305,6 +306,8 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
         for (int nbi = 0; nbi < G::NB; ++nbi)
             red[((f * G::NB + nbi) * KW + wave) * 64 + lane] = acc[f][nbi];
     __syncthreads();
+    // destination: this part's partial output (summed, with the epilogue,
+    // by a separate launch), or Y
     float *const Yd = S > 1 ? d.part + (int64_t)part * M * N : d.Y;
     // wavefront w sums (and stores) fragments (f, nbi) = w, w + KW, ...
     for (int q = wave; q < G::NF * G::NB; q += KW) {
@@ -316,8 +319,12 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = f * 16 + lg * 4 + r;
-            if (l16 < G::RL && m < M && n < N)
-                Yd[(int64_t)m * N + n] = y[r];
+            if (l16 < G::RL && m < M && n < N) {
+                if (S > 1)
+                    Yd[(int64_t)m * N + n] = y[r];
+                else
+                    epi_store(d.ep, d.Y, (int64_t)m * N + n, n, y[r]);
+            }
         }
     }
 }

@@ -68,6 +68,7 @@
 // end of the kernel).
 #include <algorithm>
 
+#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -562,6 +563,10 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     // are summed by a separate launch (split_sum_kernel)
     const bool to_part = S > 1 && !d.cnt;
     float *const Yd = to_part ? d.part + (int64_t)part * M * N : d.Y;
+    const bool vec = (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0;
+    // a layer epilogue beyond the plain fp32 store (final outputs only)
+    const bool epi = !to_part && (d.ep.bias || d.ep.resid || d.ep.act || d.ep.ybf16);
+    const bool vec_epi = epi_vec_ok(d.ep, d.Y, N);
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
 #pragma unroll
         for (int h = 0; h < 4; ++h)
@@ -571,28 +576,52 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         const int lane = tid & 63;
         const int cq = lane & 7;          // 4-column group of the row
         const int n = n0 + c.wave * WN + j * 32 + 4 * cq;
+        if (!epi) {
 #pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int rl = 8 * t + (lane >> 3);  // row within the 32-row tile
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + rl * 32 + 4 * cq);
+                const int m = m0 + i * 32 + rl;
+                if (m >= M)
+                    continue;
+                float *const dst = Yd + (int64_t)m * N + n;
+                if (n + 3 < N && vec) {
+                    // streaming store for Y (not read again here: letting it
+                    // allocate would evict the activation and code lines that
+                    // other tiles still re-read); partials, which the sum
+                    // launch reads next, stay cacheable
+                    if (to_part)
+                        *reinterpret_cast<f32x4 *>(dst) = v;
+                    else
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (n + e < N)
+                            dst[e] = v[e];
+                }
+            }
+            return;
+        }
+        // with the epilogue: one row per iteration, so that its code appears
+        // once per tile store rather than once per row (the fully unrolled
+        // accumulator loops around this must stay within the unroller's size
+        // limit)
+#pragma unroll 1
         for (int t = 0; t < 4; ++t) {
-            const int rl = 8 * t + (lane >> 3);  // row within the 32-row tile
+            const int rl = 8 * t + (lane >> 3);
             const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + rl * 32 + 4 * cq);
             const int m = m0 + i * 32 + rl;
             if (m >= M)
                 continue;
-            float *const dst = Yd + (int64_t)m * N + n;
-            if (n + 3 < N && (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0) {
-                // streaming store for Y (not read again here: letting it
-                // allocate would evict the activation and code lines that
-                // other tiles still re-read); partials, which the sum launch
-                // reads next, stay cacheable
-                if (to_part)
-                    *reinterpret_cast<f32x4 *>(dst) = v;
-                else
-                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(dst));
+            const int64_t idx = (int64_t)m * N + n;
+            if (n + 3 < N && vec_epi) {
+                epi_store4(d.ep, d.Y, idx, n, v, true);
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (n + e < N)
-                        dst[e] = v[e];
+                        epi_store(d.ep, d.Y, idx + e, n + e, v[e]);
             }
         }
     };
@@ -689,7 +718,9 @@ struct SumJob {
     const float *P;
     float *Y;
     int S, v4;
-    int64_t count;  // outputs per part, in 16-byte groups if v4
+    int64_t count;  // outputs per part, in 4-element groups if v4
+    int64_t N;
+    Epilogue ep;    // applied to the sum
 };
 struct SumArgs {
     SumJob j[QL_MAX_GROUP];
@@ -717,8 +748,9 @@ __device__ inline T sum_parts(const T *p, int S, int64_t count)
 }
 
 // One launch for the split layers of a call: flat index space over every
-// job's outputs, 16-byte groups for jobs that allow them (N % 4 == 0, Y
-// 16-byte aligned), single floats otherwise.
+// job's outputs, 4-element groups for jobs that allow them (N % 4 == 0, Y
+// aligned for one 16-byte fp32 or 8-byte bf16 store), single elements
+// otherwise; each layer's epilogue is applied to its sums.
 __global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
 {
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -732,9 +764,11 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
         const int64_t i = x - a.begin[ji];
         if (jb.v4) {
             const f32x4 y = sum_parts(reinterpret_cast<const f32x4 *>(jb.P) + i, jb.S, jb.count);
-            __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(jb.Y) + i);
+            const int n = jb.ep.bias ? (int)((4 * i) % jb.N) : 0;
+            epi_store4(jb.ep, jb.Y, 4 * i, n, y, true);
         } else {
-            jb.Y[i] = sum_parts(jb.P + i, jb.S, jb.count);
+            const int n = jb.ep.bias ? (int)(i % jb.N) : 0;
+            epi_store(jb.ep, jb.Y, i, n, sum_parts(jb.P + i, jb.S, jb.count));
         }
     }
 }
@@ -747,9 +781,9 @@ hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream)
     int64_t total = 0;
     for (int i = 0; i < n; ++i) {
         const SplitSum &q = sums[i];
-        const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & 15) == 0;
+        const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & (q.ep.ybf16 ? 7 : 15)) == 0;
         const int64_t count = v4 ? q.M * q.N / 4 : q.M * q.N;
-        a.j[i] = SumJob{q.P, q.Y, q.S, v4 ? 1 : 0, count};
+        a.j[i] = SumJob{q.P, q.Y, q.S, v4 ? 1 : 0, count, q.N, q.ep};
         a.begin[i] = total;
         total += count;
     }

@@ -20,6 +20,7 @@
 //
 // Requirements (checked by the host): M <= 4, K % 256 == 0, M * K <= 32768
 // (the activation stage fits LDS), 16-byte aligned codes and X.
+#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -223,7 +224,7 @@ __global__ __launch_bounds__(64 * WAVES) void qgemv_kernel(const LinDesc d)
             if (n0 + r < N)
 #pragma unroll
                 for (int m = 0; m < MM; ++m)
-                    d.Y[(int64_t)m * N + n0 + r] = acc[r][m];
+                    epi_store(d.ep, d.Y, (int64_t)m * N + n0 + r, n0 + r, acc[r][m]);
 }
 
 template <int FMT, int MM, int RPW>

@@ -23,7 +23,7 @@ bool fmt_ok(int f) { return f == QL_FMT_INT8 || f == QL_FMT_Q4; }
 bool fwd_fmt_ok(int f) { return fmt_ok(f) || f == QL_FMT_F16; }
 
 int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
-                 const uint16_t *scales, int64_t N, const float *Y)
+                 const uint16_t *scales, int64_t N, const void *Y, int ydt = QL_DT_F32)
 {
     const bool f16 = fmt == QL_FMT_F16;
     if (!fwd_fmt_ok(fmt) || (xdt != QL_DT_F32 && xdt != QL_DT_BF16))
@@ -38,9 +38,40 @@ int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const vo
     if (!codes || (!f16 && !scales) || (M > 0 && (!X || !Y)))
         return QL_ERR_INVALID;
     if (!aligned(codes, 16) || (!f16 && !aligned(scales, 2)) ||
-        (M > 0 && (!aligned(X, 16) || !aligned(Y, 4))))
+        (M > 0 && (!aligned(X, 16) || !aligned(Y, ydt == QL_DT_BF16 ? 2 : 4))))
         return QL_ERR_ALIGN;
     return QL_OK;
+}
+
+const ql_epilogue NO_EPILOGUE = {nullptr, QL_ACT_NONE, nullptr, QL_DT_F32};
+
+// an epilogue's enums, aliasing and alignment (before check_linear, which
+// takes its ydt)
+int check_epilogue(const ql_epilogue &ep, const void *Y)
+{
+    if ((ep.act != QL_ACT_NONE && ep.act != QL_ACT_GELU) ||
+        (ep.ydt != QL_DT_F32 && ep.ydt != QL_DT_BF16))
+        return QL_ERR_INVALID;
+    // an in-place residual add needs fp32 Y
+    if (ep.ydt == QL_DT_BF16 && ep.residual && (const void *)ep.residual == Y)
+        return QL_ERR_INVALID;
+    if (!aligned(ep.bias, 4) || !aligned(ep.residual, 4))
+        return QL_ERR_ALIGN;
+    return QL_OK;
+}
+
+int check_layer(const ql_linear_ep &l)
+{
+    const int st = check_epilogue(l.ep, l.lin.Y);
+    if (st != QL_OK)
+        return st;
+    return check_linear(l.lin.fmt, l.lin.X, l.lin.xdt, l.lin.M, l.lin.K, l.lin.codes,
+                        l.lin.scales, l.lin.N, l.lin.Y, l.ep.ydt);
+}
+
+Epilogue to_epilogue(const ql_epilogue &e)
+{
+    return Epilogue{e.bias, e.residual, e.act, e.ydt == QL_DT_BF16 ? 1 : 0};
 }
 
 // Stream-ordered pool (one per device) that the per-stream workspaces below
@@ -351,33 +382,34 @@ TileCfg choose_tile(int64_t M, bool xf32)
 }
 
 // One grouped launch over layers that share fmt and xdt (M > 0 each).
-int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
+int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
 {
     if (n == 0)
         return QL_OK;
-    const bool xf32 = ls[0]->xdt == QL_DT_F32;
+    const bool xf32 = ls[0]->lin.xdt == QL_DT_F32;
     int64_t maxM = 0;
     for (int i = 0; i < n; ++i)
-        maxM = std::max(maxM, ls[i]->M);
-    const bool f16 = ls[0]->fmt == QL_FMT_F16;
+        maxM = std::max(maxM, ls[i]->lin.M);
+    const bool f16 = ls[0]->lin.fmt == QL_FMT_F16;
     if (!xf32 && !f16 && maxM <= skinny_max_m()) {
         // few rows: streaming-bound, one launch per layer
         for (int i = 0; i < n; ++i) {
             LinDesc d{};
-            d.X = ls[i]->X;
-            d.codes = (const uint8_t *)ls[i]->codes;
-            d.scales = ls[i]->scales;
-            d.Y = ls[i]->Y;
-            d.M = (int)ls[i]->M;
-            d.N = (int)ls[i]->N;
-            d.K = (int)ls[i]->K;
+            d.X = ls[i]->lin.X;
+            d.codes = (const uint8_t *)ls[i]->lin.codes;
+            d.scales = ls[i]->lin.scales;
+            d.Y = ls[i]->lin.Y;
+            d.ep = to_epilogue(ls[i]->ep);
+            d.M = (int)ls[i]->lin.M;
+            d.N = (int)ls[i]->lin.N;
+            d.K = (int)ls[i]->lin.K;
             const bool stream_ok = d.M <= stream_max_m() && d.K % 256 == 0 &&
                                    aligned(d.scales, 16);
             hipError_t e = hipSuccess;
             if (gemv_ok(d)) {
-                e = launch_qgemv(ls[i]->fmt, d, stream);
+                e = launch_qgemv(ls[i]->lin.fmt, d, stream);
             } else if (stream_ok) {
-                const StreamPlan p = stream_plan(ls[i]->fmt, d, device_cus());
+                const StreamPlan p = stream_plan(ls[i]->lin.fmt, d, device_cus());
                 d.ksplit = p.S;
                 d.psteps = p.psteps;
                 Workspace ws{};
@@ -386,9 +418,9 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
                         return QL_ERR_HIP;
                     d.part = (float *)ws.ptr;
                 }
-                e = launch_qgemm_stream(ls[i]->fmt, p, d, stream);
+                e = launch_qgemm_stream(ls[i]->lin.fmt, p, d, stream);
                 if (e == hipSuccess && p.S > 1) {
-                    const SplitSum q{d.part, p.S, d.M, d.N, d.Y};
+                    const SplitSum q{d.part, p.S, d.M, d.N, d.Y, d.ep};
                     e = launch_split_sum(&q, 1, stream);
                 }
                 if (ws.own_alloc) {
@@ -396,7 +428,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
                     e = e == hipSuccess ? ef : e;
                 }
             } else {
-                e = launch_qgemm_skinny(ls[i]->fmt, d, stream);
+                e = launch_qgemm_skinny(ls[i]->lin.fmt, d, stream);
             }
             if (e != hipSuccess)
                 return QL_ERR_HIP;
@@ -405,43 +437,44 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     }
     maxM = 0;
     for (int i = 0; i < n; ++i)
-        maxM = std::max(maxM, ls[i]->M);
+        maxM = std::max(maxM, ls[i]->lin.M);
     const TileCfg t = choose_tile(maxM, xf32);
     // the fp16 path's kernel reads each weight row's scales as 16-byte
     // chunks and addresses a tile's rows with 32-bit offsets
     bool wide = !xf32 && t == TILE_M128;
     for (int i = 0; i < n; ++i)
-        wide = wide && ls[i]->K % 256 == 0 && ls[i]->K < ((int64_t)1 << 23) &&
-               aligned(ls[i]->scales, 16);
+        wide = wide && ls[i]->lin.K % 256 == 0 && ls[i]->lin.K < ((int64_t)1 << 23) &&
+               aligned(ls[i]->lin.scales, 16);
     wide = wide || f16;  // fp16 weights: this kernel at every M (checked by check_linear)
     const int bm = wide ? wide_tile_bm() : tile_bm(t);
     const int bn = wide ? wide_tile_bn() : tile_bn(t);
 
     // longest reduction first, so the long tiles start early
-    const ql_linear *ord[QL_MAX_GROUP];
+    const ql_linear_ep *ord[QL_MAX_GROUP];
     std::copy(ls, ls + n, ord);
     std::stable_sort(ord, ord + n,
-                     [](const ql_linear *a, const ql_linear *b) { return a->K > b->K; });
+                     [](const ql_linear_ep *a, const ql_linear_ep *b) { return a->lin.K > b->lin.K; });
 
     GroupArgs a{};
     int64_t total = 0;
     for (int i = 0; i < n; ++i) {
         LinDesc &d = a.d[i];
-        d.X = ord[i]->X;
-        d.codes = (const uint8_t *)ord[i]->codes;
-        d.scales = ord[i]->scales;
-        d.Y = ord[i]->Y;
-        d.M = (int)ord[i]->M;
-        d.N = (int)ord[i]->N;
-        d.K = (int)ord[i]->K;
-        d.tiles_m = (int)((ord[i]->M + bm - 1) / bm);
-        d.tiles_n = (int)((ord[i]->N + bn - 1) / bn);
+        d.X = ord[i]->lin.X;
+        d.codes = (const uint8_t *)ord[i]->lin.codes;
+        d.scales = ord[i]->lin.scales;
+        d.Y = ord[i]->lin.Y;
+        d.ep = to_epilogue(ord[i]->ep);
+        d.M = (int)ord[i]->lin.M;
+        d.N = (int)ord[i]->lin.N;
+        d.K = (int)ord[i]->lin.K;
+        d.tiles_m = (int)((ord[i]->lin.M + bm - 1) / bm);
+        d.tiles_n = (int)((ord[i]->lin.N + bn - 1) / bn);
         d.ksplit = 1;
-        d.psteps = (int)(ord[i]->K / 64);
+        d.psteps = (int)(ord[i]->lin.K / 64);
     }
     SplitPlan pl{};
     if (wide)
-        pl = cached_plan(ord[0]->fmt, a.d, n);
+        pl = cached_plan(ord[0]->lin.fmt, a.d, n);
     for (int i = 0; i < n; ++i) {
         LinDesc &d = a.d[i];
         if (wide) {
@@ -459,7 +492,7 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
     a.n = n;
     a.total_tiles = (int)total;
     if (!wide)
-        return launch_qgemm(ord[0]->fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+        return launch_qgemm(ord[0]->lin.fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
 
     // Workspace: one exact, row-shifted fp16 copy per distinct activation
     // tensor (layers reading the same X share it)
@@ -525,20 +558,21 @@ int launch_group(const ql_linear *const *ls, int n, hipStream_t stream)
         xs[i] = xh;
         es[i] = ex;
     }
-    hipError_t e = launch_xprep(jobs, njobs, ord[0]->fmt == QL_FMT_Q4, (int *)(wsb + cnt_off),
+    hipError_t e = launch_xprep(jobs, njobs, ord[0]->lin.fmt == QL_FMT_Q4, (int *)(wsb + cnt_off),
                                 ncnt, stream);
     for (int i = 0; i < n; ++i) {
         a.d[i].X = xs[i];
         a.d[i].xexp = es[i];
     }
     if (e == hipSuccess)
-        e = launch_qgemm_wide(ord[0]->fmt, a, stream);
+        e = launch_qgemm_wide(ord[0]->lin.fmt, a, stream);
     if (pl.ext && e == hipSuccess) {
         SplitSum sums[QL_MAX_GROUP];
         int ns = 0;
         for (int i = 0; i < n; ++i)
             if (a.d[i].ksplit > 1)
-                sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y};
+                sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
+                                      a.d[i].ep};
         e = launch_split_sum(sums, ns, stream);
     }
     const hipError_t ef = ws.own_alloc ? hipFreeAsync(ws.ptr, stream) : hipSuccess;
@@ -595,35 +629,43 @@ int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K, void *codes,
     return hstatus;
 }
 
-int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
-                    const uint16_t *scales, int64_t N, float *Y, hipStream_t stream)
+int qlinear_forward_ep(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
+                       const uint16_t *scales, int64_t N, void *Y, const ql_epilogue *ep,
+                       hipStream_t stream)
 {
-    const int st = check_linear(fmt, X, xdt, M, K, codes, scales, N, Y);
+    const ql_linear_ep l{{fmt, X, xdt, M, K, N, codes, scales, (float *)Y},
+                         ep ? *ep : NO_EPILOGUE};
+    const int st = check_layer(l);
     if (st != QL_OK || M == 0)
         return st;
-    ql_linear l{fmt, X, xdt, M, K, N, codes, scales, Y};
-    const ql_linear *p = &l;
+    const ql_linear_ep *p = &l;
     return launch_group(&p, 1, stream);
 }
 
-int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
+int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
+                    const uint16_t *scales, int64_t N, float *Y, hipStream_t stream)
+{
+    return qlinear_forward_ep(fmt, X, xdt, M, K, codes, scales, N, Y, nullptr, stream);
+}
+
+int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t stream)
 {
     if (!lin || n_lin < 1 || n_lin > QL_MAX_GROUP)
         return QL_ERR_INVALID;
     for (int i = 0; i < n_lin; ++i) {
-        const ql_linear &l = lin[i];
-        const int st = check_linear(l.fmt, l.X, l.xdt, l.M, l.K, l.codes, l.scales, l.N, l.Y);
+        const int st = check_layer(lin[i]);
         if (st != QL_OK)
             return st;
     }
     // partition the non-empty layers by (fmt, xdt); each class is one launch
-    const ql_linear *cls[6][QL_MAX_GROUP];
+    const ql_linear_ep *cls[6][QL_MAX_GROUP];
     int cnt[6] = {0, 0, 0, 0, 0, 0};
     for (int i = 0; i < n_lin; ++i) {
-        if (lin[i].M == 0)
+        const ql_linear &l = lin[i].lin;
+        if (l.M == 0)
             continue;
-        const int f = lin[i].fmt == QL_FMT_Q4 ? 0 : lin[i].fmt == QL_FMT_INT8 ? 1 : 2;
-        const int c = 2 * f + (lin[i].xdt == QL_DT_BF16 ? 1 : 0);
+        const int f = l.fmt == QL_FMT_Q4 ? 0 : l.fmt == QL_FMT_INT8 ? 1 : 2;
+        const int c = 2 * f + (l.xdt == QL_DT_BF16 ? 1 : 0);
         cls[c][cnt[c]++] = &lin[i];
     }
     for (int c = 0; c < 6; ++c) {
@@ -632,6 +674,16 @@ int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
             return st;
     }
     return QL_OK;
+}
+
+int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
+{
+    if (!lin || n_lin < 1 || n_lin > QL_MAX_GROUP)
+        return QL_ERR_INVALID;
+    ql_linear_ep l[QL_MAX_GROUP];
+    for (int i = 0; i < n_lin; ++i)
+        l[i] = ql_linear_ep{lin[i], NO_EPILOGUE};
+    return qlinear_block_forward_ep(l, n_lin, stream);
 }
 
 const char *qlinear_status_string(int status)

@@ -17,6 +17,8 @@ FMT_INT8 = 8
 FMT_F16 = 16  # unquantized fp16 weights (forward only; scales unused)
 DT_F32 = 0
 DT_BF16 = 1
+ACT_NONE = 0
+ACT_GELU = 1  # exact GELU, x * Phi(x)
 BLOCK = 32
 MAX_GROUP = 8
 
@@ -27,7 +29,8 @@ STATUS = {
 
 EXPORTS = [
     "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
-    "qlinear_forward", "qlinear_block_forward", "qlinear_status_string",
+    "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
+    "qlinear_block_forward_ep", "qlinear_status_string",
 ]
 
 
@@ -49,6 +52,19 @@ class _Linear(ctypes.Structure):
         ("scales", ctypes.c_void_p),
         ("Y", ctypes.c_void_p),
     ]
+
+
+class _Epilogue(ctypes.Structure):
+    _fields_ = [
+        ("bias", ctypes.c_void_p),
+        ("act", ctypes.c_int),
+        ("residual", ctypes.c_void_p),
+        ("ydt", ctypes.c_int),
+    ]
+
+
+class _LinearEp(ctypes.Structure):
+    _fields_ = [("lin", _Linear), ("ep", _Epilogue)]
 
 
 _LIB = None
@@ -91,6 +107,11 @@ def load():
     lib.qlinear_forward.argtypes = [ci, vp, ci, i64, i64, vp, vp, i64, vp, vp]
     lib.qlinear_forward.restype = ci
     lib.qlinear_block_forward.argtypes = [ctypes.POINTER(_Linear), ci, vp]
+    lib.qlinear_forward_ep.argtypes = [ci, vp, ci, i64, i64, vp, vp, i64, vp,
+                                       ctypes.POINTER(_Epilogue), vp]
+    lib.qlinear_forward_ep.restype = ci
+    lib.qlinear_block_forward_ep.argtypes = [ctypes.POINTER(_LinearEp), ci, vp]
+    lib.qlinear_block_forward_ep.restype = ci
     lib.qlinear_block_forward.restype = ci
     lib.qlinear_status_string.argtypes = [ci]
     lib.qlinear_status_string.restype = ctypes.c_char_p
@@ -162,6 +183,33 @@ def forward(fmt, X, codes, scales, N, Y=None, stream=None):
     return Y
 
 
+def _ydt(Y):
+    if Y.dtype == torch.float32:
+        return DT_F32
+    if Y.dtype == torch.bfloat16:
+        return DT_BF16
+    raise TypeError(f"outputs must be float32 or bfloat16, not {Y.dtype}")
+
+
+def _epilogue(Y, bias, act, residual):
+    return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y))
+
+
+def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
+               ydtype=torch.float32, stream=None):
+    """forward() with the layer epilogue fused into the output store:
+    Y = act(X . W^T + bias) + residual, Y fp32 or bf16 (ydtype, or Y's dtype
+    when Y is given).  bias fp32 [N], residual fp32 [M][N] (may be Y itself
+    for fp32 Y), each optional.  Asynchronous."""
+    M, K = X.shape
+    if Y is None:
+        Y = torch.empty((M, N), dtype=ydtype, device=X.device)
+    ep = _epilogue(Y, bias, act, residual)
+    _check(load().qlinear_forward_ep(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
+                                     _ptr(Y), ctypes.byref(ep), _stream(stream)))
+    return Y
+
+
 def make_group(entries):
     """ctypes array for block_forward from (fmt, X, codes, scales, N, Y) tuples.
     The tensors must outlive every use of the returned array."""
@@ -179,6 +227,27 @@ def block_forward(entries, stream=None, group=None):
     Asynchronous.  A prepared `group` (make_group) skips re-marshalling."""
     arr = group if group is not None else make_group(entries)
     _check(load().qlinear_block_forward(arr, len(arr), _stream(stream)))
+    return [e[5] for e in entries] if entries is not None else None
+
+
+def make_group_ep(entries):
+    """ctypes array for block_forward_ep from (fmt, X, codes, scales, N, Y,
+    bias, act, residual) tuples (bias/residual None for none; Y fp32 or bf16).
+    The tensors must outlive every use of the returned array."""
+    arr = (_LinearEp * len(entries))()
+    for i, (fmt, X, codes, scales, N, Y, bias, act, residual) in enumerate(entries):
+        M, K = X.shape
+        lin = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
+                      scales.data_ptr() if scales is not None else 0, Y.data_ptr())
+        arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual))
+    return arr
+
+
+def block_forward_ep(entries, stream=None, group=None):
+    """block_forward with an epilogue per layer: entries are (fmt, X, codes,
+    scales, N, Y, bias, act, residual) tuples.  Asynchronous."""
+    arr = group if group is not None else make_group_ep(entries)
+    _check(load().qlinear_block_forward_ep(arr, len(arr), _stream(stream)))
     return [e[5] for e in entries] if entries is not None else None
 
 

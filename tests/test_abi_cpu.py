@@ -13,6 +13,7 @@ LIB = os.path.join(ROOT, "paper_2607_08526_amd", "libqlinear.so")
 
 OK, INVALID, SHAPE, ALIGN, RANGE, UNSUPPORTED, HIP = range(7)
 Q4, INT8, F32, BF16 = 4, 8, 0, 1
+ACT_NONE, ACT_GELU = 0, 1
 
 
 def declared_functions():
@@ -41,7 +42,8 @@ def lib():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
-        "qlinear_forward", "qlinear_block_forward", "qlinear_status_string"])
+        "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
+        "qlinear_block_forward_ep", "qlinear_status_string"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -121,3 +123,52 @@ def test_block_forward_argument_errors(lib):
     empty = (_Linear * 1)()
     empty[0] = _Linear(Q4, None, BF16, 0, 64, 16, A16, A16, None)
     assert lib.qlinear_block_forward(empty, 1, None) == OK  # all layers empty: no-op
+
+
+def fwd_ep(lib, bias=None, act=ACT_NONE, residual=None, ydt=F32, Y=A16, M=4, ep=True):
+    from paper_2607_08526_amd.qlinear import _Epilogue
+    e = _Epilogue(bias, act, residual, ydt)
+    return lib.qlinear_forward_ep(INT8, A16, BF16, M, 64, A16, A16, 16, Y,
+                                  ctypes.byref(e) if ep else None, None)
+
+
+def test_forward_ep_argument_errors(lib):
+    from paper_2607_08526_amd.qlinear import _Epilogue
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.qlinear_forward_ep.argtypes = [ci, vp, ci, i64, i64, vp, vp, i64, vp,
+                                       ctypes.POINTER(_Epilogue), vp]
+    assert fwd_ep(lib, act=2) == INVALID
+    assert fwd_ep(lib, act=-1) == INVALID
+    assert fwd_ep(lib, ydt=2) == INVALID
+    assert fwd_ep(lib, bias=A2) == ALIGN
+    assert fwd_ep(lib, residual=A2) == ALIGN
+    # bf16 Y needs 2-byte alignment only; fp32 Y needs 4
+    assert fwd_ep(lib, Y=A2, ydt=F32, M=0) == OK
+    assert fwd_ep(lib, Y=A1, ydt=BF16) == ALIGN
+    assert fwd_ep(lib, Y=A2, ydt=F32) == ALIGN
+    # an in-place residual add needs fp32 Y
+    assert fwd_ep(lib, residual=A16, Y=A16, ydt=BF16) == INVALID
+    # the checks of qlinear_forward still apply; no epilogue is the plain call
+    assert lib.qlinear_forward_ep(5, A16, BF16, 4, 64, A16, A16, 16, A16, None, None) == INVALID
+    assert fwd_ep(lib, M=0, ep=False) == OK
+
+
+def test_block_forward_ep_argument_errors(lib):
+    from paper_2607_08526_amd.qlinear import _Epilogue, _Linear, _LinearEp
+    lib.qlinear_block_forward_ep.argtypes = [ctypes.POINTER(_LinearEp), ctypes.c_int,
+                                             ctypes.c_void_p]
+    arr = (_LinearEp * 2)()
+    arr[0] = _LinearEp(_Linear(INT8, A16, BF16, 4, 64, 16, A16, A16, A16),
+                       _Epilogue(A16, ACT_GELU, None, F32))
+    arr[1] = _LinearEp(_Linear(INT8, A16, BF16, 4, 64, 16, A16, A16, A16),
+                       _Epilogue(None, 7, None, F32))  # unknown act
+    assert lib.qlinear_block_forward_ep(arr, 2, None) == INVALID
+    arr[1] = _LinearEp(_Linear(INT8, A16, BF16, 4, 64, 16, A16, A16, A1),
+                       _Epilogue(None, ACT_NONE, None, BF16))  # odd bf16 Y
+    assert lib.qlinear_block_forward_ep(arr, 2, None) == ALIGN
+    assert lib.qlinear_block_forward_ep(arr, 0, None) == INVALID
+    assert lib.qlinear_block_forward_ep(arr, 9, None) == INVALID
+    empty = (_LinearEp * 1)()
+    empty[0] = _LinearEp(_Linear(Q4, None, BF16, 0, 64, 16, A16, A16, None),
+                         _Epilogue(None, ACT_GELU, None, BF16))
+    assert lib.qlinear_block_forward_ep(empty, 1, None) == OK
