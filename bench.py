@@ -34,7 +34,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_step_q4.txt")
 # valid for the sources it was measured on
 KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm_wide.hip", "paper_2607_08526_amd/csrc/xprep.hip",
                   "paper_2607_08526_amd/csrc/internal.h", "paper_2607_08526_amd/csrc/qlinear.hip"]
-GEMM_KERNEL = "qgemm_wide_kernel"
+GEMM_KERNEL = "qgemm_wide_kernel<4, false>"  # q4, no epilogue
 PREP_KERNEL = "xprep_kernel"
 COPY_BYTES = 1 << 30  # the calibration copy: 1 GiB read + 1 GiB written
 
@@ -56,7 +56,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--no-sweeps", action="store_true", help="time the step only")
+    ap.add_argument("--no-sweeps", action="store_true", help="skip the skinny/width sweeps")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the q4 step only (no sweeps, fp16 reference or epilogue step); "
+                         "the form the counter runs profile")
     ap.add_argument("--sweeps-only", action="store_true",
                     help="run the skinny-M sweep and the int8 block only (no step, no JSON line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -223,6 +226,73 @@ def time_f16_step(torch, ql, step, steps, warmup):
     end.record()
     torch.cuda.synchronize()
     return start.elapsed_time(end) / steps
+
+
+def epilogue_step(torch, ql, step, steps, warmup):
+    """The q4 step with each block's layer epilogues: QKV + bias -> bf16 (the
+    attention's input), out + bias added in place to an fp32 residual
+    stream, FFN-up + bias -> GELU -> bf16 (FFN-down's input), FFN-down + bias
+    added in place to a second residual stream (the two residual adds run
+    in one grouped launch, so they target separate tensors).  Timed fused
+    (qlinear_block_forward_ep) and unfused (the plain step, then the same
+    epilogue as separate torch ops on its fp32 outputs)."""
+    import torch.nn.functional as F
+    dev = torch.device("cuda")
+    M = step.M
+    Ns = [e[4] for e in step.blocks[0]]
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    ydt = [torch.bfloat16, torch.float32, torch.bfloat16, torch.float32]
+    acts = [ql.ACT_NONE, ql.ACT_NONE, ql.ACT_GELU, ql.ACT_NONE]
+    Ye = [torch.zeros((M, N), dtype=dt, device=dev) for N, dt in zip(Ns, ydt)]
+    bias = [[torch.randn(N, device=dev, generator=g) * 0.1 for N in Ns]
+            for _ in step.blocks]
+    groups = []
+    for blk, ents in enumerate(step.blocks):
+        ep = []
+        for i, (fmt, X, c, sc, N, _) in enumerate(ents):
+            res = Ye[i] if ydt[i] == torch.float32 else None
+            ep.append((fmt, X, c, sc, N, Ye[i], bias[blk][i], acts[i], res))
+        groups.append(ql.make_group_ep(ep))
+
+    def fused():
+        for gr in groups:
+            ql.block_forward_ep(None, group=gr)
+
+    def unfused():
+        for blk, gr in enumerate(step.groups):
+            ql.block_forward(None, group=gr)
+            Y, b = step.Y, bias[blk]
+            Ye[0].copy_(Y[0] + b[0])
+            Ye[1].add_(Y[1] + b[1])
+            Ye[2].copy_(F.gelu(Y[2] + b[2]))
+            Ye[3].add_(Y[3] + b[3])
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    n = max(3, steps // 2)
+    fused_ms, unfused_ms = timed(fused, n), timed(unfused, n)
+    plain_ms = timed(step.run, n)
+    return {
+        "note": "the q4 step with each block's epilogues (QKV+bias->bf16, out+bias+residual, "
+                "FFN-up+bias->GELU->bf16, FFN-down+bias+residual) fused into the output "
+                "stores, against the plain step followed by the same epilogue in torch ops",
+        "fused_ms_per_step": round(fused_ms, 4),
+        "unfused_ms_per_step": round(unfused_ms, 4),
+        "plain_ms_per_step": round(plain_ms, 4),
+        "fused_overhead_pct": round(100.0 * (fused_ms / plain_ms - 1.0), 2),
+        "fusion_speedup": round(unfused_ms / fused_ms, 3),
+    }
 
 
 def time_step(torch, step, steps, warmup):
@@ -508,7 +578,8 @@ def main():
                           "paper_widths": paper_widths(torch, ql, si)}), flush=True)
         return
 
-    step = Step(torch, ql, si, keep_host_block0=not args.no_cpu_baseline)
+    step = Step(torch, ql, si, keep_host_block0=not args.no_cpu_baseline,
+                with_f16=not args.step_only)
     total_ms, launch_ms, wall = time_step(torch, step, args.steps, args.warmup)
     ms_per_step = total_ms / args.steps
     tflops = step.flops / (ms_per_step * 1e-3) / 1e12
@@ -550,6 +621,9 @@ def main():
             "avg_launch_ms": round(avg_launch_ms, 5),
         },
     }
+    if args.step_only:
+        print(json.dumps(res), flush=True)
+        return
     f16_ms = time_f16_step(torch, ql, step, max(3, args.steps // 2), args.warmup)
     res["fp16_reference"] = {
         "note": "the same 24-block step with the weights in fp16 (QL_FMT_F16, the "
@@ -559,6 +633,7 @@ def main():
         "weight_GBps": round(sum(2 * w.numel() for w in step.keep_f16) / (f16_ms * 1e-3) / 1e9, 1),
         "q4_step_speedup": round(f16_ms / ms_per_step, 3),
     }
+    res["epilogue"] = epilogue_step(torch, ql, step, args.steps, args.warmup)
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)

@@ -380,7 +380,9 @@ __device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, in
     }
 }
 
-template <int FMT>
+// EPI: some layer of the launch has an epilogue (bias, GELU, residual or
+// bf16 outputs); the kernel without one keeps the plain fp32 store code only
+template <int FMT, bool EPI>
 __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
@@ -565,18 +567,18 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     float *const Yd = to_part ? d.part + (int64_t)part * M * N : d.Y;
     const bool vec = (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0;
     // a layer epilogue beyond the plain fp32 store (final outputs only)
-    const bool epi = !to_part && (d.ep.bias || d.ep.resid || d.ep.act || d.ep.ybf16);
+    const bool epi = EPI && !to_part && (d.ep.bias || d.ep.resid || d.ep.act || d.ep.ybf16);
     const bool vec_epi = epi_vec_ok(d.ep, d.Y, N);
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
-#pragma unroll
-        for (int h = 0; h < 4; ++h)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
         const int lane = tid & 63;
         const int cq = lane & 7;          // 4-column group of the row
         const int n = n0 + c.wave * WN + j * 32 + 4 * cq;
         if (!epi) {
+#pragma unroll
+            for (int h = 0; h < 4; ++h)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int rl = 8 * t + (lane >> 3);  // row within the 32-row tile
@@ -603,26 +605,56 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
             }
             return;
         }
-        // with the epilogue: one row per iteration, so that its code appears
-        // once per tile store rather than once per row (the fully unrolled
-        // accumulator loops around this must stay within the unroller's size
-        // limit)
-#pragma unroll 1
-        for (int t = 0; t < 4; ++t) {
-            const int rl = 8 * t + (lane >> 3);
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + rl * 32 + 4 * cq);
-            const int m = m0 + i * 32 + rl;
-            if (m >= M)
-                continue;
-            const int64_t idx = (int64_t)m * N + n;
-            if (n + 3 < N && vec_epi) {
-                epi_store4(d.ep, d.Y, idx, n, v, true);
-            } else {
+        // with the epilogue: the bias and the four rows' residual loads go
+        // out first (before the patch round trip, which hides part of their
+        // latency); whether the layer takes groups of four is uniform, so
+        // the common path is straight-line code with predicated stores
+        const int mb = m0 + i * 32 + (lane >> 3);  // row of iteration 0
+        if (!vec_epi) {
+            // element by element (N % 4 != 0 or unaligned operands; a row
+            // per iteration keeps this rare path's code small)
+#pragma unroll
+            for (int h = 0; h < 4; ++h)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    if (n + e < N)
-                        epi_store(d.ep, d.Y, idx + e, n + e, v[e]);
+                    patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
+#pragma unroll 1
+            for (int t = 0; t < 4; ++t) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 +
+                                                                 4 * cq);
+                const int m = mb + 8 * t;
+                if (m < M)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (n + e < N)
+                            epi_store(d.ep, d.Y, (int64_t)m * N + n + e, n + e, v[e]);
             }
+            return;
+        }
+        // groups of four (N % 4 == 0: a lane's group is whole or beyond N)
+        const bool col_ok = n < N;
+        f32x4 b4 = {0.f, 0.f, 0.f, 0.f}, r[4] = {b4, b4, b4, b4};
+        if (d.ep.bias && col_ok)
+            b4 = *reinterpret_cast<const f32x4 *>(d.ep.bias + n);
+        if (d.ep.resid) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (col_ok && mb + 8 * t < M)
+                    r[t] = *reinterpret_cast<const f32x4 *>(d.ep.resid +
+                                                            (int64_t)(mb + 8 * t) * N + n);
+        }
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 +
+                                                             4 * cq);
+            const int m = mb + 8 * t;
+            if (col_ok && m < M)
+                epi_put4(d.ep, d.Y, (int64_t)m * N + n, epi_apply4(d.ep, v, b4, r[t]), true);
         }
     };
 
@@ -749,8 +781,9 @@ __device__ inline T sum_parts(const T *p, int S, int64_t count)
 
 // One launch for the split layers of a call: flat index space over every
 // job's outputs, 4-element groups for jobs that allow them (N % 4 == 0, Y
-// aligned for one 16-byte fp32 or 8-byte bf16 store), single elements
-// otherwise; each layer's epilogue is applied to its sums.
+// aligned for one 16-byte fp32 or 8-byte bf16 store, bias and residual
+// 16-byte aligned), single elements otherwise; each layer's epilogue is
+// applied to its sums.
 __global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
 {
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -781,7 +814,8 @@ hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream)
     int64_t total = 0;
     for (int i = 0; i < n; ++i) {
         const SplitSum &q = sums[i];
-        const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & (q.ep.ybf16 ? 7 : 15)) == 0;
+        const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & (q.ep.ybf16 ? 7 : 15)) == 0 &&
+                        ((uintptr_t)q.ep.bias & 15) == 0 && ((uintptr_t)q.ep.resid & 15) == 0;
         const int64_t count = v4 ? q.M * q.N / 4 : q.M * q.N;
         a.j[i] = SumJob{q.P, q.Y, q.S, v4 ? 1 : 0, count, q.N, q.ep};
         a.begin[i] = total;
@@ -808,12 +842,18 @@ int wide_wgs_per_cu(int fmt)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
 {
     dim3 grid((unsigned)args.total_tiles), block(THREADS);
+    bool epi = false;
+    for (int i = 0; i < args.n; ++i) {
+        const Epilogue &e = args.d[i].ep;
+        epi = epi || e.bias || e.resid || e.act || e.ybf16;
+    }
+    auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, block, 0, stream, args); };
     if (fmt == QL_FMT_INT8)
-        hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_INT8>, grid, block, 0, stream, args);
+        epi ? go(qgemm_wide_kernel<QL_FMT_INT8, true>) : go(qgemm_wide_kernel<QL_FMT_INT8, false>);
     else if (fmt == QL_FMT_Q4)
-        hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_Q4>, grid, block, 0, stream, args);
+        epi ? go(qgemm_wide_kernel<QL_FMT_Q4, true>) : go(qgemm_wide_kernel<QL_FMT_Q4, false>);
     else
-        hipLaunchKernelGGL(qgemm_wide_kernel<QL_FMT_F16>, grid, block, 0, stream, args);
+        epi ? go(qgemm_wide_kernel<QL_FMT_F16, true>) : go(qgemm_wide_kernel<QL_FMT_F16, false>);
     return hipGetLastError();
 }
 
