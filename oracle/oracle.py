@@ -55,6 +55,10 @@ def load(path=None):
         lib.oracle_forward_f16_rows.restype = ctypes.c_int
         lib.oracle_epilogue.argtypes = [p, i64, i64, p, p, ctypes.c_int, p]
         lib.oracle_epilogue.restype = ctypes.c_int
+        lib.oracle_quantize_act.argtypes = [p, ctypes.c_int, i64, i64, p, p]
+        lib.oracle_quantize_act.restype = ctypes.c_int
+        lib.oracle_forward_w8a8_rows.argtypes = [p, p, i64, i64, p, p, i64, p, i64, p]
+        lib.oracle_forward_w8a8_rows.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
@@ -174,6 +178,37 @@ class Oracle:
         st = self.lib.oracle_epilogue(_ptr(Y), nrows, N, None if rw is None else _ptr(rw),
                                       None if b is None else _ptr(b), act,
                                       None if r is None else _ptr(r))
+        if st != OK:
+            raise OracleError(st)
+        return Y
+
+    # W8A8 (R8)
+    def quantize_act(self, X, xdt):
+        """Per-token int8 quantization of X: (q int8 [M][K], s fp16 bits
+        [M]); raises OracleError."""
+        X = np.ascontiguousarray(X, dtype=np.float32 if xdt == DT_F32 else np.uint16)
+        M, K = X.shape
+        q = np.zeros((M, K), dtype=np.int8)
+        s = np.zeros(M, dtype=np.uint16)
+        st = self.lib.oracle_quantize_act(_ptr(X), xdt, M, K, _ptr(q), _ptr(s))
+        if st != OK:
+            raise OracleError(st)
+        return q, s
+
+    def forward_w8a8(self, qx, sx, codes, scales, N, rows=None):
+        """Y (fp64) from per-token int8 activations (qx, sx) and int8
+        weights (codes, scales), optionally only for the listed rows."""
+        qx = np.ascontiguousarray(qx, dtype=np.int8)
+        sx = np.ascontiguousarray(sx, dtype=np.uint16)
+        codes = np.ascontiguousarray(codes, dtype=np.uint8)
+        scales = np.ascontiguousarray(scales, dtype=np.uint16)
+        M, K = qx.shape
+        rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = M if rows is None else len(rows_arr)
+        Y = np.empty((nrows, N), dtype=np.float64)
+        st = self.lib.oracle_forward_w8a8_rows(
+            _ptr(qx), _ptr(sx), M, K, _ptr(codes), _ptr(scales), N,
+            None if rows_arr is None else _ptr(rows_arr), nrows, _ptr(Y))
         if st != OK:
             raise OracleError(st)
         return Y

@@ -35,6 +35,14 @@
  *       feed-forward's GELU, the residual add): Y = act(P + bias[n]) +
  *       residual[m][n] on the fp64 product P, act the identity or the GELU
  *       in its exact form x * Phi(x) = x * (1 + erf(x / sqrt 2)) / 2.
+ *   R8  W8A8 (the paper's 8-bit-arithmetic mode, Methodology and Table II:
+ *       activations quantized alongside the weights, products in 8-bit
+ *       integers).  The granularity is not stated; here one scale per
+ *       token (row of X): s_x[m] = fp16 nearest to absmax_k |X[m][k]| / 127
+ *       and q[m][k] = clamp(rint(X[m][k] / s_x[m]), -127, 127), i.e. R2 and
+ *       R3 with the whole row as the block; int8 weights as R1-R3.  Then
+ *       Y[m][n] = s_x[m] * sum_b s[n][b] * sum_{k in b} q[m][k] * c[n][k],
+ *       each block's integer sum exact.
  *
  * Exactness of the arithmetic used for R2/R3 (why fp64 is enough):
  *   - absmax / Q: the fp64 quotient differs from the exact one by less than
@@ -308,6 +316,82 @@ int oracle_forward_f16_rows(const void *X, int xdt, int64_t M, int64_t K, const 
             for (int64_t k = 0; k < K; ++k)
                 y += x_at(X, xdt, K, m, k) * oracle_f16_to_f64(W[n * K + k]);
             Y[i * N + n] = y;
+        }
+    return ORC_OK;
+}
+
+/* ---- W8A8 (R8) ----------------------------------------------------------- */
+
+/* Per-token int8 quantization of X [M][K] (fp32 or bf16 bits): q int8
+ * [M][K], s fp16 bits [M].  ORC_ERR_RANGE for a non-finite activation or a
+ * row whose rounded scale is not finite (the outputs are then unspecified). */
+int oracle_quantize_act(const void *X, int xdt, int64_t M, int64_t K, int8_t *q, uint16_t *s)
+{
+    if (xdt != ORC_DT_F32 && xdt != ORC_DT_BF16)
+        return ORC_ERR_INVALID;
+    if (M < 0 || K <= 0)
+        return ORC_ERR_SHAPE;
+    int status = ORC_OK;
+#pragma omp parallel for schedule(static) reduction(|: status)
+    for (int64_t m = 0; m < M; ++m) {
+        double absmax = 0.0;
+        int bad = 0;
+        for (int64_t k = 0; k < K; ++k) {
+            const double v = x_at(X, xdt, K, m, k);
+            if (!isfinite(v))
+                bad = 1;
+            else if (absmax < fabs(v))
+                absmax = fabs(v);
+        }
+        const uint16_t sbits = oracle_f64_to_f16(absmax / 127.0);
+        if (bad || (sbits & 0x7C00u) == 0x7C00u) {
+            status |= ORC_ERR_RANGE;
+            continue;
+        }
+        s[m] = sbits;
+        const double sv = oracle_f16_to_f64(sbits);
+        for (int64_t k = 0; k < K; ++k) {
+            double r = sv != 0.0 ? rint(x_at(X, xdt, K, m, k) / sv) : 0.0;
+            if (r > 127.0)
+                r = 127.0;
+            if (r < -127.0)
+                r = -127.0;
+            q[m * K + k] = (int8_t)r;
+        }
+    }
+    return status ? ORC_ERR_RANGE : ORC_OK;
+}
+
+/* Y[i][n] (fp64) for rows m = rows[i] (rows == NULL: m = i) of the
+ * quantized activations (qx [M][K], sx [M]) against int8 weights (codes
+ * [N][K], scales [N][K/32]). */
+int oracle_forward_w8a8_rows(const int8_t *qx, const uint16_t *sx, int64_t M, int64_t K,
+                             const uint8_t *codes, const uint16_t *scales, int64_t N,
+                             const int64_t *rows, int64_t nrows, double *Y)
+{
+    if (N <= 0 || K <= 0 || K % ORC_BLOCK || M < 0 || nrows < 0)
+        return ORC_ERR_SHAPE;
+    for (int64_t i = 0; i < nrows; ++i) {
+        int64_t m = rows ? rows[i] : i;
+        if (m < 0 || m >= M)
+            return ORC_ERR_SHAPE;
+    }
+    const int64_t nb = K / ORC_BLOCK;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < nrows; ++i)
+        for (int64_t n = 0; n < N; ++n) {
+            const int64_t row = rows ? rows[i] : i;
+            double y = 0.0;
+            for (int64_t b = 0; b < nb; ++b) {
+                int64_t dot = 0; /* exact: |dot| <= 32 * 127 * 128 */
+                for (int j = 0; j < ORC_BLOCK; ++j) {
+                    const int64_t k = b * ORC_BLOCK + j;
+                    dot += (int64_t)qx[row * K + k] *
+                           (int64_t)code_at(ORC_FMT_INT8, codes, K, n, k);
+                }
+                y += oracle_f16_to_f64(scales[n * nb + b]) * (double)dot;
+            }
+            Y[i * N + n] = oracle_f16_to_f64(sx[row]) * y;
         }
     return ORC_OK;
 }

@@ -63,6 +63,20 @@ MUTANTS = [
      "            if (residual)\n                v += (double)residual[src * N + n];\n            if (act == ORC_ACT_GELU)\n                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));"),
     ("epilogue residual ignores the row list",
      "v += (double)residual[src * N + n];", "v += (double)residual[i * N + n];"),
+    ("activation scale divisor 128",
+     "absmax / 127.0", "absmax / 128.0"),
+    ("activation codes round half away from zero",
+     "rint(x_at(X, xdt, K, m, k) / sv)", "round(x_at(X, xdt, K, m, k) / sv)"),
+    ("activation absmax ignores negative values",
+     "            else if (absmax < fabs(v))\n                absmax = fabs(v);",
+     "            else if (absmax < v)\n                absmax = v;"),
+    ("W8A8 forward drops the activation scale",
+     "Y[i * N + n] = oracle_f16_to_f64(sx[row]) * y;", "Y[i * N + n] = y;"),
+    ("W8A8 forward uses the first row's scale",
+     "Y[i * N + n] = oracle_f16_to_f64(sx[row]) * y;", "Y[i * N + n] = oracle_f16_to_f64(sx[0]) * y;"),
+    ("W8A8 forward reads the next block's weight codes",
+     "(int64_t)code_at(ORC_FMT_INT8, codes, K, n, k);",
+     "(int64_t)code_at(ORC_FMT_INT8, codes, K, n, (k + 32) % K);"),
 ]
 
 
@@ -89,6 +103,13 @@ def pin_cases():
     cases += [(pins.test_forward_f16_subnormal_and_signed_zero_weights, ())]
     cases += [(pins.test_epilogue_gelu_normal_cdf_values, ())]
     cases += [(pins.test_epilogue_bias_residual_exact_and_order, ())]
+    cases += [(pins.test_act_quant_bruteforce, (x,)) for x in (0, 1)]
+    cases += [(pins.test_act_quant_equals_weight_quantizer_one_block, ())]
+    cases += [(pins.test_act_quant_invariants, ())]
+    cases += [(pins.test_act_quant_range_errors, ())]
+    cases += [(pins.test_forward_w8a8_integer_exact, ())]
+    cases += [(pins.test_forward_w8a8_matches_dequantized_matmul, ())]
+    cases += [(pins.test_forward_w8a8_exact_rationals_tiny, ())]
     return cases
 
 

@@ -413,6 +413,134 @@ def test_epilogue_bias_residual_exact_and_order(orc):
 
 
 # --------------------------------------------------------------------------
+# W8A8: per-token int8 activations against int8 weights
+# --------------------------------------------------------------------------
+
+def bf16_bits(x):
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def bf16_vals(bits):
+    return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("xdt", [O.DT_F32, O.DT_BF16])
+def test_act_quant_bruteforce(orc, xdt):
+    """Per-token scale = the fp16 nearest to the exact row absmax / 127 (grid
+    search in rationals), codes = the nearest multiple of the scale among
+    -127..127 (all candidates tried), ties to even; rows with exact .5 ties,
+    a zero row, a row of one huge and many tiny values."""
+    rng = np.random.default_rng(61)
+    M, K = 6, 64
+    Xf = rng.standard_normal((M, K)).astype(np.float32)
+    Xf[1] = 0.0
+    Xf[2] = np.float32(1e-6) * rng.standard_normal(K).astype(np.float32)
+    Xf[2, 5] = np.float32(300.0)
+    Xf[3, :4] = [127.0, 0.5, 1.5, -2.5]  # scale 1: exact ties
+    Xf[3, 4:] = np.clip(Xf[3, 4:], -100, 100)
+    X = Xf if xdt == O.DT_F32 else bf16_bits(Xf)
+    vals = Xf.astype(np.float64) if xdt == O.DT_F32 else bf16_vals(X)
+    q, sx = orc.quantize_act(X, xdt)
+    for m in range(M):
+        sb = exact.block_scale_bits(vals[m], 127)
+        assert sx[m] == sb, (m, sx[m], sb)
+        sv = exact.f16_value(sb)
+        for k in range(K):
+            assert q[m, k] == exact.nearest_code(vals[m, k], sv, 127), (m, k)
+    assert np.all(q[1] == 0) and sx[1] == 0
+    assert list(q[3, :4]) == [127, 0, 2, -2]
+
+
+def test_act_quant_equals_weight_quantizer_one_block(orc):
+    """With K = 32 a row is one block: the per-token activation quantizer and
+    the (separately pinned) int8 weight quantizer give the same codes and
+    scales."""
+    rng = np.random.default_rng(62)
+    X = (rng.standard_normal((40, 32)) * 10.0 ** rng.integers(-3, 4, (40, 1))).astype(np.float32)
+    q, sx = orc.quantize_act(X, O.DT_F32)
+    c, s = orc.quantize(O.FMT_INT8, X)
+    assert np.array_equal(q.view(np.uint8), c)
+    assert np.array_equal(sx, s[:, 0])
+
+
+def test_act_quant_invariants(orc):
+    """DiT-like activation rows (bf16, K = 2048): |x - s q| <= s / 2, every
+    row reaches +-127, and re-quantizing the dequantized rows is the
+    identity."""
+    rng = np.random.default_rng(63)
+    Xf = (rng.standard_normal((16, 2048)) * rng.uniform(0.1, 10, (16, 1))).astype(np.float32)
+    X = bf16_bits(Xf)
+    q, sx = orc.quantize_act(X, O.DT_BF16)
+    s = f16_vals(sx)[:, None]
+    x = bf16_vals(X)
+    assert np.all(np.abs(x - s * q) <= s / 2)
+    assert np.all(np.max(np.abs(q.astype(np.int64)), axis=1) == 127)
+    q2, s2 = orc.quantize_act((s * q).astype(np.float32), O.DT_F32)
+    assert np.array_equal(q2, q) and np.array_equal(s2, sx)
+
+
+def test_act_quant_range_errors(orc):
+    X = np.ones((3, 64), np.float32)
+    for bad in (np.nan, np.inf, 65520.0 * 127):
+        Xb = X.copy()
+        Xb[1, 7] = bad
+        with pytest.raises(O.OracleError):
+            orc.quantize_act(Xb, O.DT_F32)
+
+
+def test_forward_w8a8_integer_exact(orc):
+    """Integer activations whose row absmax is 127 (scale 1, codes = X) and
+    W = c * 2^-12 with +-127 in every block (scale 2^-12, codes = c): Y is
+    the exact integer matmul times 2^-12."""
+    rng = np.random.default_rng(64)
+    M, N, K = 9, 7, 256
+    Xi = rng.integers(-127, 128, (M, K))
+    Xi[:, 3] = 127
+    C = rng.integers(-127, 128, (N, K))
+    C.reshape(N, K // 32, 32)[:, :, 0] = 127
+    q, sx = orc.quantize_act(Xi.astype(np.float32), O.DT_F32)
+    assert np.array_equal(q, Xi) and np.all(sx == 0x3C00)
+    codes, scales = orc.quantize(O.FMT_INT8, (C * 2.0 ** -12).astype(np.float32))
+    Y = orc.forward_w8a8(q, sx, codes, scales, N)
+    assert np.array_equal(Y, (Xi @ C.T).astype(np.float64) * 2.0 ** -12)
+
+
+def test_forward_w8a8_matches_dequantized_matmul(orc):
+    """Y against numpy's fp64 matmul of the dequantized activations and
+    weights, (s_x q)(s_w c)^T; and the row-subset form."""
+    rng = np.random.default_rng(65)
+    M, N, K = 20, 33, 320
+    X = bf16_bits(rng.standard_normal((M, K)).astype(np.float32))
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    q, sx = orc.quantize_act(X, O.DT_BF16)
+    codes, scales = orc.quantize(O.FMT_INT8, W)
+    Xd = f16_vals(sx)[:, None] * q.astype(np.float64)
+    Wd = orc.dequantize(O.FMT_INT8, codes, scales, N, K)
+    ref = Xd @ Wd.T
+    Y = orc.forward_w8a8(q, sx, codes, scales, N)
+    assert np.max(np.abs(Y - ref)) <= 1e-12 * np.max(np.abs(ref))
+    rows = np.array([19, 0, 7])
+    assert np.array_equal(orc.forward_w8a8(q, sx, codes, scales, N, rows=rows), Y[rows])
+
+
+def test_forward_w8a8_exact_rationals_tiny(orc):
+    """Tiny shapes in exact rationals: s_x * sum_b s_b * sum_k q c."""
+    rng = np.random.default_rng(66)
+    M, N, K = 2, 3, 64
+    X = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float32)
+    q, sx = orc.quantize_act(X, O.DT_F32)
+    codes, scales = orc.quantize(O.FMT_INT8, W)
+    c = codes.view(np.int8)
+    Y = orc.forward_w8a8(q, sx, codes, scales, N)
+    for m in range(M):
+        for n in range(N):
+            want = exact.f16_value(sx[m]) * exact.dot_exact(q[m], c[n], scales[n])
+            assert abs(Fraction(Y[m, n]) - want) <= abs(want) * Fraction(1, 2 ** 50)
+
+
+# --------------------------------------------------------------------------
 # error conventions
 # --------------------------------------------------------------------------
 
