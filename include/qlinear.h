@@ -200,6 +200,38 @@ typedef struct {
 /* qlinear_block_forward with an epilogue per layer. */
 int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t stream);
 
+/* ---- W8A8: int8 activations against int8 weights -------------------------
+ *
+ * The paper's 8-bit-arithmetic mode (Methodology; Table II): activations are
+ * quantized alongside the weights and the products run on the integer
+ * matrix cores.  Activation granularity (the paper states none): one scale
+ * per token, sx[m] = fp16 nearest to max_k |X[m][k]| / 127 (ties to even),
+ * q[m][k] = nearest integer to X[m][k] / sx[m] (ties to even), clamped to
+ * [-127, 127]: the weight rules with the whole row as the block.  Weights:
+ * QL_FMT_INT8 codes and scales as produced by qlinear_quantize.  Then
+ *
+ *     Y[m][n] = sx[m] * sum_b s[n][b] * sum_{k in block b} q[m][k] * c[n][k]
+ *
+ * with each block's integer sum exact and the block sum accumulated in
+ * fp32. */
+
+/* Per-token int8 quantization of X [M][K] (fp32 or bf16 bits, 16-byte
+ * aligned, K % 32 == 0) into qx int8 [M][K] (16-byte aligned) and sx fp16
+ * bits [M] (2-byte aligned).  Asynchronous on `stream`; M == 0 is a no-op.
+ * A row holding a NaN or Inf, or whose scale would exceed the fp16 range
+ * (max |x| >= 65520 * 127), gets the NaN scale 0x7E00 and zero codes, so
+ * that its outputs are NaN: there is no synchronous status. */
+int qlinear_quantize_act(const void *X, int xdt, int64_t M, int64_t K, int8_t *qx,
+                         uint16_t *sx, hipStream_t stream);
+
+/* Y = the W8A8 product of (qx, sx) [M][K] and int8 weights (codes [N][K],
+ * 16-byte aligned; scales [N][K/32]), then the epilogue ep (NULL: none, fp32
+ * Y).  Asynchronous; K % 32 == 0; Y must not alias an input (except
+ * ep->residual as for qlinear_forward_ep).  Errors as qlinear_forward_ep. */
+int qlinear_forward_w8a8(const int8_t *qx, const uint16_t *sx, int64_t M, int64_t K,
+                         const void *codes, const uint16_t *scales, int64_t N, void *Y,
+                         const ql_epilogue *ep, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *qlinear_status_string(int status);
 

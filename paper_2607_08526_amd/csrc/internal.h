@@ -58,6 +58,22 @@ int tile_bn(TileCfg t);
 hipError_t launch_quantize(int fmt, const float *W, int64_t N, int64_t K, uint8_t *codes,
                            uint16_t *scales, int *status, hipStream_t stream);
 
+// W8A8 (qgemm_w8a8.hip, quantize.hip): per-token int8 activations (one
+// workgroup per row, K % 32 == 0) and their product with int8 weights.
+hipError_t launch_act_quant(const void *X, bool bf16, int64_t M, int64_t K, int8_t *q,
+                            uint16_t *sx, hipStream_t stream);
+struct W8Args {
+    const int8_t *qx;        // [M][K]
+    const uint16_t *sx;      // [M] fp16 bits
+    const int8_t *codes;     // [N][K]
+    const uint16_t *scales;  // [N][K/32] fp16 bits
+    float *Y;                // [M][N] (bf16 bit patterns if ep.ybf16)
+    Epilogue ep;
+    int M, N, K;
+    int tiles_m, tiles_n;
+};
+hipError_t launch_qgemm_w8a8(const W8Args &a, hipStream_t stream);
+
 hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
                         hipStream_t stream);
 

@@ -686,6 +686,59 @@ int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream)
     return qlinear_block_forward_ep(l, n_lin, stream);
 }
 
+int qlinear_quantize_act(const void *X, int xdt, int64_t M, int64_t K, int8_t *qx,
+                         uint16_t *sx, hipStream_t stream)
+{
+    if (xdt != QL_DT_F32 && xdt != QL_DT_BF16)
+        return QL_ERR_INVALID;
+    if (M < 0 || K <= 0 || K % QL_BLOCK)
+        return QL_ERR_SHAPE;
+    if (M >= I31 || K >= I31)
+        return QL_ERR_UNSUPPORTED;
+    if (M == 0)
+        return QL_OK;
+    if (!X || !qx || !sx)
+        return QL_ERR_INVALID;
+    if (!aligned(X, 16) || !aligned(qx, 16) || !aligned(sx, 2))
+        return QL_ERR_ALIGN;
+    return launch_act_quant(X, xdt == QL_DT_BF16, M, K, qx, sx, stream) == hipSuccess
+               ? QL_OK
+               : QL_ERR_HIP;
+}
+
+int qlinear_forward_w8a8(const int8_t *qx, const uint16_t *sx, int64_t M, int64_t K,
+                         const void *codes, const uint16_t *scales, int64_t N, void *Y,
+                         const ql_epilogue *ep, hipStream_t stream)
+{
+    const ql_epilogue e = ep ? *ep : NO_EPILOGUE;
+    int st = check_epilogue(e, Y);
+    if (st != QL_OK)
+        return st;
+    if (M < 0 || N <= 0 || K <= 0 || K % QL_BLOCK)
+        return QL_ERR_SHAPE;
+    if (M >= I31 || N >= I31 || K >= I31)
+        return QL_ERR_UNSUPPORTED;
+    if (!codes || !scales || (M > 0 && (!qx || !sx || !Y)))
+        return QL_ERR_INVALID;
+    if (!aligned(codes, 16) || !aligned(scales, 2) ||
+        (M > 0 && (!aligned(qx, 16) || !aligned(sx, 2) ||
+                   !aligned(Y, e.ydt == QL_DT_BF16 ? 2 : 4))))
+        return QL_ERR_ALIGN;
+    if (M == 0)
+        return QL_OK;
+    W8Args a{};
+    a.qx = qx;
+    a.sx = sx;
+    a.codes = (const int8_t *)codes;
+    a.scales = scales;
+    a.Y = (float *)Y;
+    a.ep = to_epilogue(e);
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    return launch_qgemm_w8a8(a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
 const char *qlinear_status_string(int status)
 {
     switch (status) {

@@ -161,7 +161,119 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float *__restrict__
     }
 }
 
+// Per-token activation quantizer of the W8A8 path: one workgroup per row of
+// X.  Scale = fp16 nearest to (row absmax) / 127 and code = nearest integer
+// to x / scale clamped to [-127, 127] (the weight rules with the whole row as
+// the block).  bf16 activations have 8 significant bits, so a correctly
+// rounded fp32 quotient already decides every rounding as the exact one
+// would (a non-half-integer quotient lies at least 2^-9 of its size from
+// every half-integer, the fp32 error is below 2^-24 of it, and exact
+// half-integers are representable); fp32 activations use fp64 as the
+// weight quantizer does.  A row holding a NaN or Inf, or whose scale would
+// overflow fp16, gets the NaN scale 0x7E00 and zero codes, so its outputs
+// come out NaN.
+template <bool BF16>
+__device__ inline void load8(const void *X, int64_t e, uint32_t (&v)[8])
+{
+    if constexpr (BF16) {
+        const uint4 a = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(X) + e);
+        const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = w[j] << 16;
+            v[2 * j + 1] = w[j] & 0xFFFF0000u;
+        }
+    } else {
+        const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const float *>(X) + e);
+        const uint4 a = p[0], b = p[1];
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void act_quant_kernel(const void *__restrict__ X, int64_t K,
+                                                        int8_t *__restrict__ q,
+                                                        uint16_t *__restrict__ sx)
+{
+    __shared__ uint32_t wmax[4];
+    const int64_t row = (int64_t)blockIdx.x * K;
+    const int tid = threadIdx.x;
+    const int64_t groups = K / 8;
+    uint32_t amax = 0;  // |x| bit patterns compare like the values; NaN/Inf >= 0x7F800000
+    for (int64_t g = tid; g < groups; g += 256) {
+        uint32_t v[8];
+        load8<BF16>(X, row + 8 * g, v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t a = v[j] & 0x7FFFFFFFu;
+            amax = a > amax ? a : amax;
+        }
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = (uint32_t)__shfl_xor((int)amax, o);
+        amax = t > amax ? t : amax;
+    }
+    if ((tid & 63) == 0)
+        wmax[tid >> 6] = amax;
+    __syncthreads();
+    amax = wmax[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w)
+        amax = wmax[w] > amax ? wmax[w] : amax;
+
+    uint32_t sbits = 0x7C00;
+    if (amax < 0x7F800000u)
+        sbits = f64_to_f16_bits((double)__uint_as_float(amax) / 127.0);
+    const bool bad = sbits == 0x7C00;
+    if (tid == 0)
+        sx[blockIdx.x] = (uint16_t)(bad ? 0x7E00 : sbits);
+    const double sd = f16_bits_to_f64(sbits);
+    const float sf = (float)sd;  // exact: an fp16 value
+    for (int64_t g = tid; g < groups; g += 256) {
+        uint32_t v[8];
+        load8<BF16>(X, row + 8 * g, v);
+        int c[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            int r = 0;
+            if (!bad && sbits != 0) {
+                const float x = __uint_as_float(v[j]);
+                float t;
+                if constexpr (BF16)
+                    t = rintf(__fdiv_rn(x, sf));
+                else
+                    t = (float)rint((double)x / sd);
+                t = t > 127.0f ? 127.0f : t;
+                t = t < -127.0f ? -127.0f : t;
+                r = (int)t;
+            }
+            c[j] = r;
+        }
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            lo |= (uint32_t)(c[j] & 0xFF) << (8 * j);
+            hi |= (uint32_t)(c[j + 4] & 0xFF) << (8 * j);
+        }
+        *reinterpret_cast<uint2 *>(q + row + 8 * g) = make_uint2(lo, hi);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_act_quant(const void *X, bool bf16, int64_t M, int64_t K, int8_t *q,
+                            uint16_t *sx, hipStream_t stream)
+{
+    if (bf16)
+        hipLaunchKernelGGL(act_quant_kernel<true>, dim3((unsigned)M), dim3(256), 0, stream, X, K,
+                           q, sx);
+    else
+        hipLaunchKernelGGL(act_quant_kernel<false>, dim3((unsigned)M), dim3(256), 0, stream, X,
+                           K, q, sx);
+    return hipGetLastError();
+}
 
 hipError_t launch_quantize(int fmt, const float *W, int64_t N, int64_t K, uint8_t *codes,
                            uint16_t *scales, int *status, hipStream_t stream)

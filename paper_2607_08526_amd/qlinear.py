@@ -30,7 +30,8 @@ STATUS = {
 EXPORTS = [
     "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
     "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
-    "qlinear_block_forward_ep", "qlinear_status_string",
+    "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
+    "qlinear_status_string",
 ]
 
 
@@ -112,6 +113,11 @@ def load():
     lib.qlinear_forward_ep.restype = ci
     lib.qlinear_block_forward_ep.argtypes = [ctypes.POINTER(_LinearEp), ci, vp]
     lib.qlinear_block_forward_ep.restype = ci
+    lib.qlinear_quantize_act.argtypes = [vp, ci, i64, i64, vp, vp, vp]
+    lib.qlinear_quantize_act.restype = ci
+    lib.qlinear_forward_w8a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp,
+                                         ctypes.POINTER(_Epilogue), vp]
+    lib.qlinear_forward_w8a8.restype = ci
     lib.qlinear_block_forward.restype = ci
     lib.qlinear_status_string.argtypes = [ci]
     lib.qlinear_status_string.restype = ctypes.c_char_p
@@ -249,6 +255,32 @@ def block_forward_ep(entries, stream=None, group=None):
     arr = group if group is not None else make_group_ep(entries)
     _check(load().qlinear_block_forward_ep(arr, len(arr), _stream(stream)))
     return [e[5] for e in entries] if entries is not None else None
+
+
+def quantize_act(X, qx=None, sx=None, stream=None):
+    """Per-token int8 quantization of activations X [M][K] (fp32 or bf16):
+    returns (qx int8 [M][K], sx fp16 bits as int16 [M]).  Asynchronous."""
+    M, K = X.shape
+    if qx is None:
+        qx = torch.empty((M, K), dtype=torch.int8, device=X.device)
+    if sx is None:
+        sx = torch.empty(M, dtype=torch.int16, device=X.device)
+    _check(load().qlinear_quantize_act(_ptr(X), _xdt(X), M, K, _ptr(qx), _ptr(sx),
+                                       _stream(stream)))
+    return qx, sx
+
+
+def forward_w8a8(qx, sx, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
+                 ydtype=torch.float32, stream=None):
+    """W8A8 product of per-token int8 activations (quantize_act) and int8
+    weights (quantize(FMT_INT8, ...)), with the layer epilogue.  Asynchronous."""
+    M, K = qx.shape
+    if Y is None:
+        Y = torch.empty((M, N), dtype=ydtype, device=qx.device)
+    ep = _epilogue(Y, bias, act, residual)
+    _check(load().qlinear_forward_w8a8(_ptr(qx), _ptr(sx), M, K, _ptr(codes), _ptr(scales), N,
+                                       _ptr(Y), ctypes.byref(ep), _stream(stream)))
+    return Y
 
 
 class QuantizedLinear:

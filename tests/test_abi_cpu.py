@@ -43,7 +43,8 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
         "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
-        "qlinear_block_forward_ep", "qlinear_status_string"])
+        "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
+        "qlinear_status_string"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -172,3 +173,40 @@ def test_block_forward_ep_argument_errors(lib):
     empty[0] = _LinearEp(_Linear(Q4, None, BF16, 0, 64, 16, A16, A16, None),
                          _Epilogue(None, ACT_GELU, None, BF16))
     assert lib.qlinear_block_forward_ep(empty, 1, None) == OK
+
+
+def test_w8a8_argument_errors(lib):
+    from paper_2607_08526_amd.qlinear import _Epilogue
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.qlinear_quantize_act.argtypes = [vp, ci, i64, i64, vp, vp, vp]
+    lib.qlinear_forward_w8a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp,
+                                         ctypes.POINTER(_Epilogue), vp]
+    qa = lambda X=A16, xdt=BF16, M=4, K=64, q=A16, s=A16: lib.qlinear_quantize_act(
+        X, xdt, M, K, q, s, None)
+    assert qa(xdt=2) == INVALID
+    assert qa(K=48) == SHAPE
+    assert qa(M=-1) == SHAPE
+    assert qa(X=None) == INVALID
+    assert qa(q=None) == INVALID
+    assert qa(X=A2) == ALIGN
+    assert qa(q=A2) == ALIGN
+    assert qa(s=A1) == ALIGN
+    assert qa(M=1 << 31) == UNSUPPORTED
+    assert qa(M=0, X=None, q=None, s=None) == OK
+
+    def fw(q=A16, s=A16, M=4, K=64, c=A16, sc=A16, N=16, Y=A16, ep=None):
+        return lib.qlinear_forward_w8a8(q, s, M, K, c, sc, N, Y,
+                                        ctypes.byref(ep) if ep is not None else None, None)
+    assert fw(K=40) == SHAPE
+    assert fw(N=0) == SHAPE
+    assert fw(c=None) == INVALID
+    assert fw(sc=None) == INVALID
+    assert fw(q=None) == INVALID
+    assert fw(Y=None) == INVALID
+    assert fw(q=A2) == ALIGN
+    assert fw(c=A2) == ALIGN
+    assert fw(s=A1) == ALIGN
+    assert fw(Y=A2) == ALIGN
+    assert fw(ep=_Epilogue(None, 5, None, F32)) == INVALID
+    assert fw(Y=A1, ep=_Epilogue(None, ACT_NONE, None, BF16)) == ALIGN
+    assert fw(M=0, q=None, s=None, Y=None) == OK
