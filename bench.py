@@ -445,6 +445,60 @@ def block_int8(torch, ql, si):
             "weight_GBps": round(wbytes / t / 1e9, 1)}
 
 
+# non-packed fp32 VALU lane operations per second: 256 CUs x 4 SIMDs x 16
+# lanes x 2.4 GHz (the published 157.3 TFLOP/s counts packed FMAs, which this
+# build does not emit)
+VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+INT8_MFMA_PEAK_TOPS = 5000.0
+
+
+def block_w8a8(torch, ql, si):
+    """One DiT block (d = 2048, 2048 tokens) in W8A8: the per-token
+    quantization of both activation tensors and the four int8 products, on
+    the same int8 weights and activations as block_int8; graph-timed."""
+    dev = torch.device("cuda")
+    xa, xb = si.block_activations()
+    xa_d = torch.from_numpy(xa.view("int16")).to(dev)
+    xb_d = torch.from_numpy(xb.view("int16")).to(dev)
+    qa, sa = ql.quantize_act(xa_d)
+    qb, sb = ql.quantize_act(xb_d)
+    lin = si.block_linears()
+    ws, Ys = [], []
+    for i, (name, N, K) in enumerate(lin):
+        ws.append(ql.quantize(ql.FMT_INT8, torch.from_numpy(si.block_int8_weight(i)).to(dev)))
+        Ys.append(torch.empty((xa.shape[0], N), dtype=torch.float32, device=dev))
+    wide = [K == 4 * si.D_MODEL for _, _, K in lin]
+
+    def quant():
+        ql.quantize_act(xa_d, qa, sa)
+        ql.quantize_act(xb_d, qb, sb)
+
+    def gemms():
+        for i, (_, N, K) in enumerate(lin):
+            q, s_ = (qb, sb) if wide[i] else (qa, sa)
+            ql.forward_w8a8(q, s_, ws[i][0], ws[i][1], N, Y=Ys[i])
+
+    def both():
+        quant()
+        gemms()
+
+    t_all = graph_time(torch, both)[0]
+    t_q = graph_time(torch, quant)[0]
+    t_g = graph_time(torch, gemms)[0]
+    M = xa.shape[0]
+    mnk = sum(M * N * K for _, N, K in lin)
+    valu_floor_us = mnk / 16 / VALU_LANE_OPS * 1e6  # cvt + FMA per output per 32-k block
+    tops = 2.0 * mnk / (t_all * 1e-3) / 1e12
+    return {"note": "per-token int8 activations x int8 block-32 weights: activation "
+                    "quantization (both X) + 4 int8-MFMA products, same inputs as block_int8",
+            "us_per_block": round(t_all * 1e3, 2), "act_quant_us": round(t_q * 1e3, 2),
+            "gemm_us": round(t_g * 1e3, 2), "TOPs": round(tops, 1),
+            "gemm_TOPs": round(2.0 * mnk / (t_g * 1e-3) / 1e12, 1),
+            "int8_mfma_frac": round(2.0 * mnk / (t_g * 1e-3) / 1e12 / INT8_MFMA_PEAK_TOPS, 4),
+            "valu_floor_us": round(valu_floor_us, 1),
+            "valu_frac": round(valu_floor_us / (t_g * 1e3), 4)}
+
+
 def paper_widths(torch, ql, si):
     """The paper's two DiT widths (q4, distinct weights per block) at the
     tokens of one 10 s clip: one step = every block's grouped call, timed as
@@ -575,6 +629,7 @@ def main():
     if args.sweeps_only:
         print(json.dumps({"skinny": skinny_sweep(torch, ql, si),
                           "block_int8": block_int8(torch, ql, si),
+                          "block_w8a8": block_w8a8(torch, ql, si),
                           "paper_widths": paper_widths(torch, ql, si)}), flush=True)
         return
 
@@ -637,6 +692,7 @@ def main():
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)
+        res["block_w8a8"] = block_w8a8(torch, ql, si)
         res["paper_widths"] = paper_widths(torch, ql, si)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(step, si, args.cpu_seconds)
