@@ -59,6 +59,8 @@ def load(path=None):
         lib.oracle_quantize_act.restype = ctypes.c_int
         lib.oracle_forward_w8a8_rows.argtypes = [p, p, i64, i64, p, p, i64, p, i64, p]
         lib.oracle_forward_w8a8_rows.restype = ctypes.c_int
+        lib.oracle_steer.argtypes = [p, i64, i64, p, ctypes.c_double, ctypes.c_double]
+        lib.oracle_steer.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
@@ -178,6 +180,18 @@ class Oracle:
         st = self.lib.oracle_epilogue(_ptr(Y), nrows, N, None if rw is None else _ptr(rw),
                                       None if b is None else _ptr(b), act,
                                       None if r is None else _ptr(r))
+        if st != OK:
+            raise OracleError(st)
+        return Y
+
+    # steering (R9)
+    def steer(self, Y, direction, hnorm, alpha):
+        """Y + alpha * hnorm * direction[n] on every row (Eq. 2), fp64; a
+        new array."""
+        Y = np.array(Y, dtype=np.float64, order="C", copy=True)
+        d = np.ascontiguousarray(direction, dtype=np.float32)
+        nrows, N = Y.shape
+        st = self.lib.oracle_steer(_ptr(Y), nrows, N, _ptr(d), float(hnorm), float(alpha))
         if st != OK:
             raise OracleError(st)
         return Y

@@ -35,6 +35,10 @@
  *       feed-forward's GELU, the residual add): Y = act(P + bias[n]) +
  *       residual[m][n] on the fp64 product P, act the identity or the GELU
  *       in its exact form x * Phi(x) = x * (1 + erf(x / sqrt 2)) / 2.
+ *   R9  steering (Methodology, additive injection, Eq. 2): the chosen
+ *       block's output h gains alpha * ||h_bar|| * d for every token, d a
+ *       unit direction [N], ||h_bar|| the layer's mean residual norm and
+ *       alpha >= 0 the strength; alpha = 0 leaves h untouched.
  *   R8  W8A8 (the paper's 8-bit-arithmetic mode, Methodology and Table II:
  *       activations quantized alongside the weights, products in 8-bit
  *       integers).  The granularity is not stated; here one scale per
@@ -424,6 +428,26 @@ int oracle_epilogue(double *Y, int64_t nrows, int64_t N, const int64_t *rows,
             Y[i * N + n] = v;
         }
     }
+    return ORC_OK;
+}
+
+/* ---- steering (R9) ------------------------------------------------------ */
+
+/* In place on Y (fp64, nrows x N): Y[i][n] += alpha * hnorm * dir[n], the
+ * additive injection of Eq. 2; alpha == 0 leaves Y untouched. */
+int oracle_steer(double *Y, int64_t nrows, int64_t N, const float *dir, double hnorm,
+                 double alpha)
+{
+    if (N <= 0 || nrows < 0)
+        return ORC_ERR_SHAPE;
+    if (!dir)
+        return ORC_ERR_INVALID;
+    if (alpha == 0.0)
+        return ORC_OK;
+    const double c = alpha * hnorm;
+    for (int64_t i = 0; i < nrows; ++i)
+        for (int64_t n = 0; n < N; ++n)
+            Y[i * N + n] += c * (double)dir[n];
     return ORC_OK;
 }
 

@@ -63,6 +63,12 @@ MUTANTS = [
      "            if (residual)\n                v += (double)residual[src * N + n];\n            if (act == ORC_ACT_GELU)\n                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));"),
     ("epilogue residual ignores the row list",
      "v += (double)residual[src * N + n];", "v += (double)residual[i * N + n];"),
+    ("steering ignores the residual norm",
+     "const double c = alpha * hnorm;", "const double c = alpha;"),
+    ("steering applied at zero strength",
+     "    if (alpha == 0.0)\n        return ORC_OK;\n    const double c", "    const double c"),
+    ("steering indexes the direction by row",
+     "Y[i * N + n] += c * (double)dir[n];", "Y[i * N + n] += c * (double)dir[(i + n) % N];"),
     ("activation scale divisor 128",
      "absmax / 127.0", "absmax / 128.0"),
     ("activation codes round half away from zero",
@@ -103,6 +109,8 @@ def pin_cases():
     cases += [(pins.test_forward_f16_subnormal_and_signed_zero_weights, ())]
     cases += [(pins.test_epilogue_gelu_normal_cdf_values, ())]
     cases += [(pins.test_epilogue_bias_residual_exact_and_order, ())]
+    cases += [(pins.test_steer_zero_strength_is_identity, ())]
+    cases += [(pins.test_steer_rank_one_shift, ())]
     cases += [(pins.test_act_quant_bruteforce, (x,)) for x in (0, 1)]
     cases += [(pins.test_act_quant_equals_weight_quantizer_one_block, ())]
     cases += [(pins.test_act_quant_invariants, ())]

@@ -413,6 +413,47 @@ def test_epilogue_bias_residual_exact_and_order(orc):
 
 
 # --------------------------------------------------------------------------
+# steering: additive injection (Eq. 2)
+# --------------------------------------------------------------------------
+
+def unit_direction(rng, N):
+    d = rng.standard_normal(N)
+    return (d / np.linalg.norm(d)).astype(np.float32)
+
+
+def test_steer_zero_strength_is_identity(orc):
+    """alpha = 0 leaves every value bit for bit, -0.0 and NaN included."""
+    rng = np.random.default_rng(71)
+    Y = rng.standard_normal((5, 16))
+    Y[0, 0], Y[1, 1] = -0.0, np.nan
+    out = orc.steer(Y, unit_direction(rng, 16), 3.5, 0.0)
+    assert np.array_equal(out.view(np.uint64), Y.view(np.uint64))
+
+
+def test_steer_rank_one_shift(orc):
+    """Every row moves by the same vector, of length alpha * ||h_bar|| along
+    the unit direction d (cosine 1), and the shift is linear in alpha
+    (dyadic strengths: exact)."""
+    rng = np.random.default_rng(72)
+    N = 64
+    d = unit_direction(rng, N)
+    Y = rng.standard_normal((7, N))
+    hnorm = 12.5
+    for alpha in (0.25, 0.5, 1.0):
+        shift = orc.steer(np.zeros_like(Y), d, hnorm, alpha)
+        assert np.all(shift == shift[0])
+        assert abs(np.linalg.norm(shift[0]) - alpha * hnorm * np.linalg.norm(d.astype(np.float64))) \
+            <= 1e-13 * alpha * hnorm
+        cosv = shift[0] @ d.astype(np.float64) / np.linalg.norm(shift[0]) / np.linalg.norm(
+            d.astype(np.float64))
+        assert abs(cosv - 1.0) < 1e-15
+        assert np.array_equal(orc.steer(Y, d, hnorm, alpha), Y + shift)
+    s1 = orc.steer(np.zeros((1, N)), d, hnorm, 0.25)
+    s2 = orc.steer(np.zeros((1, N)), d, hnorm, 0.5)
+    assert np.array_equal(2 * s1, s2)
+
+
+# --------------------------------------------------------------------------
 # W8A8: per-token int8 activations against int8 weights
 # --------------------------------------------------------------------------
 
