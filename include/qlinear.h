@@ -166,6 +166,7 @@ int qlinear_block_forward(const ql_linear *lin, int n_lin, hipStream_t stream);
  * that stores each output element:
  *
  *     Y[m][n] = act(P[m][n] + bias[n]) + residual[m][n]
+ *               (+ alpha * steer_norm * steer_dir[n], see below)
  *
  * with P the product of qlinear_forward, in fp32.  act: QL_ACT_NONE, or
  * QL_ACT_GELU in its exact form x * (1 + erf(x / sqrt 2)) / 2.  bias fp32
@@ -181,6 +182,15 @@ typedef struct {
     int act;                /* ql_act */
     const float *residual;  /* [M][N] or NULL */
     int ydt;                /* ql_dtype of Y */
+    /* Steering (Methodology, additive injection, Eq. 2) on the block's
+     * output: + alpha * steer_norm * steer_dir[n], alpha = *steer_strength
+     * read from device memory by every launch (a captured graph picks up a
+     * new strength without re-capture); skipped, bit for bit, when alpha is
+     * 0.  steer_dir: unit direction fp32 [N] (4-byte aligned) or NULL for
+     * none; steer_norm: the layer's mean residual norm ||h_bar||. */
+    const float *steer_dir;
+    float steer_norm;
+    const float *steer_strength;  /* device fp32 scalar; required with steer_dir */
 } ql_epilogue;
 
 /* qlinear_forward with an epilogue (ep == NULL: none, fp32 Y).  Y is fp32 or
@@ -231,6 +241,15 @@ int qlinear_quantize_act(const void *X, int xdt, int64_t M, int64_t K, int8_t *q
 int qlinear_forward_w8a8(const int8_t *qx, const uint16_t *sx, int64_t M, int64_t K,
                          const void *codes, const uint16_t *scales, int64_t N, void *Y,
                          const ql_epilogue *ep, hipStream_t stream);
+
+/* The steering injection alone (Methodology, additive injection, Eq. 2):
+ * h[m][n] += alpha * hnorm * dir[n] on the residual stream h fp32 [M][N] in
+ * place, alpha = *strength read from device memory at run time; nothing is
+ * written when alpha is 0 (h stays bit for bit).  dir: unit direction fp32
+ * [N].  Pointers 4-byte aligned; h must not alias dir or strength.
+ * Asynchronous on `stream`; M == 0 is a no-op. */
+int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
+                  const float *strength, hipStream_t stream);
 
 /* Static description of a status code. */
 const char *qlinear_status_string(int status);

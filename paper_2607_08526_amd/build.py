@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libqlinear.so")
 SOURCES = ["qlinear.hip", "quantize.hip", "qgemm.hip", "qgemm_wide.hip", "qgemm_skinny.hip", "xprep.hip", "qgemm_stream.hip", "qgemv.hip",
-           "qgemm_w8a8.hip"]
+           "qgemm_w8a8.hip", "steer.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

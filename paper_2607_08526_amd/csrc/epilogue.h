@@ -1,8 +1,13 @@
 // Fused epilogue of a linear layer, applied by whichever kernel stores a
 // final output element (never to split partials): the rest of a DiT block's
-// linear -- bias, the feed-forward's GELU, the residual add --
+// linear -- bias, the feed-forward's GELU, the residual add -- and the
+// steering injection of the paper's Eq. 2 on the block's output,
 //
-//   Y[m][n] = act(P[m][n] + bias[n]) + resid[m][n]          (fp32)
+//   Y[m][n] = act(P[m][n] + bias[n]) + resid[m][n] + alpha hnorm d[n]  (fp32)
+//
+// with alpha read from device memory by every launch (a captured graph
+// picks up a new strength without re-capture); at alpha = 0 the term is
+// skipped, so the output is bit for bit the unsteered one.
 //
 // act the identity or the GELU in its exact (erf) form x * Phi(x) =
 // x * (1 + erf(x / sqrt 2)) / 2, then stored as fp32 or as bf16 (round to
@@ -40,6 +45,11 @@ __device__ inline float epi_value(const Epilogue &e, int64_t idx, int n, float v
         v = epi_gelu(v);
     if (e.resid)
         v += e.resid[idx];
+    if (e.steer) {
+        const float a = *e.strength;
+        if (a != 0.0f)
+            v += (a * e.hnorm) * e.steer[n];
+    }
     return v;
 }
 
@@ -67,13 +77,35 @@ __device__ inline void epi_store(const Epilogue &e, float *Y, int64_t idx, int n
 __device__ inline bool epi_vec_ok(const Epilogue &e, const float *Y, int64_t N)
 {
     return (N & 3) == 0 && ((uintptr_t)Y & (e.ybf16 ? 7 : 15)) == 0 &&
-           ((uintptr_t)e.bias & 15) == 0 && ((uintptr_t)e.resid & 15) == 0;
+           ((uintptr_t)e.bias & 15) == 0 && ((uintptr_t)e.resid & 15) == 0 &&
+           ((uintptr_t)e.steer & 15) == 0;
 }
 
-// the epilogue of four consecutive elements, their bias and residual values
-// already loaded (b4, r4: ignored when the layer has none)
+// the steering term of four consecutive columns n .. n + 3 (zero, and not
+// to be added, when alpha is 0: see epi_apply4)
 template <typename V4>
-__device__ inline V4 epi_apply4(const Epilogue &e, V4 v, V4 b4, V4 r4)
+__device__ inline V4 epi_steer4(const Epilogue &e, int n, float &alpha)
+{
+    V4 s4 = {0.f, 0.f, 0.f, 0.f};
+    alpha = 0.0f;
+    if (e.steer) {
+        alpha = *e.strength;
+        if (alpha != 0.0f) {
+            const float c = alpha * e.hnorm;
+            s4 = *reinterpret_cast<const V4 *>(e.steer + n);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                s4[q] = c * s4[q];
+        }
+    }
+    return s4;
+}
+
+// the epilogue of four consecutive elements, their bias, residual and
+// steering values already loaded (b4, r4, s4: ignored when the layer has
+// none, s4 also when alpha is 0)
+template <typename V4>
+__device__ inline V4 epi_apply4(const Epilogue &e, V4 v, V4 b4, V4 r4, V4 s4, float alpha)
 {
     if (e.bias)
         v += b4;
@@ -84,6 +116,8 @@ __device__ inline V4 epi_apply4(const Epilogue &e, V4 v, V4 b4, V4 r4)
     }
     if (e.resid)
         v += r4;
+    if (alpha != 0.0f)
+        v += s4;
     return v;
 }
 
@@ -120,7 +154,9 @@ __device__ inline void epi_store4(const Epilogue &e, float *Y, int64_t idx, int 
         b4 = *reinterpret_cast<const V4 *>(e.bias + n);
     if (e.resid)
         r4 = *reinterpret_cast<const V4 *>(e.resid + idx);
-    epi_put4(e, Y, idx, epi_apply4(e, v, b4, r4), nt);
+    float alpha;
+    const V4 s4 = epi_steer4<V4>(e, n, alpha);
+    epi_put4(e, Y, idx, epi_apply4(e, v, b4, r4, s4, alpha), nt);
 }
 
 }  // namespace qlk

@@ -10,13 +10,23 @@
 namespace qlk {
 
 // A layer's epilogue as the kernels see it (see epilogue.h): Y[m][n] =
-// act(P + bias[n]) + resid[m][n], stored as fp32 or (ybf16) bf16.
+// act(P + bias[n]) + resid[m][n] (+ alpha * hnorm * steer[n] when
+// alpha = *strength is not 0), stored as fp32 or (ybf16) bf16.
 struct Epilogue {
-    const float *bias;   // [N] or nullptr
-    const float *resid;  // [M][N] or nullptr
-    int act;             // QL_ACT_NONE / QL_ACT_GELU
-    int ybf16;           // Y holds bf16 bit patterns
+    const float *bias;      // [N] or nullptr
+    const float *resid;     // [M][N] or nullptr
+    const float *steer;     // unit direction [N] or nullptr
+    const float *strength;  // device scalar alpha, read at every launch
+    float hnorm;            // the layer's mean residual norm
+    int act;                // QL_ACT_NONE / QL_ACT_GELU
+    int ybf16;              // Y holds bf16 bit patterns
 };
+
+// an epilogue beyond the plain fp32 store
+__host__ __device__ inline bool epi_active(const Epilogue &e)
+{
+    return e.bias || e.resid || e.steer || e.act || e.ybf16;
+}
 
 // Activations and packed codes of one linear layer as the kernels see it.
 struct LinDesc {
@@ -73,6 +83,10 @@ struct W8Args {
     int tiles_m, tiles_n;
 };
 hipError_t launch_qgemm_w8a8(const W8Args &a, hipStream_t stream);
+
+// The steering injection alone, in place on h [M][N] fp32 (steer.hip).
+hipError_t launch_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
+                        const float *strength, hipStream_t stream);
 
 hipError_t launch_qgemm(int fmt, bool xf32, TileCfg t, const GroupArgs &args,
                         hipStream_t stream);

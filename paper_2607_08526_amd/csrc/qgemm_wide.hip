@@ -567,7 +567,7 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     float *const Yd = to_part ? d.part + (int64_t)part * M * N : d.Y;
     const bool vec = (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0;
     // a layer epilogue beyond the plain fp32 store (final outputs only)
-    const bool epi = EPI && !to_part && (d.ep.bias || d.ep.resid || d.ep.act || d.ep.ybf16);
+    const bool epi = EPI && !to_part && epi_active(d.ep);
     const bool vec_epi = epi_vec_ok(d.ep, d.Y, N);
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
         const int lane = tid & 63;
@@ -636,6 +636,8 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         f32x4 b4 = {0.f, 0.f, 0.f, 0.f}, r[4] = {b4, b4, b4, b4};
         if (d.ep.bias && col_ok)
             b4 = *reinterpret_cast<const f32x4 *>(d.ep.bias + n);
+        float alpha = 0.0f;
+        const f32x4 s4 = col_ok ? epi_steer4<f32x4>(d.ep, n, alpha) : b4;
         if (d.ep.resid) {
 #pragma unroll
             for (int t = 0; t < 4; ++t)
@@ -654,7 +656,8 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
                                                              4 * cq);
             const int m = mb + 8 * t;
             if (col_ok && m < M)
-                epi_put4(d.ep, d.Y, (int64_t)m * N + n, epi_apply4(d.ep, v, b4, r[t]), true);
+                epi_put4(d.ep, d.Y, (int64_t)m * N + n, epi_apply4(d.ep, v, b4, r[t], s4, alpha),
+                         true);
         }
     };
 
@@ -781,9 +784,9 @@ __device__ inline T sum_parts(const T *p, int S, int64_t count)
 
 // One launch for the split layers of a call: flat index space over every
 // job's outputs, 4-element groups for jobs that allow them (N % 4 == 0, Y
-// aligned for one 16-byte fp32 or 8-byte bf16 store, bias and residual
-// 16-byte aligned), single elements otherwise; each layer's epilogue is
-// applied to its sums.
+// aligned for one 16-byte fp32 or 8-byte bf16 store, bias, residual and
+// steering direction 16-byte aligned), single elements otherwise; each
+// layer's epilogue is applied to its sums.
 __global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
 {
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -795,12 +798,14 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const SumArgs a)
                 ji = i;
         const SumJob &jb = a.j[ji];
         const int64_t i = x - a.begin[ji];
+        // the column is needed only by the per-column terms
+        const bool col = jb.ep.bias || jb.ep.steer;
         if (jb.v4) {
             const f32x4 y = sum_parts(reinterpret_cast<const f32x4 *>(jb.P) + i, jb.S, jb.count);
-            const int n = jb.ep.bias ? (int)((4 * i) % jb.N) : 0;
+            const int n = col ? (int)((4 * i) % jb.N) : 0;
             epi_store4(jb.ep, jb.Y, 4 * i, n, y, true);
         } else {
-            const int n = jb.ep.bias ? (int)(i % jb.N) : 0;
+            const int n = col ? (int)(i % jb.N) : 0;
             epi_store(jb.ep, jb.Y, i, n, sum_parts(jb.P + i, jb.S, jb.count));
         }
     }
@@ -815,7 +820,8 @@ hipError_t launch_split_sum(const SplitSum *sums, int n, hipStream_t stream)
     for (int i = 0; i < n; ++i) {
         const SplitSum &q = sums[i];
         const bool v4 = q.N % 4 == 0 && ((uintptr_t)q.Y & (q.ep.ybf16 ? 7 : 15)) == 0 &&
-                        ((uintptr_t)q.ep.bias & 15) == 0 && ((uintptr_t)q.ep.resid & 15) == 0;
+                        ((uintptr_t)q.ep.bias & 15) == 0 && ((uintptr_t)q.ep.resid & 15) == 0 &&
+                        ((uintptr_t)q.ep.steer & 15) == 0;
         const int64_t count = v4 ? q.M * q.N / 4 : q.M * q.N;
         a.j[i] = SumJob{q.P, q.Y, q.S, v4 ? 1 : 0, count, q.N, q.ep};
         a.begin[i] = total;
@@ -845,7 +851,7 @@ hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream)
     bool epi = false;
     for (int i = 0; i < args.n; ++i) {
         const Epilogue &e = args.d[i].ep;
-        epi = epi || e.bias || e.resid || e.act || e.ybf16;
+        epi = epi || epi_active(e);
     }
     auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, block, 0, stream, args); };
     if (fmt == QL_FMT_INT8)

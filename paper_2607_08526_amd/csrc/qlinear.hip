@@ -43,7 +43,7 @@ int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const vo
     return QL_OK;
 }
 
-const ql_epilogue NO_EPILOGUE = {nullptr, QL_ACT_NONE, nullptr, QL_DT_F32};
+const ql_epilogue NO_EPILOGUE = {nullptr, QL_ACT_NONE, nullptr, QL_DT_F32, nullptr, 0.0f, nullptr};
 
 // an epilogue's enums, aliasing and alignment (before check_linear, which
 // takes its ydt)
@@ -55,7 +55,10 @@ int check_epilogue(const ql_epilogue &ep, const void *Y)
     // an in-place residual add needs fp32 Y
     if (ep.ydt == QL_DT_BF16 && ep.residual && (const void *)ep.residual == Y)
         return QL_ERR_INVALID;
-    if (!aligned(ep.bias, 4) || !aligned(ep.residual, 4))
+    if (ep.steer_dir && !ep.steer_strength)
+        return QL_ERR_INVALID;
+    if (!aligned(ep.bias, 4) || !aligned(ep.residual, 4) ||
+        (ep.steer_dir && (!aligned(ep.steer_dir, 4) || !aligned(ep.steer_strength, 4))))
         return QL_ERR_ALIGN;
     return QL_OK;
 }
@@ -71,7 +74,13 @@ int check_layer(const ql_linear_ep &l)
 
 Epilogue to_epilogue(const ql_epilogue &e)
 {
-    return Epilogue{e.bias, e.residual, e.act, e.ydt == QL_DT_BF16 ? 1 : 0};
+    return Epilogue{e.bias,
+                    e.residual,
+                    e.steer_dir,
+                    e.steer_dir ? e.steer_strength : nullptr,
+                    e.steer_norm,
+                    e.act,
+                    e.ydt == QL_DT_BF16 ? 1 : 0};
 }
 
 // Stream-ordered pool (one per device) that the per-stream workspaces below
@@ -737,6 +746,23 @@ int qlinear_forward_w8a8(const int8_t *qx, const uint16_t *sx, int64_t M, int64_
     a.N = (int)N;
     a.K = (int)K;
     return launch_qgemm_w8a8(a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
+int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
+                  const float *strength, hipStream_t stream)
+{
+    if (M < 0 || N <= 0)
+        return QL_ERR_SHAPE;
+    if (M >= I31 || N >= I31)
+        return QL_ERR_UNSUPPORTED;
+    if (!dir || !strength || (M > 0 && !h))
+        return QL_ERR_INVALID;
+    if (!aligned(h, 4) || !aligned(dir, 4) || !aligned(strength, 4))
+        return QL_ERR_ALIGN;
+    if (M == 0)
+        return QL_OK;
+    return launch_steer(h, M, N, dir, hnorm, strength, stream) == hipSuccess ? QL_OK
+                                                                             : QL_ERR_HIP;
 }
 
 const char *qlinear_status_string(int status)

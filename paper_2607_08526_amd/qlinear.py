@@ -31,7 +31,7 @@ EXPORTS = [
     "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
     "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
     "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
-    "qlinear_status_string",
+    "qlinear_steer", "qlinear_status_string",
 ]
 
 
@@ -61,6 +61,9 @@ class _Epilogue(ctypes.Structure):
         ("act", ctypes.c_int),
         ("residual", ctypes.c_void_p),
         ("ydt", ctypes.c_int),
+        ("steer_dir", ctypes.c_void_p),
+        ("steer_norm", ctypes.c_float),
+        ("steer_strength", ctypes.c_void_p),
     ]
 
 
@@ -118,6 +121,8 @@ def load():
     lib.qlinear_forward_w8a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp,
                                          ctypes.POINTER(_Epilogue), vp]
     lib.qlinear_forward_w8a8.restype = ci
+    lib.qlinear_steer.argtypes = [vp, i64, i64, vp, ctypes.c_float, vp, vp]
+    lib.qlinear_steer.restype = ci
     lib.qlinear_block_forward.restype = ci
     lib.qlinear_status_string.argtypes = [ci]
     lib.qlinear_status_string.restype = ctypes.c_char_p
@@ -197,12 +202,18 @@ def _ydt(Y):
     raise TypeError(f"outputs must be float32 or bfloat16, not {Y.dtype}")
 
 
-def _epilogue(Y, bias, act, residual):
-    return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y))
+def _epilogue(Y, bias, act, residual, steer=None):
+    """steer: None, or (direction fp32 [N], hnorm float, strength: a device
+    fp32 tensor of one element, re-read by every launch)."""
+    if steer is None:
+        return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y), None, 0.0, None)
+    d, hnorm, strength = steer
+    return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y), _ptr(d), float(hnorm),
+                     _ptr(strength))
 
 
 def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
-               ydtype=torch.float32, stream=None):
+               ydtype=torch.float32, steer=None, stream=None):
     """forward() with the layer epilogue fused into the output store:
     Y = act(X . W^T + bias) + residual, Y fp32 or bf16 (ydtype, or Y's dtype
     when Y is given).  bias fp32 [N], residual fp32 [M][N] (may be Y itself
@@ -210,7 +221,7 @@ def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residu
     M, K = X.shape
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=X.device)
-    ep = _epilogue(Y, bias, act, residual)
+    ep = _epilogue(Y, bias, act, residual, steer)
     _check(load().qlinear_forward_ep(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
                                      _ptr(Y), ctypes.byref(ep), _stream(stream)))
     return Y
@@ -238,14 +249,17 @@ def block_forward(entries, stream=None, group=None):
 
 def make_group_ep(entries):
     """ctypes array for block_forward_ep from (fmt, X, codes, scales, N, Y,
-    bias, act, residual) tuples (bias/residual None for none; Y fp32 or bf16).
-    The tensors must outlive every use of the returned array."""
+    bias, act, residual[, steer]) tuples (bias/residual/steer None for none;
+    Y fp32 or bf16).  The tensors must outlive every use of the returned
+    array."""
     arr = (_LinearEp * len(entries))()
-    for i, (fmt, X, codes, scales, N, Y, bias, act, residual) in enumerate(entries):
+    for i, e in enumerate(entries):
+        fmt, X, codes, scales, N, Y, bias, act, residual = e[:9]
+        steer = e[9] if len(e) > 9 else None
         M, K = X.shape
         lin = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                       scales.data_ptr() if scales is not None else 0, Y.data_ptr())
-        arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual))
+        arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual, steer))
     return arr
 
 
@@ -271,16 +285,26 @@ def quantize_act(X, qx=None, sx=None, stream=None):
 
 
 def forward_w8a8(qx, sx, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
-                 ydtype=torch.float32, stream=None):
+                 ydtype=torch.float32, steer=None, stream=None):
     """W8A8 product of per-token int8 activations (quantize_act) and int8
     weights (quantize(FMT_INT8, ...)), with the layer epilogue.  Asynchronous."""
     M, K = qx.shape
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=qx.device)
-    ep = _epilogue(Y, bias, act, residual)
+    ep = _epilogue(Y, bias, act, residual, steer)
     _check(load().qlinear_forward_w8a8(_ptr(qx), _ptr(sx), M, K, _ptr(codes), _ptr(scales), N,
                                        _ptr(Y), ctypes.byref(ep), _stream(stream)))
     return Y
+
+
+def steer(h, direction, hnorm, strength, stream=None):
+    """h += alpha * hnorm * direction on every row, in place (Eq. 2), with
+    alpha = strength[0] read on the device at run time (skipped exactly when
+    alpha is 0).  Asynchronous."""
+    M, N = h.shape
+    _check(load().qlinear_steer(_ptr(h), M, N, _ptr(direction), float(hnorm), _ptr(strength),
+                                _stream(stream)))
+    return h
 
 
 class QuantizedLinear:

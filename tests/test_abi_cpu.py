@@ -44,7 +44,7 @@ def test_header_declares_the_boundary():
         "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
         "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
         "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
-        "qlinear_status_string"])
+        "qlinear_steer", "qlinear_status_string"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -126,9 +126,10 @@ def test_block_forward_argument_errors(lib):
     assert lib.qlinear_block_forward(empty, 1, None) == OK  # all layers empty: no-op
 
 
-def fwd_ep(lib, bias=None, act=ACT_NONE, residual=None, ydt=F32, Y=A16, M=4, ep=True):
+def fwd_ep(lib, bias=None, act=ACT_NONE, residual=None, ydt=F32, Y=A16, M=4, ep=True,
+           sdir=None, sstr=None):
     from paper_2607_08526_amd.qlinear import _Epilogue
-    e = _Epilogue(bias, act, residual, ydt)
+    e = _Epilogue(bias, act, residual, ydt, sdir, 1.0, sstr)
     return lib.qlinear_forward_ep(INT8, A16, BF16, M, 64, A16, A16, 16, Y,
                                   ctypes.byref(e) if ep else None, None)
 
@@ -149,6 +150,11 @@ def test_forward_ep_argument_errors(lib):
     assert fwd_ep(lib, Y=A2, ydt=F32) == ALIGN
     # an in-place residual add needs fp32 Y
     assert fwd_ep(lib, residual=A16, Y=A16, ydt=BF16) == INVALID
+    # steering needs its device strength; 4-byte alignment
+    assert fwd_ep(lib, sdir=A16, sstr=None) == INVALID
+    assert fwd_ep(lib, sdir=A2, sstr=A16) == ALIGN
+    assert fwd_ep(lib, sdir=A16, sstr=A2) == ALIGN
+    assert fwd_ep(lib, sdir=None, sstr=A2, M=0) == OK
     # the checks of qlinear_forward still apply; no epilogue is the plain call
     assert lib.qlinear_forward_ep(5, A16, BF16, 4, 64, A16, A16, 16, A16, None, None) == INVALID
     assert fwd_ep(lib, M=0, ep=False) == OK
@@ -210,3 +216,18 @@ def test_w8a8_argument_errors(lib):
     assert fw(ep=_Epilogue(None, 5, None, F32)) == INVALID
     assert fw(Y=A1, ep=_Epilogue(None, ACT_NONE, None, BF16)) == ALIGN
     assert fw(M=0, q=None, s=None, Y=None) == OK
+
+
+def test_steer_argument_errors(lib):
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    lib.qlinear_steer.argtypes = [vp, i64, i64, vp, ctypes.c_float, vp, vp]
+    st = lambda h=A16, M=4, N=16, d=A16, s=A16: lib.qlinear_steer(h, M, N, d, 1.0, s, None)
+    assert st(N=0) == SHAPE
+    assert st(M=-1) == SHAPE
+    assert st(d=None) == INVALID
+    assert st(s=None) == INVALID
+    assert st(h=None) == INVALID
+    assert st(h=A2) == ALIGN
+    assert st(d=A1) == ALIGN
+    assert st(M=1 << 31) == UNSUPPORTED
+    assert st(M=0, h=None) == OK
