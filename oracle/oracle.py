@@ -61,6 +61,9 @@ def load(path=None):
         lib.oracle_forward_w8a8_rows.restype = ctypes.c_int
         lib.oracle_steer.argtypes = [p, i64, i64, p, ctypes.c_double, ctypes.c_double]
         lib.oracle_steer.restype = ctypes.c_int
+        lib.oracle_attention_rows.argtypes = [p, i64, p, i64, p, i64, i64, i64, i64, i64,
+                                              ctypes.c_double, p, i64, p]
+        lib.oracle_attention_rows.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         _LIBS[path] = lib
@@ -183,6 +186,25 @@ class Oracle:
         if st != OK:
             raise OracleError(st)
         return Y
+
+    # attention (R10)
+    def attention(self, Q, K, V, B, T, H, dh, scale=None, rows=None):
+        """Softmax attention (fp64) of bf16 bit-pattern operands Q, K, V, each
+        [B*T][>= H*dh] (row strides from their shapes): returns O [nrows][H*dh]
+        for the listed query rows (b * T + t; all if None)."""
+        Q = np.ascontiguousarray(Q, dtype=np.uint16)
+        K = np.ascontiguousarray(K, dtype=np.uint16)
+        V = np.ascontiguousarray(V, dtype=np.uint16)
+        scale = 1.0 / np.sqrt(dh) if scale is None else scale
+        rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = B * T if rows is None else len(rows_arr)
+        O = np.empty((nrows, H * dh), dtype=np.float64)
+        st = self.lib.oracle_attention_rows(
+            _ptr(Q), Q.shape[1], _ptr(K), K.shape[1], _ptr(V), V.shape[1], B, T, H, dh,
+            float(scale), None if rows_arr is None else _ptr(rows_arr), nrows, _ptr(O))
+        if st != OK:
+            raise OracleError(st)
+        return O
 
     # steering (R9)
     def steer(self, Y, direction, hnorm, alpha):

@@ -35,6 +35,13 @@
  *       feed-forward's GELU, the residual add): Y = act(P + bias[n]) +
  *       residual[m][n] on the fp64 product P, act the identity or the GELU
  *       in its exact form x * Phi(x) = x * (1 + erf(x / sqrt 2)) / 2.
+ *   R10 the self-attention around the linears (the GPU path's attention,
+ *       Methodology; the fused attention the paper names as its open
+ *       lever): per batch b, head h and query t,
+ *       O[b,t,h,:] = sum_j p_j V[b,j,h,:] / sum_j p_j,
+ *       p_j = exp(s_j - max_i s_i), s_j = scale * <Q[b,t,h,:], K[b,j,h,:]>,
+ *       over all T keys of the same batch (no mask: the DiT attends
+ *       bidirectionally); Q, K, V bf16 read from rows with strides.
  *   R9  steering (Methodology, additive injection, Eq. 2): the chosen
  *       block's output h gains alpha * ||h_bar|| * d for every token, d a
  *       unit direction [N], ||h_bar|| the layer's mean residual norm and
@@ -448,6 +455,58 @@ int oracle_steer(double *Y, int64_t nrows, int64_t N, const float *dir, double h
     for (int64_t i = 0; i < nrows; ++i)
         for (int64_t n = 0; n < N; ++n)
             Y[i * N + n] += c * (double)dir[n];
+    return ORC_OK;
+}
+
+/* ---- attention (R10) ----------------------------------------------------- */
+
+/* O (fp64) for the listed query rows r = rows[i] = b * T + t (rows == NULL:
+ * r = i) and every head: O[i][h * dh + c].  Q, K, V: bf16 bit patterns,
+ * row r of Q at Q + r * ldq, head h at column h * dh (likewise K, V). */
+int oracle_attention_rows(const uint16_t *Q, int64_t ldq, const uint16_t *K, int64_t ldk,
+                          const uint16_t *V, int64_t ldv, int64_t B, int64_t T, int64_t H,
+                          int64_t dh, double scale, const int64_t *rows, int64_t nrows, double *O)
+{
+    if (B <= 0 || T <= 0 || H <= 0 || dh <= 0 || nrows < 0)
+        return ORC_ERR_SHAPE;
+    if (!Q || !K || !V || !O)
+        return ORC_ERR_INVALID;
+    for (int64_t i = 0; i < nrows; ++i) {
+        const int64_t r = rows ? rows[i] : i;
+        if (r < 0 || r >= B * T)
+            return ORC_ERR_SHAPE;
+    }
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t i = 0; i < nrows; ++i)
+        for (int64_t h = 0; h < H; ++h) {
+            const int64_t r = rows ? rows[i] : i;
+            const int64_t b = r / T;
+            double smax = -INFINITY;
+            for (int64_t j = 0; j < T; ++j) {
+                double dot = 0.0;
+                for (int64_t c = 0; c < dh; ++c)
+                    dot += oracle_bf16_to_f64(Q[r * ldq + h * dh + c]) *
+                           oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);
+                if (scale * dot > smax)
+                    smax = scale * dot;
+            }
+            double denom = 0.0;
+            double *out = O + i * H * dh + h * dh;
+            for (int64_t c = 0; c < dh; ++c)
+                out[c] = 0.0;
+            for (int64_t j = 0; j < T; ++j) {
+                double dot = 0.0;
+                for (int64_t c = 0; c < dh; ++c)
+                    dot += oracle_bf16_to_f64(Q[r * ldq + h * dh + c]) *
+                           oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);
+                const double p = exp(scale * dot - smax);
+                denom += p;
+                for (int64_t c = 0; c < dh; ++c)
+                    out[c] += p * oracle_bf16_to_f64(V[(b * T + j) * ldv + h * dh + c]);
+            }
+            for (int64_t c = 0; c < dh; ++c)
+                out[c] /= denom;
+        }
     return ORC_OK;
 }
 

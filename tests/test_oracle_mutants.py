@@ -63,6 +63,19 @@ MUTANTS = [
      "            if (residual)\n                v += (double)residual[src * N + n];\n            if (act == ORC_ACT_GELU)\n                v = v * 0.5 * (1.0 + erf(v / sqrt(2.0)));"),
     ("epilogue residual ignores the row list",
      "v += (double)residual[src * N + n];", "v += (double)residual[i * N + n];"),
+    ("attention ignores the scale",
+     "const double p = exp(scale * dot - smax);", "const double p = exp(dot - smax);"),
+    ("attention weights values by the key rows",
+     "out[c] += p * oracle_bf16_to_f64(V[(b * T + j) * ldv + h * dh + c]);",
+     "out[c] += p * oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);"),
+    ("attention keys from the first sequence",
+     "oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);\n                const double p",
+     "oracle_bf16_to_f64(K[j * ldk + h * dh + c]);\n                const double p"),
+    ("attention heads share head 0's queries",
+     "                    dot += oracle_bf16_to_f64(Q[r * ldq + h * dh + c]) *\n                           oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);\n                const double p",
+     "                    dot += oracle_bf16_to_f64(Q[r * ldq + c]) *\n                           oracle_bf16_to_f64(K[(b * T + j) * ldk + h * dh + c]);\n                const double p"),
+    ("attention not normalized",
+     "                out[c] /= denom;", "                out[c] /= (double)T;"),
     ("steering ignores the residual norm",
      "const double c = alpha * hnorm;", "const double c = alpha;"),
     ("steering applied at zero strength",
@@ -109,6 +122,11 @@ def pin_cases():
     cases += [(pins.test_forward_f16_subnormal_and_signed_zero_weights, ())]
     cases += [(pins.test_epilogue_gelu_normal_cdf_values, ())]
     cases += [(pins.test_epilogue_bias_residual_exact_and_order, ())]
+    cases += [(pins.test_attention_zero_queries_average_values, ())]
+    cases += [(pins.test_attention_single_key_returns_its_value, ())]
+    cases += [(pins.test_attention_two_keys_sigmoid, ())]
+    cases += [(pins.test_attention_dominant_key, ())]
+    cases += [(pins.test_attention_key_permutation_and_heads, ())]
     cases += [(pins.test_steer_zero_strength_is_identity, ())]
     cases += [(pins.test_steer_rank_one_shift, ())]
     cases += [(pins.test_act_quant_bruteforce, (x,)) for x in (0, 1)]

@@ -413,6 +413,92 @@ def test_epilogue_bias_residual_exact_and_order(orc):
 
 
 # --------------------------------------------------------------------------
+# attention (softmax over all keys of the same sequence)
+# --------------------------------------------------------------------------
+
+def bf16_exact(rng, shape, scale=1.0):
+    """bf16 bit patterns of N(0, scale^2) draws, and their exact values."""
+    bits = bf16_bits((rng.standard_normal(shape) * scale).astype(np.float32))
+    return bits, bf16_vals(bits)
+
+
+def test_attention_zero_queries_average_values(orc):
+    """Q = 0: every score is 0, the weights are uniform and each output is
+    the mean of its sequence's value rows (numpy's mean)."""
+    rng = np.random.default_rng(91)
+    B, T, H, dh = 2, 9, 3, 8
+    Q = np.zeros((B * T, H * dh), np.uint16)
+    K, _ = bf16_exact(rng, (B * T, H * dh))
+    V, Vv = bf16_exact(rng, (B * T, H * dh))
+    O = orc.attention(Q, K, V, B, T, H, dh)
+    for b in range(B):
+        want = Vv[b * T:(b + 1) * T].mean(axis=0)
+        assert np.allclose(O[b * T:(b + 1) * T], want[None, :], rtol=0, atol=1e-15)
+
+
+def test_attention_single_key_returns_its_value(orc):
+    """T = 1: the only weight is 1 and the output is the value row itself,
+    exactly."""
+    rng = np.random.default_rng(92)
+    Q, _ = bf16_exact(rng, (3, 16))
+    K, _ = bf16_exact(rng, (3, 16))
+    V, Vv = bf16_exact(rng, (3, 16))
+    assert np.array_equal(orc.attention(Q, K, V, 3, 1, 2, 8), Vv)
+
+
+def test_attention_two_keys_sigmoid(orc):
+    """Two keys: the weights are the logistic function of the score
+    difference, w1 = 1 / (1 + e^(s2 - s1))."""
+    rng = np.random.default_rng(93)
+    dh = 16
+    Q, Qv = bf16_exact(rng, (2, dh))
+    K, Kv = bf16_exact(rng, (2, dh))
+    V, Vv = bf16_exact(rng, (2, dh))
+    O = orc.attention(Q, K, V, 1, 2, 1, dh, scale=0.25)
+    for t in range(2):
+        s1, s2 = 0.25 * Qv[t] @ Kv[0], 0.25 * Qv[t] @ Kv[1]
+        w1 = 1.0 / (1.0 + np.exp(s2 - s1))
+        assert np.allclose(O[t], w1 * Vv[0] + (1 - w1) * Vv[1], rtol=1e-14, atol=1e-15)
+
+
+def test_attention_dominant_key(orc):
+    """A key whose score exceeds all others by more than 800 takes all the
+    weight (e^-800 underflows): the output is exactly its value row."""
+    rng = np.random.default_rng(94)
+    T, dh = 6, 8
+    Q = bf16_bits(np.full((T, dh), 4.0, np.float32))
+    Kf = (rng.standard_normal((T, dh)) * 0.1).astype(np.float32)
+    Kf[3] = 64.0
+    K = bf16_bits(Kf)
+    V, Vv = bf16_exact(rng, (T, dh))
+    O = orc.attention(Q, K, V, 1, T, 1, dh, scale=1.0)
+    assert np.array_equal(O, np.repeat(Vv[3:4], T, axis=0))
+
+
+def test_attention_key_permutation_and_heads(orc):
+    """Permuting the keys together with their values leaves the output
+    unchanged (up to summation order), the batches do not mix, heads are
+    independent, and a row subset is the same rows of the full result."""
+    rng = np.random.default_rng(95)
+    B, T, H, dh = 2, 12, 2, 8
+    Q, _ = bf16_exact(rng, (B * T, H * dh))
+    K, _ = bf16_exact(rng, (B * T, H * dh))
+    V, _ = bf16_exact(rng, (B * T, H * dh))
+    O = orc.attention(Q, K, V, B, T, H, dh)
+    perm = np.concatenate([rng.permutation(T), T + rng.permutation(T)])
+    assert np.allclose(orc.attention(Q, K[perm], V[perm], B, T, H, dh), O, rtol=1e-13, atol=1e-14)
+    K2, V2 = K.copy(), V.copy()
+    K2[T:], V2[T:] = bf16_exact(rng, (T, H * dh))[0], bf16_exact(rng, (T, H * dh))[0]
+    assert np.array_equal(orc.attention(Q, K2, V2, B, T, H, dh)[:T], O[:T])
+    K3 = K.copy()
+    K3[:, dh:] = bf16_exact(rng, (B * T, dh))[0]
+    O3 = orc.attention(Q, K3, V, B, T, H, dh)
+    assert np.array_equal(O3[:, :dh], O[:, :dh]) and not np.allclose(O3[:, dh:], O[:, dh:])
+    rows = np.array([23, 0, 11, 12])
+    assert np.array_equal(orc.attention(Q, K, V, B, T, H, dh, rows=rows), O[rows])
+
+
+# --------------------------------------------------------------------------
 # steering: additive injection (Eq. 2)
 # --------------------------------------------------------------------------
 
