@@ -251,6 +251,29 @@ int qlinear_forward_w8a8(const int8_t *qx, const uint16_t *sx, int64_t M, int64_
 int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
                   const float *strength, hipStream_t stream);
 
+/* ---- self-attention ------------------------------------------------------
+ *
+ * The DiT block's self-attention (Methodology: the GPU path's attention; a
+ * FlashAttention-class fused kernel is the open lever the paper names), in
+ * one pass over the keys with a running maximum and sum:
+ *
+ *     O[b,t,h,:] = sum_j p_j V[b,j,h,:] / sum_j p_j,
+ *     p_j = exp(s_j - max_i s_i),  s_j = scale * <Q[b,t,h,:], K[b,j,h,:]>
+ *
+ * over all T keys of sequence b (no mask).  Q, K, V: bf16 bit patterns;
+ * row b * T + t of Q starts at q + (b * T + t) * ldq and head h at column
+ * h * dh (likewise K, V), so the fused [tokens][3 d] output of a QKV linear
+ * is read in place (q = qkv, k = qkv + d, v = qkv + 2 d, ld = 3 d).  O: rows
+ * of ldo elements, fp32 or bf16 (odt).  Head dimension 64 only
+ * (QL_ERR_UNSUPPORTED otherwise); B * H <= 65535.  q, k, v 16-byte aligned
+ * with ld % 8 == 0; o 16-byte (fp32) or 8-byte (bf16) aligned with
+ * ldo % 4 == 0.  The probabilities enter the value product rounded to bf16
+ * (fp32 accumulation).  Asynchronous on `stream`. */
+int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t ldk,
+                      const uint16_t *v, int64_t ldv, int64_t B, int64_t T, int64_t H,
+                      int64_t dh, float scale, void *o, int64_t ldo, int odt,
+                      hipStream_t stream);
+
 /* Static description of a status code. */
 const char *qlinear_status_string(int status);
 

@@ -84,6 +84,19 @@ struct W8Args {
 };
 hipError_t launch_qgemm_w8a8(const W8Args &a, hipStream_t stream);
 
+// Fused self-attention (attention.hip), head dimension 64: Q, K, V bf16
+// rows with strides (elements, multiples of 8), O fp32 or bf16.
+struct AttnArgs {
+    const uint16_t *q, *k, *v;
+    int64_t ldq, ldk, ldv;
+    void *o;
+    int64_t ldo;
+    int B, T, H;
+    float scale_log2e;  // scale * log2(e)
+    int obf16;
+};
+hipError_t launch_attention(const AttnArgs &a, hipStream_t stream);
+
 // The steering injection alone, in place on h [M][N] fp32 (steer.hip).
 hipError_t launch_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
                         const float *strength, hipStream_t stream);

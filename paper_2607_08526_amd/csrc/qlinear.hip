@@ -765,6 +765,40 @@ int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
                                                                              : QL_ERR_HIP;
 }
 
+int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t ldk,
+                      const uint16_t *v, int64_t ldv, int64_t B, int64_t T, int64_t H,
+                      int64_t dh, float scale, void *o, int64_t ldo, int odt, hipStream_t stream)
+{
+    if (odt != QL_DT_F32 && odt != QL_DT_BF16)
+        return QL_ERR_INVALID;
+    if (B <= 0 || T <= 0 || H <= 0 || dh <= 0 || ldq < H * dh || ldk < H * dh ||
+        ldv < H * dh || ldo < H * dh)
+        return QL_ERR_SHAPE;
+    if (dh != 64 || B * T >= I31 || B * H > 65535 || ldq >= I31 || ldk >= I31 ||
+        ldv >= I31 || ldo >= I31)
+        return QL_ERR_UNSUPPORTED;
+    if (!q || !k || !v || !o || !(scale == scale) || scale > 3.0e38f || scale < -3.0e38f)
+        return QL_ERR_INVALID;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || ldq % 8 || ldk % 8 ||
+        ldv % 8 || !aligned(o, odt == QL_DT_BF16 ? 8 : 16) || ldo % 4)
+        return QL_ERR_ALIGN;
+    AttnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.ldq = ldq;
+    a.ldk = ldk;
+    a.ldv = ldv;
+    a.o = o;
+    a.ldo = ldo;
+    a.B = (int)B;
+    a.T = (int)T;
+    a.H = (int)H;
+    a.scale_log2e = (float)((double)scale * 1.4426950408889634);
+    a.obf16 = odt == QL_DT_BF16 ? 1 : 0;
+    return launch_attention(a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
 const char *qlinear_status_string(int status)
 {
     switch (status) {

@@ -31,7 +31,7 @@ EXPORTS = [
     "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
     "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
     "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
-    "qlinear_steer", "qlinear_status_string",
+    "qlinear_steer", "qlinear_attention", "qlinear_status_string",
 ]
 
 
@@ -123,6 +123,9 @@ def load():
     lib.qlinear_forward_w8a8.restype = ci
     lib.qlinear_steer.argtypes = [vp, i64, i64, vp, ctypes.c_float, vp, vp]
     lib.qlinear_steer.restype = ci
+    lib.qlinear_attention.argtypes = [vp, i64, vp, i64, vp, i64, i64, i64, i64, i64,
+                                      ctypes.c_float, vp, i64, ci, vp]
+    lib.qlinear_attention.restype = ci
     lib.qlinear_block_forward.restype = ci
     lib.qlinear_status_string.argtypes = [ci]
     lib.qlinear_status_string.restype = ctypes.c_char_p
@@ -305,6 +308,24 @@ def steer(h, direction, hnorm, strength, stream=None):
     _check(load().qlinear_steer(_ptr(h), M, N, _ptr(direction), float(hnorm), _ptr(strength),
                                 _stream(stream)))
     return h
+
+
+def attention(q, k, v, B, T, H, dh=64, scale=None, O=None, odtype=torch.float32, stream=None):
+    """Softmax self-attention over each sequence's T keys.  q, k, v: bf16 (or
+    int16 bit patterns) 2-D row views [B*T][>= H*dh] with unit column stride
+    (e.g. column slices of a fused QKV output).  Returns O [B*T][H*dh] fp32
+    or bf16.  Asynchronous."""
+    for t in (q, k, v):
+        if t.dim() != 2 or t.stride(1) != 1:
+            raise ValueError("q, k, v must be 2-D row views with unit column stride")
+    if O is None:
+        O = torch.empty((B * T, H * dh), dtype=odtype, device=q.device)
+    odt = DT_BF16 if O.dtype == torch.bfloat16 else DT_F32
+    scale = 1.0 / float(dh) ** 0.5 if scale is None else scale
+    _check(load().qlinear_attention(_ptr(q), q.stride(0), _ptr(k), k.stride(0), _ptr(v),
+                                    v.stride(0), B, T, H, dh, float(scale), _ptr(O),
+                                    O.stride(0), odt, _stream(stream)))
+    return O
 
 
 class QuantizedLinear:

@@ -44,7 +44,7 @@ def test_header_declares_the_boundary():
         "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
         "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
         "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
-        "qlinear_steer", "qlinear_status_string"])
+        "qlinear_steer", "qlinear_attention", "qlinear_status_string"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -231,3 +231,25 @@ def test_steer_argument_errors(lib):
     assert st(d=A1) == ALIGN
     assert st(M=1 << 31) == UNSUPPORTED
     assert st(M=0, h=None) == OK
+
+
+def test_attention_argument_errors(lib):
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.qlinear_attention.argtypes = [vp, i64, vp, i64, vp, i64, i64, i64, i64, i64,
+                                      ctypes.c_float, vp, i64, ci, vp]
+
+    def at(q=A16, ld=128, B=1, T=8, H=2, dh=64, scale=0.125, o=A16, ldo=128, odt=F32):
+        return lib.qlinear_attention(q, ld, A16, ld, A16, ld, B, T, H, dh, scale, o, ldo, odt,
+                                     None)
+    assert at(odt=2) == INVALID
+    assert at(T=0) == SHAPE
+    assert at(ld=64) == SHAPE
+    assert at(ldo=100) == SHAPE
+    assert at(dh=32, ld=64, ldo=64) == UNSUPPORTED
+    assert at(B=40000, H=2) == UNSUPPORTED
+    assert at(q=None) == INVALID
+    assert at(scale=float("nan")) == INVALID
+    assert at(q=A2) == ALIGN
+    assert at(ld=132) == ALIGN
+    assert at(o=0x10008, odt=F32) == ALIGN
+    assert at(ldo=130) == ALIGN
