@@ -295,6 +295,85 @@ def epilogue_step(torch, ql, step, steps, warmup):
     }
 
 
+def attention_bench(torch, ql, si, step):
+    """The fused attention at the DiT shape (2 sequences x 1024 tokens, 32
+    heads of 64), read in place from a fused QKV tensor; graph-timed."""
+    import numpy as np
+    B, T, d = 2, step.M // 2, si.D_MODEL
+    H = d // 64
+    rng = np.random.default_rng(17)
+    qkv = torch.from_numpy(si.f32_to_bf16_bits(rng.standard_normal((B * T, 3 * d)).astype(
+        np.float32)).view(np.int16)).cuda()
+    O = torch.empty((B * T, d), dtype=torch.bfloat16, device="cuda")
+    fn = lambda: ql.attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], B, T, H, O=O)
+    med = graph_time(torch, fn)[0]
+    flops = 4.0 * B * H * T * T * 64
+    tf = flops / (med * 1e-3) / 1e12
+    return {"shape": f"B={B} T={T} H={H} dh=64, bf16 out", "us": round(med * 1e3, 2),
+            "TFLOPs": round(tf, 1), "mfma_frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4)}
+
+
+def dit_step(torch, ql, si, step):
+    """A sequential DiT denoising step in one HIP graph: per block, QKV
+    linear (+ bias -> bf16), attention (-> bf16), out projection added in
+    place into the fp32 residual stream, FFN-up (+ bias -> GELU -> bf16)
+    feeding FFN-down, added in place, with the steering injection at one
+    block (strength re-read at every replay).  The normalization before the
+    attention and the feed-forward is not built: FFN-up reads a fixed bf16
+    activation tensor in its place.  Same q4 weights as the step."""
+    import numpy as np
+    dev = torch.device("cuda")
+    M, d = step.M, si.D_MODEL
+    B, T, H = 2, M // 2, d // 64
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    lin = [(e[4], e[1].shape[1]) for e in step.blocks[0]]  # (N, K)
+    qkv = torch.empty((M, 3 * d), dtype=torch.bfloat16, device=dev)
+    att = torch.empty((M, d), dtype=torch.bfloat16, device=dev)
+    up = torch.empty((M, 4 * d), dtype=torch.bfloat16, device=dev)
+    h = torch.zeros((M, d), dtype=torch.float32, device=dev)
+    direction = torch.randn(d, device=dev, generator=g)
+    direction /= direction.norm()
+    strength = torch.zeros(1, dtype=torch.float32, device=dev)
+    steer_block = len(step.blocks) // 2
+    calls = []
+    for blk, ents in enumerate(step.blocks):
+        bias = [torch.randn(N, device=dev, generator=g) * 0.1 for N, _ in lin]
+        (f0, _, c0, s0, N0, _), (f1, _, c1, s1, N1, _), (f2, _, c2, s2, N2, _), \
+            (f3, _, c3, s3, N3, _) = ents
+        st = (direction, 30.0, strength) if blk == steer_block else None
+        calls.append((
+            ql.make_group_ep([(f0, step.xa, c0, s0, N0, qkv, bias[0], ql.ACT_NONE, None)]),
+            ql.make_group_ep([(f1, att.view(torch.int16), c1, s1, N1, h, bias[1], ql.ACT_NONE, h)]),
+            ql.make_group_ep([(f2, step.xa, c2, s2, N2, up, bias[2], ql.ACT_GELU, None)]),
+            ql.make_group_ep([(f3, up.view(torch.int16), c3, s3, N3, h, bias[3], ql.ACT_NONE, h,
+                               st)]),
+            bias))
+    qv = qkv.view(torch.int16)
+
+    def run():
+        for g0, g1, g2, g3, _ in calls:
+            ql.block_forward_ep(None, group=g0)
+            ql.attention(qv[:, :d], qv[:, d:2 * d], qv[:, 2 * d:], B, T, H, O=att)
+            ql.block_forward_ep(None, group=g1)
+            ql.block_forward_ep(None, group=g2)
+            ql.block_forward_ep(None, group=g3)
+
+    t0 = graph_time(torch, run, reps=10, warm=3)[0]
+    strength.fill_(0.15)
+    t1 = graph_time(torch, run, reps=10, warm=3)[0]
+    strength.zero_()
+    lin_flops = step.flops
+    att_flops = 4.0 * B * H * T * T * 64 * len(step.blocks)
+    return {"note": "24 sequential DiT blocks (QKV+bias->bf16, attention, out-proj+bias into the "
+                    "fp32 residual, FFN-up+bias->GELU->bf16, FFN-down+bias into the residual, "
+                    "steering at one block) captured as one HIP graph; the normalizations "
+                    "are not built (FFN-up reads a fixed bf16 tensor)",
+            "ms_per_step": round(t0, 4), "ms_per_step_steering_on": round(t1, 4),
+            "TFLOPs": round((lin_flops + att_flops) / (t0 * 1e-3) / 1e12, 1),
+            "attention_flop_share": round(att_flops / (lin_flops + att_flops), 4)}
+
+
 def time_step(torch, step, steps, warmup):
     for _ in range(warmup):
         step.run()
@@ -689,6 +768,8 @@ def main():
         "q4_step_speedup": round(f16_ms / ms_per_step, 3),
     }
     res["epilogue"] = epilogue_step(torch, ql, step, args.steps, args.warmup)
+    res["attention"] = attention_bench(torch, ql, si, step)
+    res["dit_step"] = dit_step(torch, ql, si, step)
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)
