@@ -260,7 +260,8 @@ int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
  *     O[b,t,h,:] = sum_j p_j V[b,j,h,:] / sum_j p_j,
  *     p_j = exp(s_j - max_i s_i),  s_j = scale * <Q[b,t,h,:], K[b,j,h,:]>
  *
- * over all T keys of sequence b (no mask).  Q, K, V: bf16 bit patterns;
+ * over all T keys of sequence b (no mask), scale >= 0 and finite
+ * (QL_ERR_INVALID otherwise).  Q, K, V: bf16 bit patterns;
  * row b * T + t of Q starts at q + (b * T + t) * ldq and head h at column
  * h * dh (likewise K, V), so the fused [tokens][3 d] output of a QKV linear
  * is read in place (q = qkv, k = qkv + d, v = qkv + 2 d, ld = 3 d).  O: rows

@@ -26,7 +26,6 @@
 // Per workgroup: 128 queries (4 wavefronts x 32) of one (b, h); keys in
 // tiles of 64, double-buffered in LDS (K row-major, V transposed) through
 // registers.
-#include "epilogue.h"
 #include "internal.h"
 
 namespace qlk {
@@ -46,10 +45,13 @@ constexpr int KROW = DH + PAD;     // Ks row: one key
 constexpr int VROW = BKEY + PAD;   // Vt row: one value channel
 constexpr int STAGE = (BKEY * KROW + DH * VROW) * 2;  // bytes
 
-__device__ inline uint32_t bf16_rne(float x)
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// two fp32 values rounded to nearest even bf16, packed (v_cvt_pk_bf16_f32)
+__device__ inline uint32_t pack_bf16(float lo, float hi)
 {
-    const uint32_t u = __float_as_uint(x);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;  // finite, non-negative inputs
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
@@ -140,40 +142,45 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
             }
             sc[sub] = acc;
         }
-        // scale (to base 2), mask keys beyond T, running maximum
-        float mt = -INFINITY;
+        // running maximum of the raw scores (keys beyond T excluded; the
+        // scale c = scale * log2 e >= 0 is applied inside the exponent:
+        // p = 2^(s c - m c))
         const bool tail = (kt + 1) * BKEY > T;
+        auto valid = [&](int sub, int r) {
+            return kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3) < T;
+        };
+        float mt = -INFINITY;
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float x = sc[sub][r] * a.scale_log2e;
-                if (tail) {
-                    const int key = kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3);
-                    x = key < T ? x : -INFINITY;
-                }
-                sc[sub][r] = x;
-                mt = fmaxf(mt, x);
-            }
+            for (int r = 0; r < 16; ++r)
+                mt = fmaxf(mt, !tail || valid(sub, r) ? sc[sub][r] : -INFINITY);
         mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const float c = a.scale_log2e;
         const float mnew = fmaxf(mrun, mt);
-        const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);  // 0 on the first tile
+        const float alpha = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mrun - mnew) * c);
         mrun = mnew;
+        const float mc = mnew * c;
         float ls = 0.0f;
         u32x4 pb[2][2];  // P^T operands: [sub][chunk c], 8 bf16 each
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
+            for (int ch = 0; ch < 2; ++ch) {
                 uint32_t w[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = __builtin_amdgcn_exp2f(sc[sub][8 * c + 2 * e] - mnew);
-                    const float p1 = __builtin_amdgcn_exp2f(sc[sub][8 * c + 2 * e + 1] - mnew);
+                    const int r0 = 8 * ch + 2 * e;
+                    float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][r0], c, -mc));
+                    float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][r0 + 1], c, -mc));
+                    if (tail) {
+                        p0 = valid(sub, r0) ? p0 : 0.0f;
+                        p1 = valid(sub, r0 + 1) ? p1 : 0.0f;
+                    }
                     ls += p0 + p1;
-                    w[e] = bf16_rne(p0) | (bf16_rne(p1) << 16);
+                    w[e] = pack_bf16(p0, p1);
                 }
-                pb[sub][c] = u32x4{w[0], w[1], w[2], w[3]};
+                pb[sub][ch] = u32x4{w[0], w[1], w[2], w[3]};
             }
         lrun = lrun * alpha + ls;
 #pragma unroll
@@ -212,9 +219,7 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
                                oacc[t][4 * g + 2] * inv, oacc[t][4 * g + 3] * inv};
             if (a.obf16) {
                 uint16_t *o = static_cast<uint16_t *>(a.o) + orow + ch;
-                const uint32_t w0 = epi_bf16(v[0]) | (epi_bf16(v[1]) << 16);
-                const uint32_t w1 = epi_bf16(v[2]) | (epi_bf16(v[3]) << 16);
-                *reinterpret_cast<u32x2 *>(o) = u32x2{w0, w1};
+                *reinterpret_cast<u32x2 *>(o) = u32x2{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
             } else {
                 *reinterpret_cast<f32x4_t *>(static_cast<float *>(a.o) + orow + ch) = v;
             }

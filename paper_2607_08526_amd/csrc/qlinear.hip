@@ -777,7 +777,7 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
     if (dh != 64 || B * T >= I31 || B * H > 65535 || ldq >= I31 || ldk >= I31 ||
         ldv >= I31 || ldo >= I31)
         return QL_ERR_UNSUPPORTED;
-    if (!q || !k || !v || !o || !(scale == scale) || scale > 3.0e38f || scale < -3.0e38f)
+    if (!q || !k || !v || !o || !(scale >= 0.0f) || scale > 3.0e38f)
         return QL_ERR_INVALID;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || ldq % 8 || ldk % 8 ||
         ldv % 8 || !aligned(o, odt == QL_DT_BF16 ? 8 : 16) || ldo % 4)

@@ -249,6 +249,7 @@ def test_attention_argument_errors(lib):
     assert at(B=40000, H=2) == UNSUPPORTED
     assert at(q=None) == INVALID
     assert at(scale=float("nan")) == INVALID
+    assert at(scale=-0.5) == INVALID
     assert at(q=A2) == ALIGN
     assert at(ld=132) == ALIGN
     assert at(o=0x10008, odt=F32) == ALIGN
