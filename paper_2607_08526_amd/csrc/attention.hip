@@ -75,10 +75,14 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
         qb[s] = __builtin_bit_cast(bf16x8, v);
     }
 
-    // staging: thread t moves rows 2 (t / 8) and 2 (t / 8) + 1 of the tile,
-    // elements 8 (t % 8) .. + 7 of K and of V (V written transposed, the two
-    // keys of a row pair packed into one 32-bit word)
+    // staging: thread t moves rows 2 (t / 8) and 2 (t / 8) + 1 of the K tile,
+    // elements 8 (t % 8) .. + 7, and rows 2 (t % 32), 2 (t % 32) + 1 of the V
+    // tile, elements 8 (t / 32) .. + 7.  V is written transposed, the two
+    // keys of a row pair packed into one 32-bit word; with 32 row pairs per
+    // wavefront those writes spread over the LDS banks (8 row pairs per
+    // wavefront put every write of an instruction into 8 banks)
     const int pr = tid >> 3, c8 = 8 * (tid & 7);
+    const int vpr = tid & 31, vc8 = 8 * (tid >> 5);
     u32x4 pk[2], pv[2];
     auto fetch = [&](int kt) {
 #pragma unroll
@@ -87,8 +91,10 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
             u32x4 zk = {0u, 0u, 0u, 0u}, zv = zk;
             if (key < T) {
                 zk = *reinterpret_cast<const u32x4 *>(a.k + (seq + key) * a.ldk + h * DH + c8);
-                zv = *reinterpret_cast<const u32x4 *>(a.v + (seq + key) * a.ldv + h * DH + c8);
             }
+            const int vkey = kt * BKEY + 2 * vpr + i;
+            if (vkey < T)
+                zv = *reinterpret_cast<const u32x4 *>(a.v + (seq + vkey) * a.ldv + h * DH + vc8);
             pk[i] = zk;
             pv[i] = zv;
         }
@@ -103,7 +109,7 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
         for (int e = 0; e < 8; ++e) {
             const uint32_t lo = (pv[0][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
             const uint32_t hi = (pv[1][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            *reinterpret_cast<uint32_t *>(vt + (c8 + e) * VROW + 2 * pr) = lo | (hi << 16);
+            *reinterpret_cast<uint32_t *>(vt + (vc8 + e) * VROW + 2 * vpr) = lo | (hi << 16);
         }
     };
 
