@@ -218,9 +218,12 @@ def _epilogue(Y, bias, act, residual, steer=None):
 def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
                ydtype=torch.float32, steer=None, stream=None):
     """forward() with the layer epilogue fused into the output store:
-    Y = act(X . W^T + bias) + residual, Y fp32 or bf16 (ydtype, or Y's dtype
-    when Y is given).  bias fp32 [N], residual fp32 [M][N] (may be Y itself
-    for fp32 Y), each optional.  Asynchronous."""
+    Y = act(X . W^T + bias) + residual (+ alpha * hnorm * d), Y fp32 or bf16
+    (ydtype, or Y's dtype when Y is given).  bias fp32 [N], residual fp32
+    [M][N] (may be Y itself for fp32 Y), each optional; steer = (d fp32 [N],
+    hnorm, strength) adds the steering term with alpha = strength[0] read on
+    the device by the launch (skipped exactly when alpha is 0).
+    Asynchronous."""
     M, K = X.shape
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=X.device)
@@ -290,7 +293,8 @@ def quantize_act(X, qx=None, sx=None, stream=None):
 def forward_w8a8(qx, sx, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
                  ydtype=torch.float32, steer=None, stream=None):
     """W8A8 product of per-token int8 activations (quantize_act) and int8
-    weights (quantize(FMT_INT8, ...)), with the layer epilogue.  Asynchronous."""
+    weights (quantize(FMT_INT8, ...)), with the layer epilogue (arguments as
+    forward_ep).  Asynchronous."""
     M, K = qx.shape
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=qx.device)
