@@ -104,24 +104,31 @@ def test_steer_in_epilogue(gpu, orc, fmt, xdt, M, N, K):
     bd, rd, dd = dev_f32(torch, bias), dev_f32(torch, resid), dev_f32(torch, d)
     strength = torch.zeros(1, dtype=torch.float32, device="cuda")
     P = orc.forward(fmt, X, xdt, cr, sr, N)
-    # with bias and residual, and steering alone (the per-column term
-    # without any other)
-    for b_, r_ in ((True, True), (False, False)):
-        kw = dict(bias=bd if b_ else None, residual=rd if r_ else None)
+    # with bias and residual, steering alone (the per-column term without
+    # any other), and steering with GELU into bf16 outputs
+    for b_, r_, act, ydt in ((True, True, O.ACT_NONE, torch.float32),
+                             (False, False, O.ACT_NONE, torch.float32),
+                             (True, False, O.ACT_GELU, torch.bfloat16)):
+        kw = dict(bias=bd if b_ else None, residual=rd if r_ else None, act=act, ydtype=ydt)
         plain = ql.forward_ep(fmt, Xd, cd, sd, N, **kw)
-        base = orc.epilogue(P, bias if b_ else None, O.ACT_NONE, resid if r_ else None)
+        base = orc.epilogue(P, bias if b_ else None, act, resid if r_ else None)
         for alpha in (0.0, 0.25):
             strength.fill_(alpha)
             Y = ql.forward_ep(fmt, Xd, cd, sd, N, steer=(dd, hnorm, strength), **kw)
             torch.cuda.synchronize()
-            Yg = Y.cpu().numpy()
             if alpha == 0.0:
-                assert np.array_equal(Yg.view(np.uint32), plain.cpu().numpy().view(np.uint32))
+                assert torch.equal(Y.view(torch.int16) if ydt == torch.bfloat16 else Y.view(
+                    torch.int32), plain.view(torch.int16) if ydt == torch.bfloat16 else
+                    plain.view(torch.int32))
                 continue
+            Yg = Y.float().cpu().numpy()
             Yr = orc.steer(base, d, hnorm, alpha)
-            lim = TOL[xdt] * np.max(np.abs(P)) + 1e-6 * (np.abs(Yr) + np.max(np.abs(P))) \
+            lim = 1.13 * TOL[xdt] * np.max(np.abs(P)) \
+                + 1e-6 * (np.abs(Yr) + np.max(np.abs(P)) + np.max(np.abs(bias))) \
                 + steer_bound(d, hnorm, alpha, Yr)
-            assert np.all(np.abs(Yg - Yr) <= lim), (M, N, K, b_)
+            if ydt == torch.bfloat16:
+                lim = lim + 2.0 ** -8 * np.abs(Yr)
+            assert np.all(np.abs(Yg - Yr) <= lim), (M, N, K, b_, act)
 
 
 def test_steer_w8a8(gpu, orc):
