@@ -74,7 +74,7 @@ __device__ inline void epi_store(const Epilogue &e, float *Y, int64_t idx, int n
 // Whether four consecutive elements of a row (n % 4 == 0, n + 3 < N) can be
 // handled as one group: one 16-byte (fp32) or 8-byte (bf16) store, and
 // 16-byte loads of the bias and residual.
-__device__ inline bool epi_vec_ok(const Epilogue &e, const float *Y, int64_t N)
+__host__ __device__ inline bool epi_vec_ok(const Epilogue &e, const float *Y, int64_t N)
 {
     return (N & 3) == 0 && ((uintptr_t)Y & (e.ybf16 ? 7 : 15)) == 0 &&
            ((uintptr_t)e.bias & 15) == 0 && ((uintptr_t)e.resid & 15) == 0 &&

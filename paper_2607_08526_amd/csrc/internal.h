@@ -50,6 +50,12 @@ struct LinDesc {
     int ksplit, psteps;
     float *part;
     int *cnt;
+    // part_out: plain partial outputs part[ksplit][M][N] (cnt == nullptr)
+    // even when ksplit == 1, for a layer whose epilogue cannot take groups
+    // of four outputs (N % 4 != 0 or an unaligned operand): the epilogue is
+    // then applied by launch_split_sum, so the large-M kernel needs no
+    // element-by-element epilogue code
+    int part_out;
 };
 
 struct GroupArgs {

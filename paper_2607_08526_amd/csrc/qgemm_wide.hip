@@ -563,12 +563,11 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     float *const patch = reinterpret_cast<float *>(ring + 1024) + c.wave * 1024;
     // destination: Y, or this part's plain partial output when the parts
     // are summed by a separate launch (split_sum_kernel)
-    const bool to_part = S > 1 && !d.cnt;
+    const bool to_part = (S > 1 && !d.cnt) || d.part_out;
     float *const Yd = to_part ? d.part + (int64_t)part * M * N : d.Y;
     const bool vec = (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0;
     // a layer epilogue beyond the plain fp32 store (final outputs only)
     const bool epi = EPI && !to_part && epi_active(d.ep);
-    const bool vec_epi = epi_vec_ok(d.ep, d.Y, N);
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
         const int lane = tid & 63;
         const int cq = lane & 7;          // 4-column group of the row
@@ -607,30 +606,10 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         }
         // with the epilogue: the bias and the four rows' residual loads go
         // out first (before the patch round trip, which hides part of their
-        // latency); whether the layer takes groups of four is uniform, so
-        // the common path is straight-line code with predicated stores
+        // latency).  The layer takes groups of four (the host routes any
+        // other layer with an epilogue through plain partials and the sum
+        // launch), so this is straight-line code with predicated stores.
         const int mb = m0 + i * 32 + (lane >> 3);  // row of iteration 0
-        if (!vec_epi) {
-            // element by element (N % 4 != 0 or unaligned operands; a row
-            // per iteration keeps this rare path's code small)
-#pragma unroll
-            for (int h = 0; h < 4; ++h)
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
-#pragma unroll 1
-            for (int t = 0; t < 4; ++t) {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 +
-                                                                 4 * cq);
-                const int m = mb + 8 * t;
-                if (m < M)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (n + e < N)
-                            epi_store(d.ep, d.Y, (int64_t)m * N + n + e, n + e, v[e]);
-            }
-            return;
-        }
         // groups of four (N % 4 == 0: a lane's group is whole or beyond N)
         const bool col_ok = n < N;
         f32x4 b4 = {0.f, 0.f, 0.f, 0.f}, r[4] = {b4, b4, b4, b4};

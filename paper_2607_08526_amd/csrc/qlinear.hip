@@ -7,6 +7,7 @@
 #include <queue>
 #include <vector>
 
+#include "epilogue.h"
 #include "internal.h"
 
 using namespace qlk;
@@ -519,22 +520,31 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
             bytes += round256((size_t)a.d[i].M * a.d[i].K * 2) + round256((size_t)a.d[i].M * 4);
         }
     }
+    // layers whose epilogue cannot take groups of four outputs write plain
+    // fp32 partials, and the sum launch applies their epilogue
+    bool any_part_out = false;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        d.part_out = epi_active(d.ep) && !epi_vec_ok(d.ep, d.Y, d.N) ? 1 : 0;
+        any_part_out = any_part_out || d.part_out;
+    }
     // split layers: fp32 partials (tiles [tiles][S][BM * BN], or plain
     // outputs [S][M][N] for a plan summed by a separate launch), then the
     // arrival counters of the in-kernel reductions
     size_t poff[QL_MAX_GROUP], coff[QL_MAX_GROUP];
     int ncnt = 0;
     for (int i = 0; i < n; ++i) {
-        if (a.d[i].ksplit == 1)
+        const LinDesc &d = a.d[i];
+        if (d.ksplit == 1 && !d.part_out)
             continue;
         poff[i] = bytes;
-        bytes += round256(pl.ext ? (size_t)a.d[i].ksplit * a.d[i].M * a.d[i].N * 4
-                                 : (size_t)a.d[i].tiles_m * a.d[i].tiles_n * a.d[i].ksplit *
-                                       bm * bn * 4);
+        bytes += round256(pl.ext || d.part_out
+                              ? (size_t)d.ksplit * d.M * d.N * 4
+                              : (size_t)d.tiles_m * d.tiles_n * d.ksplit * bm * bn * 4);
     }
     const size_t cnt_off = bytes;
     for (int i = 0; i < n; ++i) {
-        if (a.d[i].ksplit == 1 || pl.ext)
+        if (a.d[i].ksplit == 1 || pl.ext || a.d[i].part_out)
             continue;
         coff[i] = cnt_off + (size_t)ncnt * 4;
         ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
@@ -545,9 +555,9 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
         return QL_ERR_HIP;
     uint8_t *const wsb = ws.ptr;
     for (int i = 0; i < n; ++i)
-        if (a.d[i].ksplit > 1) {
+        if (a.d[i].ksplit > 1 || a.d[i].part_out) {
             a.d[i].part = (float *)(wsb + poff[i]);
-            a.d[i].cnt = pl.ext ? nullptr : (int *)(wsb + coff[i]);
+            a.d[i].cnt = pl.ext || a.d[i].part_out ? nullptr : (int *)(wsb + coff[i]);
         }
     // one pre-pass launch over every distinct activation tensor; it also
     // clears the split counters
@@ -575,11 +585,11 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
     }
     if (e == hipSuccess)
         e = launch_qgemm_wide(ord[0]->lin.fmt, a, stream);
-    if (pl.ext && e == hipSuccess) {
+    if ((pl.ext || any_part_out) && e == hipSuccess) {
         SplitSum sums[QL_MAX_GROUP];
         int ns = 0;
         for (int i = 0; i < n; ++i)
-            if (a.d[i].ksplit > 1)
+            if ((pl.ext && a.d[i].ksplit > 1) || a.d[i].part_out)
                 sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
                                       a.d[i].ep};
         e = launch_split_sum(sums, ns, stream);
