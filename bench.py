@@ -696,7 +696,8 @@ def main():
         print(json.dumps(summarize_traffic(*args.summarize_traffic), indent=1))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "single-GPU benchmark: --gpus must be 1 (the multi-GPU "
+                                   "sharding is a design, not implemented)"}))
         sys.exit(2)
     import torch
 
