@@ -42,7 +42,9 @@ constexpr int BQ = 128, BKEY = 64;  // queries per workgroup, keys per tile
 constexpr int THREADS = 256;
 constexpr int PAD = 8;             // bf16 elements of padding per LDS row
 constexpr int KROW = DH + PAD;     // Ks row: one key
-constexpr int VROW = BKEY + PAD;   // Vt row: one value channel
+// Vt row: one value channel, 34 words (= 2 mod 32 banks), so that the 16
+// rows of one phase of 8-byte operand reads land on distinct banks
+constexpr int VROW = BKEY + 4;
 constexpr int STAGE = (BKEY * KROW + DH * VROW) * 2;  // bytes
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
