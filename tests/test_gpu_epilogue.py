@@ -219,3 +219,41 @@ def test_block_forward_ep_grouped(gpu, orc):
             torch.cuda.synchronize()
             for e, (Pr, Yr, bias, yb) in zip(entries, refs):
                 check(host_y(torch, e[5]), Pr, Yr, bias, O.DT_BF16, yb, (M, fmt, e[4]))
+
+
+def test_block_forward_ep_routed_layers(gpu, orc):
+    """A grouped call on the large-M path mixing layers whose epilogue takes
+    groups of four outputs with layers that the host routes through plain
+    partials and the sum launch: an odd N, and a bias that is 4-byte but not
+    16-byte aligned; long reductions cut into parts in the same launch."""
+    torch, ql = gpu
+    M = 384
+    _, xa = si.small_case(3400, M, 1, 512)
+    _, xb = si.small_case(3401, M, 1, 4096)
+    rng = np.random.default_rng(3402)
+    shapes = [(702, 512), (256, 4096), (1000, 512), (257, 4096)]
+    entries, refs = [], []
+    for fmt in (O.FMT_Q4, O.FMT_INT8):
+        entries.clear()
+        refs.clear()
+        for i, (N, K) in enumerate(shapes):
+            W, _ = si.small_case(3410 + i, 1, N, K)
+            cd, sd = ql.quantize(fmt, dev_f32(torch, W))
+            cr, sr = orc.quantize(fmt, W)
+            X = xb if K == 4096 else xa
+            bias = (rng.standard_normal(N) * 0.5).astype(np.float32)
+            if i == 2:  # a bias view one float past a 16-byte boundary
+                store = dev_f32(torch, np.concatenate([[0.0], bias]).astype(np.float32))
+                bd = store[1:]
+            else:
+                bd = dev_f32(torch, bias)
+            act = O.ACT_GELU if i % 2 else O.ACT_NONE
+            resid = rng.standard_normal((M, N)).astype(np.float32)
+            Y = dev_f32(torch, resid)  # in-place residual add
+            entries.append((fmt, dev_x(torch, X, O.DT_BF16), cd, sd, N, Y, bd, act, Y))
+            P = orc.forward(fmt, X, O.DT_BF16, cr, sr, N)
+            refs.append((P, orc.epilogue(P, bias, act, resid), bias))
+        ql.block_forward_ep(entries)
+        torch.cuda.synchronize()
+        for e, (P, Yr, bias) in zip(entries, refs):
+            check(host_y(torch, e[5]), P, Yr, bias, O.DT_BF16, False, (fmt, e[4]))
