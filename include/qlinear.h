@@ -56,7 +56,8 @@
  *   - All argument checks happen before anything is enqueued; a call that
  *     returns an error has enqueued nothing.
  *   - Alignment: codes and X must be 16-byte aligned, scales 2-byte and Y
- *     4-byte aligned (QL_ERR_ALIGN otherwise).
+ *     4-byte aligned (2-byte for bf16 Y); the entry points after
+ *     qlinear_block_forward state their own rules (QL_ERR_ALIGN otherwise).
  *   - Work runs on the caller's HIP stream; only qlinear_quantize waits for
  *     its own work.  Buffers must stay alive until the stream has passed the
  *     enqueued work.  Asynchronous device faults surface at the caller's next
