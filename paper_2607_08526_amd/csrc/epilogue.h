@@ -144,6 +144,40 @@ __device__ inline void epi_put4(const Epilogue &e, float *Y, int64_t idx, V4 v, 
     }
 }
 
+// the store of epi_put4 split in two: the value as stored (fp32, or bf16
+// packed in the low 8 bytes), then the store itself
+template <typename V4>
+__device__ inline V4 epi_pack4(const Epilogue &e, V4 v)
+{
+    if (e.ybf16) {
+        V4 w = v;
+        w[0] = __uint_as_float(epi_bf16(v[0]) | (epi_bf16(v[1]) << 16));
+        w[1] = __uint_as_float(epi_bf16(v[2]) | (epi_bf16(v[3]) << 16));
+        return w;
+    }
+    return v;
+}
+
+template <typename V4>
+__device__ inline void epi_store_packed4(const Epilogue &e, float *Y, int64_t idx, V4 w, bool nt)
+{
+    if (e.ybf16) {
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 b = {__float_as_uint(w[0]), __float_as_uint(w[1])};
+        u32x2 *dst = reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(Y) + idx);
+        if (nt)
+            __builtin_nontemporal_store(b, dst);
+        else
+            *dst = b;
+    } else {
+        V4 *dst = reinterpret_cast<V4 *>(Y + idx);
+        if (nt)
+            __builtin_nontemporal_store(w, dst);
+        else
+            *dst = w;
+    }
+}
+
 // elements idx .. idx + 3 (columns n .. n + 3) of a group that epi_vec_ok
 // allows, loads included
 template <typename V4>

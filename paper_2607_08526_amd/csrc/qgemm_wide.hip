@@ -568,6 +568,27 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     const bool vec = (N & 3) == 0 && ((uintptr_t)Yd & 15) == 0;
     // a layer epilogue beyond the plain fp32 store (final outputs only)
     const bool epi = EPI && !to_part && epi_active(d.ep);
+    // the per-column epilogue operands (bias, steering term) of this lane's
+    // column groups, loaded once before the first store: a load issued after
+    // stores waits for them too (the vector memory counter retires in order)
+    f32x4 bcol[NSUB], scol[NSUB];
+    float alpha = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j) {
+        bcol[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        scol[j] = bcol[j];
+    }
+    if (epi) {
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j) {
+            const int n = n0 + c.wave * WN + j * 32 + 4 * (tid & 7);
+            if (n < N) {
+                if (d.ep.bias)
+                    bcol[j] = *reinterpret_cast<const f32x4 *>(d.ep.bias + n);
+                scol[j] = epi_steer4<f32x4>(d.ep, n, alpha);
+            }
+        }
+    }
     auto store_tile = [&](int i, int j, const f32x4 (&y)[4]) {
         const int lane = tid & 63;
         const int cq = lane & 7;          // 4-column group of the row
@@ -604,19 +625,15 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
             }
             return;
         }
-        // with the epilogue: the bias and the four rows' residual loads go
-        // out first (before the patch round trip, which hides part of their
-        // latency).  The layer takes groups of four (the host routes any
+        // with the epilogue: the four rows' residual loads go out first
+        // (before the patch round trip, which hides part of their latency).  The layer takes groups of four (the host routes any
         // other layer with an epilogue through plain partials and the sum
         // launch), so this is straight-line code with predicated stores.
         const int mb = m0 + i * 32 + (lane >> 3);  // row of iteration 0
         // groups of four (N % 4 == 0: a lane's group is whole or beyond N)
         const bool col_ok = n < N;
-        f32x4 b4 = {0.f, 0.f, 0.f, 0.f}, r[4] = {b4, b4, b4, b4};
-        if (d.ep.bias && col_ok)
-            b4 = *reinterpret_cast<const f32x4 *>(d.ep.bias + n);
-        float alpha = 0.0f;
-        const f32x4 s4 = col_ok ? epi_steer4<f32x4>(d.ep, n, alpha) : b4;
+        const f32x4 b4 = bcol[j], s4 = scol[j];
+        f32x4 r[4] = {b4, b4, b4, b4};
         if (d.ep.resid) {
 #pragma unroll
             for (int t = 0; t < 4; ++t)
@@ -629,15 +646,21 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 patch[(8 * h + 4 * c.g + e) * 32 + c.l32] = y[h][e];
+        // all four rows read, finished and packed before the first store: a
+        // store's data registers cannot be overwritten until the store has
+        // read them, so reusing them for the next row's patch read would
+        // wait out each store's whole latency
+        f32x4 w[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 +
-                                                             4 * cq);
-            const int m = mb + 8 * t;
-            if (col_ok && m < M)
-                epi_put4(d.ep, d.Y, (int64_t)m * N + n, epi_apply4(d.ep, v, b4, r[t], s4, alpha),
-                         true);
-        }
+        for (int t = 0; t < 4; ++t)
+            w[t] = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 + 4 * cq);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            w[t] = epi_pack4(d.ep, epi_apply4(d.ep, w[t], b4, r[t], s4, alpha));
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (col_ok && mb + 8 * t < M)
+                epi_store_packed4(d.ep, d.Y, (int64_t)(mb + 8 * t) * N + n, w[t], true);
     };
 
     if (S > 1 && d.cnt) {
