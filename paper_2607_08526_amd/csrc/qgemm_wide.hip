@@ -626,9 +626,12 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
             return;
         }
         // with the epilogue: the four rows' residual loads go out first
-        // (before the patch round trip, which hides part of their latency).  The layer takes groups of four (the host routes any
-        // other layer with an epilogue through plain partials and the sum
-        // launch), so this is straight-line code with predicated stores.
+        // (before the patch round trip, which hides part of their latency),
+        // without allocating in the caches (each row is read once; the
+        // activation and code lines that other tiles re-read stay).  The
+        // layer takes groups of four (the host routes any other layer with an
+        // epilogue through plain partials and the sum launch), so this is
+        // straight-line code with predicated stores.
         const int mb = m0 + i * 32 + (lane >> 3);  // row of iteration 0
         // groups of four (N % 4 == 0: a lane's group is whole or beyond N)
         const bool col_ok = n < N;
@@ -638,8 +641,8 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
 #pragma unroll
             for (int t = 0; t < 4; ++t)
                 if (col_ok && mb + 8 * t < M)
-                    r[t] = *reinterpret_cast<const f32x4 *>(d.ep.resid +
-                                                            (int64_t)(mb + 8 * t) * N + n);
+                    r[t] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(
+                        d.ep.resid + (int64_t)(mb + 8 * t) * N + n));
         }
 #pragma unroll
         for (int h = 0; h < 4; ++h)
