@@ -24,13 +24,18 @@
  * Y [M][N], all row-major.
  *
  * Accuracy of the forward product against the exact sum above: fp32
- * activations and bf16 activations at M <= 64 (or when K % 64 != 0) are
+ * activations and bf16 activations at M <= 64 (or when K % 256 != 0) are
  * contracted with the exact codes and fp32 block partials (error a few fp32
  * roundings).  bf16 activations at larger M take the fp16 path: X is copied
  * exactly to fp16 with a power-of-two shift per row, each weight enters the
- * matrix cores as fp16(c * s * 2^f) with one shift f per weight row, so the
- * one extra rounding is that of c * s to 11 significant bits (relative
- * 2^-12 per weight; about 2e-4 of max |Y| at transformer shapes).
+ * matrix cores as fp16(c * fp16(s * 2^f)) with one shift f per weight row
+ * (Q * max_b s * 2^f in [2^14, 2^15)), so the one extra rounding is that of
+ * c * s to 11 significant bits: relative error at most 2^-11 per weight for
+ * every block whose scale is at least Q * 2^-28 of its row's largest scale
+ * (2^-21 for int8, 2^-25 for q4).  Smaller blocks' scaled scales are fp16
+ * subnormals; their weights are off by less than 2^-31 of the row's largest
+ * dequantized weight.  Measured: about 2e-4 of max |Y| at transformer
+ * shapes.
  *
  * Data formats (all buffers are DEVICE memory owned by the caller):
  *   W       fp32 [N][K]
@@ -275,6 +280,38 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
                       const uint16_t *v, int64_t ldv, int64_t B, int64_t T, int64_t H,
                       int64_t dh, float scale, void *o, int64_t ldo, int odt,
                       hipStream_t stream);
+
+/* ---- kernel path selection (diagnostics and tests) -----------------------
+ *
+ * The forward product of the quantized formats has several kernels, each
+ * exact to its own stated accuracy over the shapes it takes; the library
+ * normally picks one by shape (see the accuracy paragraph at the top).
+ * qlinear_force_path makes every later call of qlinear_forward[_ep] and
+ * qlinear_block_forward[_ep] on quantized weights use one kernel, so that
+ * the kernels can be run on the same inputs and compared:
+ *   QL_PATH_GEMV    wavefront-reduction GEMV: bf16 X, 1 <= M <= 4,
+ *                   K % 256 == 0, K <= 8192
+ *   QL_PATH_STREAM  weight-streaming kernel: bf16 X, M <= 32, K % 256 == 0,
+ *                   K <= 2^24, 16-byte aligned scales
+ *   QL_PATH_SKINNY  few-row exact MFMA kernel: bf16 X, M <= 64
+ *   QL_PATH_TILED   tiled exact MFMA kernel: any M, bf16 or fp32 X
+ *   QL_PATH_WIDE    the large-M fp16 path: bf16 X, K % 256 == 0,
+ *                   K < 2^23, 16-byte aligned scales
+ * A call whose layers a forced kernel cannot take returns
+ * QL_ERR_UNSUPPORTED and enqueues nothing.  fp16 weights (QL_FMT_F16) are
+ * not affected.  The setting is process-wide (not per thread or stream);
+ * QL_PATH_AUTO restores the normal choice.  Returns QL_ERR_INVALID for an
+ * unknown value. */
+typedef enum {
+    QL_PATH_AUTO = 0,
+    QL_PATH_GEMV = 1,
+    QL_PATH_STREAM = 2,
+    QL_PATH_SKINNY = 3,
+    QL_PATH_TILED = 4,
+    QL_PATH_WIDE = 5
+} ql_path;
+
+int qlinear_force_path(int path);
 
 /* Static description of a status code. */
 const char *qlinear_status_string(int status);

@@ -170,6 +170,9 @@ bool gemv_ok(const LinDesc &d);
 hipError_t launch_qgemv(int fmt, const LinDesc &d, hipStream_t stream);
 
 int stream_max_m();
+// longest reduction the streaming kernel takes: its per-lane 32-bit load
+// offsets span up to 64 weight rows (64 K bytes) and 32 activation rows
+int stream_max_k();
 // mx: activation rows staged (4, 8, 16, 32); rw: weight rows per workgroup;
 // kw: wavefronts per workgroup; S, psteps: K parts of psteps 32-blocks each
 // (S > 1: LinDesc::part receives plain partial outputs [S][M][N])

@@ -167,16 +167,19 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
     const int bw0 = min(pb0 + wave * per, pb1), bw1 = min(bw0 + per, pb1);
     const int nch = (bw1 - bw0) / G::BPC;
 
-    // per-lane load offsets (from wave-uniform bases that advance per chunk)
-    uint32_t coff[G::NCI], xoff[G::NXI], soff;
+    // per-lane load offsets from wave-uniform 64-bit bases that advance per
+    // chunk.  The bases hold the row group's first row n0, so a lane's
+    // offset only spans the group's RW rows (< 64 K bytes; the host takes
+    // this path for K <= 2^24 only, which keeps every offset below 2^31).
+    uint32_t coff[G::NCI], xoff[G::NXI];
     bool cact[G::NCI];
 #pragma unroll
     for (int r = 0; r < G::NCI; ++r) {
         const int o = (r * 64 + lane) * 16;  // byte offset in the chunk's code area
         const int j = o / G::CB, pp = (o % G::CB) / 16;
         cact[r] = j < RW;
-        const int n = min(n0 + min(j, RW - 1), N - 1);
-        coff[r] = (uint32_t)(n * crow_bytes + cswz<FMT>(j, pp) * 16);
+        const int dn = min(n0 + min(j, RW - 1), N - 1) - n0;
+        coff[r] = (uint32_t)(dn * crow_bytes + cswz<FMT>(j, pp) * 16);
     }
 #pragma unroll
     for (int r = 0; r < G::NXI; ++r) {
@@ -188,7 +191,10 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
     // 32-block run, h < NSL
     const int sp = lane & 3;
 
-    const uint8_t *const cbase = d.codes + (FMT == QL_FMT_INT8 ? bw0 * 32 : bw0 * 16);
+    const uint8_t *const cbase =
+        d.codes + (int64_t)n0 * crow_bytes + (FMT == QL_FMT_INT8 ? bw0 * 32 : bw0 * 16);
+    const uint8_t *const sbase8 =
+        reinterpret_cast<const uint8_t *>(d.scales) + (int64_t)n0 * nb * 2;
     const uint8_t *const xbase = reinterpret_cast<const uint8_t *>(d.X) + bw0 * 64;
 
     auto issue = [&](int c) {
@@ -204,14 +210,13 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
             // scales of blocks bw0 + 4c .. + 31 (pieces past the row end
             // repeat its last piece; their values are never read)
             const int g = c / 8;
-            const uint8_t *sb = reinterpret_cast<const uint8_t *>(d.scales);
 #pragma unroll
             for (int h = 0; h < G::NSL; ++h) {
                 const int sj = 16 * h + (lane >> 2);
-                const int srowi = min(n0 + min(sj, RW - 1), N - 1);
+                const int dn = min(n0 + min(sj, RW - 1), N - 1) - n0;
                 const int b = min(bw0 + 32 * g + 8 * ((sp ^ ((sj >> 2) & 3))), nb - 8);
                 if (sj < RW)
-                    dma16(sb, (uint32_t)(srowi * nb * 2 + b * 2),
+                    dma16(sbase8, (uint32_t)(dn * nb * 2 + b * 2),
                           lds_addr(sring + (g & 1) * G::SLOT) + h * 1024);
             }
         }
@@ -405,6 +410,7 @@ int stream_geo(int fmt, int mx, int rw, int &stage, int &ring)
 }  // namespace
 
 int stream_max_m() { return 32; }
+int stream_max_k() { return 1 << 24; }
 
 // Choice of rows per workgroup, wavefronts and K parts.  Each wavefront
 // keeps R - 1 chunks of loads in flight, so a workgroup streams its bytes

@@ -2,6 +2,7 @@
 // argument checks, tile-shape choice and launch.  Every check happens before
 // anything is enqueued; no entry point throws or aborts.
 #include <algorithm>
+#include <atomic>
 #include <functional>
 #include <mutex>
 #include <queue>
@@ -391,6 +392,99 @@ TileCfg choose_tile(int64_t M, bool xf32)
     return TILE_M128;
 }
 
+// Kernel path forced by qlinear_force_path (QL_PATH_AUTO: the dispatch
+// below chooses).  Process-wide; read once per call.
+std::atomic<int> g_forced_path{QL_PATH_AUTO};
+
+// Few-row kernels, one launch per layer (bf16 activations, quantized
+// weights).  Which kernel each layer takes, decided for every layer before
+// anything is launched.
+enum class RowPath { GEMV, STREAM, SKINNY };
+
+bool stream_fits(const LinDesc &d)
+{
+    return d.M <= stream_max_m() && d.K % 256 == 0 && d.K <= stream_max_k() &&
+           aligned(d.scales, 16);
+}
+
+// the large-M kernel's shape limits (bf16 X): whole 256-k steps, 16-byte
+// scale chunks, 32-bit row offsets within a tile
+bool wide_fits(const ql_linear &l)
+{
+    return l.xdt == QL_DT_BF16 && l.K % 256 == 0 && l.K < ((int64_t)1 << 23) &&
+           (l.fmt == QL_FMT_F16 || aligned(l.scales, 16));
+}
+
+int launch_rows(const ql_linear_ep *const *ls, int n, int forced, hipStream_t stream)
+{
+    LinDesc ds[QL_MAX_GROUP];
+    RowPath path[QL_MAX_GROUP];
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = ds[i];
+        d = LinDesc{};
+        d.X = ls[i]->lin.X;
+        d.codes = (const uint8_t *)ls[i]->lin.codes;
+        d.scales = ls[i]->lin.scales;
+        d.Y = ls[i]->lin.Y;
+        d.ep = to_epilogue(ls[i]->ep);
+        d.M = (int)ls[i]->lin.M;
+        d.N = (int)ls[i]->lin.N;
+        d.K = (int)ls[i]->lin.K;
+        switch (forced) {
+        case QL_PATH_GEMV:
+            if (!gemv_ok(d))
+                return QL_ERR_UNSUPPORTED;
+            path[i] = RowPath::GEMV;
+            break;
+        case QL_PATH_STREAM:
+            if (!stream_fits(d))
+                return QL_ERR_UNSUPPORTED;
+            path[i] = RowPath::STREAM;
+            break;
+        case QL_PATH_SKINNY:
+            if (d.M > skinny_max_m())
+                return QL_ERR_UNSUPPORTED;
+            path[i] = RowPath::SKINNY;
+            break;
+        default:
+            path[i] = gemv_ok(d) ? RowPath::GEMV
+                    : stream_fits(d) ? RowPath::STREAM : RowPath::SKINNY;
+        }
+    }
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = ds[i];
+        const int fmt = ls[i]->lin.fmt;
+        hipError_t e = hipSuccess;
+        if (path[i] == RowPath::GEMV) {
+            e = launch_qgemv(fmt, d, stream);
+        } else if (path[i] == RowPath::STREAM) {
+            const StreamPlan p = stream_plan(fmt, d, device_cus());
+            d.ksplit = p.S;
+            d.psteps = p.psteps;
+            Workspace ws{};
+            if (p.S > 1) {
+                if (!take_workspace(round256((size_t)p.S * d.M * d.N * 4), stream, ws))
+                    return QL_ERR_HIP;
+                d.part = (float *)ws.ptr;
+            }
+            e = launch_qgemm_stream(fmt, p, d, stream);
+            if (e == hipSuccess && p.S > 1) {
+                const SplitSum q{d.part, p.S, d.M, d.N, d.Y, d.ep};
+                e = launch_split_sum(&q, 1, stream);
+            }
+            if (ws.own_alloc) {
+                const hipError_t ef = hipFreeAsync(ws.ptr, stream);
+                e = e == hipSuccess ? ef : e;
+            }
+        } else {
+            e = launch_qgemm_skinny(fmt, d, stream);
+        }
+        if (e != hipSuccess)
+            return QL_ERR_HIP;
+    }
+    return QL_OK;
+}
+
 // One grouped launch over layers that share fmt and xdt (M > 0 each).
 int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
 {
@@ -401,50 +495,20 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->lin.M);
     const bool f16 = ls[0]->lin.fmt == QL_FMT_F16;
-    if (!xf32 && !f16 && maxM <= skinny_max_m()) {
-        // few rows: streaming-bound, one launch per layer
-        for (int i = 0; i < n; ++i) {
-            LinDesc d{};
-            d.X = ls[i]->lin.X;
-            d.codes = (const uint8_t *)ls[i]->lin.codes;
-            d.scales = ls[i]->lin.scales;
-            d.Y = ls[i]->lin.Y;
-            d.ep = to_epilogue(ls[i]->ep);
-            d.M = (int)ls[i]->lin.M;
-            d.N = (int)ls[i]->lin.N;
-            d.K = (int)ls[i]->lin.K;
-            const bool stream_ok = d.M <= stream_max_m() && d.K % 256 == 0 &&
-                                   aligned(d.scales, 16);
-            hipError_t e = hipSuccess;
-            if (gemv_ok(d)) {
-                e = launch_qgemv(ls[i]->lin.fmt, d, stream);
-            } else if (stream_ok) {
-                const StreamPlan p = stream_plan(ls[i]->lin.fmt, d, device_cus());
-                d.ksplit = p.S;
-                d.psteps = p.psteps;
-                Workspace ws{};
-                if (p.S > 1) {
-                    if (!take_workspace(round256((size_t)p.S * d.M * d.N * 4), stream, ws))
-                        return QL_ERR_HIP;
-                    d.part = (float *)ws.ptr;
-                }
-                e = launch_qgemm_stream(ls[i]->lin.fmt, p, d, stream);
-                if (e == hipSuccess && p.S > 1) {
-                    const SplitSum q{d.part, p.S, d.M, d.N, d.Y, d.ep};
-                    e = launch_split_sum(&q, 1, stream);
-                }
-                if (ws.own_alloc) {
-                    const hipError_t ef = hipFreeAsync(ws.ptr, stream);
-                    e = e == hipSuccess ? ef : e;
-                }
-            } else {
-                e = launch_qgemm_skinny(ls[i]->lin.fmt, d, stream);
-            }
-            if (e != hipSuccess)
-                return QL_ERR_HIP;
-        }
-        return QL_OK;
-    }
+    // fp16 weights have one kernel; a forced path applies to quantized ones
+    const int forced = f16 ? QL_PATH_AUTO : g_forced_path.load(std::memory_order_relaxed);
+    const bool per_layer = forced == QL_PATH_AUTO
+                          ? !xf32 && !f16 && maxM <= skinny_max_m()
+                          : forced == QL_PATH_GEMV || forced == QL_PATH_STREAM ||
+                                forced == QL_PATH_SKINNY;
+    if (per_layer && xf32)
+        return QL_ERR_UNSUPPORTED;  // the few-row kernels take bf16 activations
+    if (per_layer)
+        return launch_rows(ls, n, forced, stream);
+    if (forced == QL_PATH_WIDE)
+        for (int i = 0; i < n; ++i)
+            if (!wide_fits(ls[i]->lin))
+                return QL_ERR_UNSUPPORTED;
     maxM = 0;
     for (int i = 0; i < n; ++i)
         maxM = std::max(maxM, ls[i]->lin.M);
@@ -453,8 +517,9 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
     // chunks and addresses a tile's rows with 32-bit offsets
     bool wide = !xf32 && t == TILE_M128;
     for (int i = 0; i < n; ++i)
-        wide = wide && ls[i]->lin.K % 256 == 0 && ls[i]->lin.K < ((int64_t)1 << 23) &&
-               aligned(ls[i]->lin.scales, 16);
+        wide = wide && wide_fits(ls[i]->lin);
+    if (forced == QL_PATH_WIDE || forced == QL_PATH_TILED)
+        wide = forced == QL_PATH_WIDE;
     wide = wide || f16;  // fp16 weights: this kernel at every M (checked by check_linear)
     const int bm = wide ? wide_tile_bm() : tile_bm(t);
     const int bn = wide ? wide_tile_bn() : tile_bn(t);
@@ -642,7 +707,7 @@ int qlinear_quantize(int fmt, const float *W, int64_t N, int64_t K, void *codes,
     ok = ok && hipMemcpyAsync(&hstatus, dstatus, sizeof(int), hipMemcpyDeviceToHost, stream) ==
                    hipSuccess;
     ok = ok && hipStreamSynchronize(stream) == hipSuccess;
-    hipFree(dstatus);
+    ok = hipFree(dstatus) == hipSuccess && ok;
     if (!ok)
         return QL_ERR_HIP;
     return hstatus;
@@ -807,6 +872,14 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
     a.scale_log2e = (float)((double)scale * 1.4426950408889634);
     a.obf16 = odt == QL_DT_BF16 ? 1 : 0;
     return launch_attention(a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
+int qlinear_force_path(int path)
+{
+    if (path < QL_PATH_AUTO || path > QL_PATH_WIDE)
+        return QL_ERR_INVALID;
+    g_forced_path.store(path, std::memory_order_relaxed);
+    return QL_OK;
 }
 
 const char *qlinear_status_string(int status)

@@ -32,7 +32,10 @@ EXPORTS = [
     "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
     "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
     "qlinear_steer", "qlinear_attention", "qlinear_status_string",
+    "qlinear_force_path",
 ]
+
+PATH_AUTO, PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED, PATH_WIDE = range(6)
 
 
 class QLinearError(RuntimeError):
@@ -127,6 +130,8 @@ def load():
                                       ctypes.c_float, vp, i64, ci, vp]
     lib.qlinear_attention.restype = ci
     lib.qlinear_block_forward.restype = ci
+    lib.qlinear_force_path.argtypes = [ci]
+    lib.qlinear_force_path.restype = ci
     lib.qlinear_status_string.argtypes = [ci]
     lib.qlinear_status_string.restype = ctypes.c_char_p
     if len(_hip_runtimes_mapped()) > 1:
@@ -149,6 +154,83 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
+# Argument checks of the binding.  The library receives bare pointers and
+# sizes, so a tensor of the wrong dtype, shape or layout would be read or
+# written out of bounds; these checks run before the library is called.
+_TWO_BYTE = (torch.int16, torch.uint16, torch.bfloat16, torch.float16)
+_BF16_BITS = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _require(t, name, dtypes, shape=None, min_cols=None):
+    """t must be a contiguous (or, with min_cols, unit-column-stride 2-D)
+    device tensor of one of `dtypes`, with `shape` (None entries: any)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor, not {type(t).__name__}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must have dtype {' or '.join(str(d) for d in dtypes)}, "
+                        f"not {t.dtype}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(w is not None and w != h for w, h in zip(shape, t.shape)):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected "
+                             f"{tuple('*' if w is None else w for w in shape)}")
+    if min_cols is not None:
+        if t.dim() != 2 or t.stride(1) != 1 or t.shape[1] < min_cols or \
+                (t.shape[0] > 1 and t.stride(0) < min_cols):
+            raise ValueError(f"{name} must be a 2-D row view with unit column stride and at "
+                             f"least {min_cols} columns per row")
+    elif not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _on_device(*tensors):
+    """Every tensor given (None skipped) must be device memory; checked
+    after the dtype and shape checks of a call."""
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise ValueError("every tensor argument must be a device (cuda) tensor")
+
+
+def _require_weights(fmt, codes, scales, N, K):
+    if fmt == FMT_F16:
+        _require(codes, "codes (fp16 weights)", _TWO_BYTE, (N, K))
+        return
+    if fmt not in (FMT_INT8, FMT_Q4):
+        raise ValueError(f"unknown weight format {fmt}")
+    if K % BLOCK:
+        raise ValueError(f"K = {K} is not a multiple of {BLOCK}")
+    _require(codes, "codes", (torch.uint8, torch.int8), (N, K if fmt == FMT_INT8 else K // 2))
+    _require(scales, "scales", _TWO_BYTE, (N, K // BLOCK))
+
+
+def _require_x(X):
+    if not isinstance(X, torch.Tensor) or X.dim() != 2:
+        raise ValueError("activations X must be a 2-D tensor [M][K]")
+    _require(X, "X", (torch.float32,) + _BF16_BITS)
+    return X.shape
+
+
+def _require_y(Y, M, N, ydtypes=(torch.float32,)):
+    _require(Y, "Y", ydtypes, (M, N))
+
+
+def _require_ep(bias, residual, M, N):
+    if bias is not None:
+        _require(bias, "bias", (torch.float32,), (N,))
+    if residual is not None:
+        _require(residual, "residual", (torch.float32,), (M, N))
+
+
+def _require_steer(steer, N):
+    if steer is None:
+        return
+    d, hnorm, strength = steer
+    _require(d, "steering direction", (torch.float32,), (N,))
+    _require(strength, "steering strength", (torch.float32,))
+    if strength.numel() < 1:
+        raise ValueError("steering strength must hold one element")
+
+
 def codes_bytes(fmt, N, K):
     return int(load().qlinear_codes_bytes(fmt, N, K))
 
@@ -169,9 +251,16 @@ def empty_scales(N, K, device="cuda"):
 
 def quantize(fmt, W, codes=None, scales=None, stream=None):
     """Quantize fp32 W [N][K] (device) -> (codes, scales).  Synchronous."""
+    if fmt not in (FMT_INT8, FMT_Q4):
+        raise ValueError(f"quantize takes FMT_INT8 or FMT_Q4, not {fmt}")
+    _require(W, "W", (torch.float32,), (None, None))
     N, K = W.shape
+    if K % BLOCK:
+        raise ValueError(f"K = {K} is not a multiple of {BLOCK}")
     codes = empty_codes(fmt, N, K, W.device) if codes is None else codes
     scales = empty_scales(N, K, W.device) if scales is None else scales
+    _require_weights(fmt, codes, scales, N, K)
+    _on_device(W, codes, scales)
     _check(load().qlinear_quantize(fmt, _ptr(W), N, K, _ptr(codes), _ptr(scales),
                                    _stream(stream)))
     return codes, scales
@@ -189,9 +278,12 @@ def forward(fmt, X, codes, scales, N, Y=None, stream=None):
     """Y [M][N] fp32 = X [M][K] . dequant(codes, scales)^T.  Asynchronous.
     FMT_F16: codes are the fp16 weights [N][K] (any 2-byte dtype), scales
     None."""
-    M, K = X.shape
+    M, K = _require_x(X)
+    _require_weights(fmt, codes, scales, N, K)
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    _require_y(Y, M, N)
+    _on_device(X, codes, scales, Y)
     _check(load().qlinear_forward(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
                                   _ptr(Y), _stream(stream)))
     return Y
@@ -224,10 +316,15 @@ def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residu
     hnorm, strength) adds the steering term with alpha = strength[0] read on
     the device by the launch (skipped exactly when alpha is 0).
     Asynchronous."""
-    M, K = X.shape
+    M, K = _require_x(X)
+    _require_weights(fmt, codes, scales, N, K)
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=X.device)
+    _require_y(Y, M, N, (torch.float32, torch.bfloat16))
+    _require_ep(bias, residual, M, N)
+    _require_steer(steer, N)
     ep = _epilogue(Y, bias, act, residual, steer)
+    _on_device(X, codes, scales, Y, bias, residual, *(steer[::2] if steer else ()))
     _check(load().qlinear_forward_ep(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
                                      _ptr(Y), ctypes.byref(ep), _stream(stream)))
     return Y
@@ -236,9 +333,14 @@ def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residu
 def make_group(entries):
     """ctypes array for block_forward from (fmt, X, codes, scales, N, Y) tuples.
     The tensors must outlive every use of the returned array."""
+    if not 1 <= len(entries) <= MAX_GROUP:
+        raise ValueError(f"a group holds 1 to {MAX_GROUP} linears, not {len(entries)}")
     arr = (_Linear * len(entries))()
     for i, (fmt, X, codes, scales, N, Y) in enumerate(entries):
-        M, K = X.shape
+        M, K = _require_x(X)
+        _require_weights(fmt, codes, scales, N, K)
+        _require_y(Y, M, N)
+        _on_device(X, codes, scales, Y)
         arr[i] = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                          scales.data_ptr() if scales is not None else 0, Y.data_ptr())
     return arr
@@ -258,11 +360,18 @@ def make_group_ep(entries):
     bias, act, residual[, steer]) tuples (bias/residual/steer None for none;
     Y fp32 or bf16).  The tensors must outlive every use of the returned
     array."""
+    if not 1 <= len(entries) <= MAX_GROUP:
+        raise ValueError(f"a group holds 1 to {MAX_GROUP} linears, not {len(entries)}")
     arr = (_LinearEp * len(entries))()
     for i, e in enumerate(entries):
         fmt, X, codes, scales, N, Y, bias, act, residual = e[:9]
         steer = e[9] if len(e) > 9 else None
-        M, K = X.shape
+        M, K = _require_x(X)
+        _require_weights(fmt, codes, scales, N, K)
+        _require_y(Y, M, N, (torch.float32, torch.bfloat16))
+        _require_ep(bias, residual, M, N)
+        _require_steer(steer, N)
+        _on_device(X, codes, scales, Y, bias, residual, *(steer[::2] if steer else ()))
         lin = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                       scales.data_ptr() if scales is not None else 0, Y.data_ptr())
         arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual, steer))
@@ -280,11 +389,14 @@ def block_forward_ep(entries, stream=None, group=None):
 def quantize_act(X, qx=None, sx=None, stream=None):
     """Per-token int8 quantization of activations X [M][K] (fp32 or bf16):
     returns (qx int8 [M][K], sx fp16 bits as int16 [M]).  Asynchronous."""
-    M, K = X.shape
+    M, K = _require_x(X)
     if qx is None:
         qx = torch.empty((M, K), dtype=torch.int8, device=X.device)
     if sx is None:
         sx = torch.empty(M, dtype=torch.int16, device=X.device)
+    _require(qx, "qx", (torch.int8,), (M, K))
+    _require(sx, "sx", _TWO_BYTE, (M,))
+    _on_device(X, qx, sx)
     _check(load().qlinear_quantize_act(_ptr(X), _xdt(X), M, K, _ptr(qx), _ptr(sx),
                                        _stream(stream)))
     return qx, sx
@@ -295,10 +407,17 @@ def forward_w8a8(qx, sx, codes, scales, N, Y=None, bias=None, act=ACT_NONE, resi
     """W8A8 product of per-token int8 activations (quantize_act) and int8
     weights (quantize(FMT_INT8, ...)), with the layer epilogue (arguments as
     forward_ep).  Asynchronous."""
+    _require(qx, "qx", (torch.int8,), (None, None))
     M, K = qx.shape
+    _require(sx, "sx", _TWO_BYTE, (M,))
+    _require_weights(FMT_INT8, codes, scales, N, K)
     if Y is None:
         Y = torch.empty((M, N), dtype=ydtype, device=qx.device)
+    _require_y(Y, M, N, (torch.float32, torch.bfloat16))
+    _require_ep(bias, residual, M, N)
+    _require_steer(steer, N)
     ep = _epilogue(Y, bias, act, residual, steer)
+    _on_device(qx, sx, codes, scales, Y, bias, residual, *(steer[::2] if steer else ()))
     _check(load().qlinear_forward_w8a8(_ptr(qx), _ptr(sx), M, K, _ptr(codes), _ptr(scales), N,
                                        _ptr(Y), ctypes.byref(ep), _stream(stream)))
     return Y
@@ -308,7 +427,10 @@ def steer(h, direction, hnorm, strength, stream=None):
     """h += alpha * hnorm * direction on every row, in place (Eq. 2), with
     alpha = strength[0] read on the device at run time (skipped exactly when
     alpha is 0).  Asynchronous."""
+    _require(h, "h", (torch.float32,), (None, None))
     M, N = h.shape
+    _require_steer((direction, hnorm, strength), N)
+    _on_device(h, direction, strength)
     _check(load().qlinear_steer(_ptr(h), M, N, _ptr(direction), float(hnorm), _ptr(strength),
                                 _stream(stream)))
     return h
@@ -319,17 +441,39 @@ def attention(q, k, v, B, T, H, dh=64, scale=None, O=None, odtype=torch.float32,
     int16 bit patterns) 2-D row views [B*T][>= H*dh] with unit column stride
     (e.g. column slices of a fused QKV output).  Returns O [B*T][H*dh] fp32
     or bf16.  Asynchronous."""
-    for t in (q, k, v):
-        if t.dim() != 2 or t.stride(1) != 1:
-            raise ValueError("q, k, v must be 2-D row views with unit column stride")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _require(t, name, _BF16_BITS, min_cols=H * dh)
+        if t.shape[0] != B * T:
+            raise ValueError(f"{name} has {t.shape[0]} rows, expected B * T = {B * T}")
     if O is None:
         O = torch.empty((B * T, H * dh), dtype=odtype, device=q.device)
+    _require(O, "O", (torch.float32, torch.bfloat16), min_cols=H * dh)
+    if O.shape[0] != B * T:
+        raise ValueError(f"O has {O.shape[0]} rows, expected B * T = {B * T}")
     odt = DT_BF16 if O.dtype == torch.bfloat16 else DT_F32
     scale = 1.0 / float(dh) ** 0.5 if scale is None else scale
+    _on_device(q, k, v, O)
     _check(load().qlinear_attention(_ptr(q), q.stride(0), _ptr(k), k.stride(0), _ptr(v),
                                     v.stride(0), B, T, H, dh, float(scale), _ptr(O),
                                     O.stride(0), odt, _stream(stream)))
     return O
+
+
+class forced_path:
+    """Context manager: every quantized forward call inside it runs on one
+    kernel (PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED or PATH_WIDE;
+    qlinear_force_path).  Process-wide; restores automatic choice on exit."""
+
+    def __init__(self, path):
+        self.path = path
+
+    def __enter__(self):
+        _check(load().qlinear_force_path(self.path))
+        return self
+
+    def __exit__(self, *exc):
+        _check(load().qlinear_force_path(PATH_AUTO))
+        return False
 
 
 class QuantizedLinear:

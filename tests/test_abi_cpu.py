@@ -44,7 +44,18 @@ def test_header_declares_the_boundary():
         "qlinear_codes_bytes", "qlinear_scales_bytes", "qlinear_quantize",
         "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
         "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
-        "qlinear_steer", "qlinear_attention", "qlinear_status_string"])
+        "qlinear_steer", "qlinear_attention", "qlinear_status_string",
+        "qlinear_force_path"])
+
+
+def test_force_path_values(lib):
+    """The path knob takes the six documented values (setting it launches
+    nothing) and rejects others; left at automatic choice."""
+    for p in range(6):
+        assert lib.qlinear_force_path(p) == OK
+    for bad in (-1, 6, 99):
+        assert lib.qlinear_force_path(bad) == INVALID
+    assert lib.qlinear_force_path(0) == OK
 
 
 def test_library_exports_every_declared_symbol(lib):

@@ -227,6 +227,49 @@ def test_forward_row_scales_far_apart(gpu, orc, fmt):
 
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_block_scales_far_apart(gpu, orc, fmt):
+    """Weight rows whose blocks lie many binary decades apart (block
+    magnitudes 2^-20 .. 2^16 within one row, rows whose largest block
+    exceeds 2^15 so that the large-M path shifts them down, rows of tiny
+    blocks only), on the exact small-M path (M = 40) and the folded large-M
+    path (M = 200).
+
+    Bound, element by element: the large-M path enters each weight as
+    fp16(c * s') with s' = s * 2^f and f set by the row's largest scale.
+    When s' is a normal fp16 (s at least Q * 2^-28 of the row's largest
+    scale) that is one rounding, relative error <= 2^-11; below it s' itself
+    is rounded to a subnormal, an absolute error <= (Q + 2) * 2^-25 in the
+    shifted units, i.e. <= (Q + 2) * Q * smax * 2^-39 per unit of |x|.  The
+    fp32 accumulation adds <= K * 2^-24 of sum |x| |w|.  So
+      |Yg - Yr| <= (2^-11 + (K + 8) 2^-24) (|X| |W|^T)[m][n]
+                   + (Q + 2) Q smax[n] 2^-39 sum_k |X[m][k]|."""
+    Q = QMAX[fmt]
+    rng = np.random.default_rng(3100 + fmt)
+    N, K = 64, 1024
+    nb = K // 32
+    u = rng.integers(-20, 17, (N, nb)).astype(np.float64)
+    u[0] = 16.0            # every block large: negative row shift
+    u[1] = -20.0           # every block tiny: large positive row shift
+    u[2, ::2], u[2, 1::2] = 16.0, -20.0   # 36 binary decades inside one row
+    u[3, 0] = 16.0         # one large block, the rest random
+    W = (rng.standard_normal((N, K)) * np.repeat(2.0 ** u, 32, axis=1)).astype(np.float32)
+    codes, scales = quantize_both(gpu, orc, fmt, W)
+    Wd = orc.dequantize(fmt, codes, scales, N, K)
+    smax = np.max(np.abs(Wd), axis=1) / Q
+    for M in (40, 200):
+        X = si.small_case(3200 + M + fmt, M, 1, K)[1]
+        Xv = si.bf16_bits_to_f32(X).astype(np.float64)
+        Yg = forward_gpu(gpu, fmt, X, O.DT_BF16, codes, scales, N).astype(np.float64)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        A = np.abs(Xv) @ np.abs(Wd).T
+        lim = (2.0 ** -11 + (K + 8) * 2.0 ** -24) * A + \
+            (Q + 2) * Q * 2.0 ** -39 * np.outer(np.abs(Xv).sum(axis=1), smax)
+        bad = np.argwhere(np.abs(Yg - Yr) > lim)
+        assert len(bad) == 0, (M, bad[:5], (Yg - Yr)[tuple(bad[0])], lim[tuple(bad[0])])
+        assert rel_err(Yg, Yr) <= TOL[O.DT_BF16]
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 @pytest.mark.parametrize("xdt", [O.DT_BF16, O.DT_F32])
 def test_forward_power_of_two_exact(gpu, orc, fmt, xdt):
     """W = c * 2^-12, integer X: the exact result is representable, so the
@@ -422,13 +465,13 @@ def test_forward_f16_weights(gpu, orc):
 
 
 def test_forward_f16_block_and_errors(gpu, orc):
-    """A grouped call of one block's four fp16-weight linears (sampled rows
+    """A grouped call of one block's four fp16-weight linears (every row
     against the oracle), and the calls the format does not take."""
     torch, ql = gpu
     xa, xb = si.paper_activations(1)
     d = si.PAPER_WIDTHS[1][1]
     entries, refs = [], []
-    rows = sample_rows(xa.shape[0], 8, 3)
+    rows = np.arange(xa.shape[0])
     for i, (_, N, K) in enumerate(si.block_linears(d)):
         W16 = f16_bits(si.paper_weight(1, 0, i))
         X = xb if K == 4 * d else xa
@@ -439,6 +482,7 @@ def test_forward_f16_block_and_errors(gpu, orc):
     ql.block_forward(entries)
     torch.cuda.synchronize()
     for e, Yr in zip(entries, refs):
+        assert bool(torch.isfinite(e[5]).all())
         assert rel_err(e[5].cpu().numpy()[rows], Yr) <= TOL[O.DT_BF16]
     w = torch.zeros((16, 512), dtype=torch.int16, device="cuda")
     for X, status in ((torch.zeros((4, 512), dtype=torch.float32, device="cuda"), 5),
@@ -477,9 +521,24 @@ def sample_rows(M, k, seed):
     return np.array(sorted(rows), dtype=np.int64)
 
 
+def tile_rows(M, k, seed, tile=128):
+    """At least k distinct rows of an M-row output: one random row inside
+    every `tile`-row band (so every row tile of a grouped launch is sampled),
+    the first and last rows, and random others up to k."""
+    rng = np.random.default_rng(seed)
+    rows = {0, M - 1}
+    for t0 in range(0, M, tile):
+        rows.add(int(rng.integers(t0, min(t0 + tile, M))))
+    rest = [r for r in rng.permutation(M).tolist() if r not in rows]
+    rows |= set(rest[:max(0, k - len(rows))])
+    return np.array(sorted(rows), dtype=np.int64)
+
+
 def run_block(gpu, orc, fmt, weights, xa, xb, rows, check_codes=True):
-    """One DiT block's four linears through qlinear_block_forward; checks the
-    sampled rows of every output against the oracle."""
+    """One DiT block's four linears through qlinear_block_forward.  Every Y
+    starts NaN-filled: the whole output of every linear must be finite (every
+    element written) and the sampled rows must match the oracle (all N
+    columns)."""
     torch, ql = gpu
     xa_d, xb_d = dev_x(torch, xa, O.DT_BF16), dev_x(torch, xb, O.DT_BF16)
     entries, host = [], []
@@ -492,13 +551,14 @@ def run_block(gpu, orc, fmt, weights, xa, xb, rows, check_codes=True):
             assert np.array_equal(host_codes(cd), cr)
         else:
             cr, sr = host_codes(cd), host_scales(sd)
-        Y = torch.empty((xa.shape[0], N), dtype=torch.float32, device="cuda")
+        Y = torch.full((xa.shape[0], N), float("nan"), dtype=torch.float32, device="cuda")
         entries.append((fmt, xb_d if K == 4 * xa.shape[1] else xa_d, cd, sd, N, Y))
         host.append((cr, sr, N, K))
     ql.block_forward(entries)
     torch.cuda.synchronize()
     errs = []
-    for (fmt_, X_d, cd, sd, N, Y), (cr, sr, N_, K) in zip(entries, host):
+    for i, ((fmt_, X_d, cd, sd, N, Y), (cr, sr, N_, K)) in enumerate(zip(entries, host)):
+        assert bool(torch.isfinite(Y).all()), f"linear {i}: unwritten (NaN) or non-finite outputs"
         X = xb if K == 4 * xa.shape[1] else xa
         Yr = orc.forward(fmt, X, O.DT_BF16, cr, sr, N, rows=rows)
         Yg = Y.cpu().numpy()[rows]
@@ -509,17 +569,26 @@ def run_block(gpu, orc, fmt, weights, xa, xb, rows, check_codes=True):
 def test_block_int8_config(gpu, orc):
     xa, xb = si.block_activations()
     weights = [si.block_int8_weight(i) for i in range(4)]
-    rows = sample_rows(xa.shape[0], 14, 0)
+    rows = tile_rows(xa.shape[0], 64, 0)
+    assert len(rows) >= 64
     errs = run_block(gpu, orc, O.FMT_INT8, weights, xa, xb, rows)
     print("block int8 errs", errs)
     assert max(errs) <= TOL[O.DT_BF16]
 
 
-@pytest.mark.parametrize("blk", [0, 23])
-def test_step_q4_config_sampled_blocks(gpu, orc, blk):
-    xa, xb = si.block_activations()
+@pytest.fixture(scope="module")
+def block_x():
+    return si.block_activations()
+
+
+@pytest.mark.parametrize("blk", range(si.N_BLOCKS))
+def test_step_q4_config_every_block(gpu, orc, block_x, blk):
+    """All 24 blocks of the q4 denoising step: codes and scales bit for bit,
+    every output finite, 64 rows (one in every 128-row tile) x all N of each
+    linear against the oracle."""
+    xa, xb = block_x
     weights = [si.step_q4_weight(blk, i) for i in range(4)]
-    rows = sample_rows(xa.shape[0], 6, blk)
+    rows = tile_rows(xa.shape[0], 64, 1000 + blk)
     errs = run_block(gpu, orc, O.FMT_Q4, weights, xa, xb, rows)
     print(f"step q4 block {blk} errs", errs)
     assert max(errs) <= TOL[O.DT_BF16]
@@ -573,3 +642,85 @@ def test_block_forward_mixed_group(gpu, orc):
         if M == 0:
             continue
         assert rel_err(e[5].cpu().numpy(), Yr) <= TOL[xdt]
+
+
+# --------------------------------------------------------------------------
+# the same shapes through every kernel that takes them (qlinear_force_path)
+# --------------------------------------------------------------------------
+
+EXACT_PATHS = ("GEMV", "STREAM", "SKINNY", "TILED")
+
+
+def takes(path, M, K):
+    """Shape limits of each forced kernel (include/qlinear.h)."""
+    return {"GEMV": 1 <= M <= 4 and K % 256 == 0 and K <= 8192,
+            "STREAM": M <= 32 and K % 256 == 0,
+            "SKINNY": M <= 64,
+            "TILED": True,
+            "WIDE": K % 256 == 0}[path]
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forced_paths_agree(gpu, orc, fmt):
+    """Each shape runs through every kernel that takes it: the exact kernels
+    (GEMV, streaming, few-row MFMA, tiled MFMA) each within 1e-5 of the
+    oracle and within 2e-6 of one another; the large-M fp16 path within the
+    bf16 tolerance.  A kernel that cannot take a shape refuses it
+    (QL_ERR_UNSUPPORTED) and leaves Y untouched."""
+    torch, ql = gpu
+    shapes = [(1, 300, 2048), (3, 257, 1024), (4, 64, 8192), (8, 300, 2048), (17, 200, 512),
+              (32, 513, 2304), (64, 96, 768), (130, 260, 1280), (40, 48, 96)]
+    try:
+        for (M, N, K) in shapes:
+            W, X = si.small_case(7000 + M + N + K + fmt, M, N, K)
+            codes, scales = quantize_both(gpu, orc, fmt, W)
+            cd = torch.from_numpy(codes).cuda()
+            sd = torch.from_numpy(scales.view(np.int16)).cuda()
+            xd = dev_x(torch, X, O.DT_BF16)
+            Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+            got = {}
+            for name in EXACT_PATHS + ("WIDE",):
+                Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+                ql.load().qlinear_force_path(getattr(ql, "PATH_" + name))
+                if not takes(name, M, K):
+                    with pytest.raises(ql.QLinearError) as err:
+                        ql.forward(fmt, xd, cd, sd, N, Y)
+                    assert err.value.status == 5, (name, M, K)
+                    torch.cuda.synchronize()
+                    assert bool(torch.isnan(Y).all()), (name, M, K)
+                    continue
+                ql.forward(fmt, xd, cd, sd, N, Y)
+                torch.cuda.synchronize()
+                got[name] = Y.cpu().numpy().astype(np.float64)
+                tol = TOL[O.DT_BF16] if name == "WIDE" else 1e-5
+                assert rel_err(got[name], Yr) <= tol, (name, M, N, K, rel_err(got[name], Yr))
+            exact = [got[p] for p in EXACT_PATHS if p in got]
+            assert len(exact) >= 1
+            for Ya in exact[1:]:
+                assert rel_err(Ya, exact[0]) <= 2e-6, (M, N, K)
+    finally:
+        ql.load().qlinear_force_path(ql.PATH_AUTO)
+
+
+def test_forced_path_fp32_activations(gpu, orc):
+    """fp32 activations: only the tiled kernel takes them; the few-row and
+    fp16-path kernels refuse."""
+    torch, ql = gpu
+    M, N, K = 12, 40, 256
+    W, X = si.small_case(7100, M, N, K, O.DT_F32)
+    codes, scales = orc.quantize(O.FMT_INT8, W)
+    cd = torch.from_numpy(codes).cuda()
+    sd = torch.from_numpy(scales.view(np.int16)).cuda()
+    xd = dev_x(torch, X, O.DT_F32)
+    try:
+        for name in ("GEMV", "STREAM", "SKINNY", "WIDE"):
+            ql.load().qlinear_force_path(getattr(ql, "PATH_" + name))
+            with pytest.raises(ql.QLinearError) as err:
+                ql.forward(O.FMT_INT8, xd, cd, sd, N)
+            assert err.value.status == 5, name
+        ql.load().qlinear_force_path(ql.PATH_TILED)
+        Yg = ql.forward(O.FMT_INT8, xd, cd, sd, N)
+        torch.cuda.synchronize()
+        assert rel_err(Yg.cpu().numpy(), orc.forward(O.FMT_INT8, X, O.DT_F32, codes, scales, N)) <= 1e-5
+    finally:
+        ql.load().qlinear_force_path(ql.PATH_AUTO)
