@@ -216,6 +216,25 @@ typedef struct {
 /* qlinear_block_forward with an epilogue per layer. */
 int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t stream);
 
+/* qlinear_block_forward_ep for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  The same kernels and results, bit for bit, but the
+ * workspace (fp16 activation copies, row shifts, split partials and arrival
+ * counters) lives in a static device array of the library, 96 MiB
+ * (100663296 bytes) per device, held from the first call on a device until
+ * the process ends.  The call allocates and frees nothing, through HIP or
+ * any allocating library.  A call whose workspace would exceed the array
+ * returns QL_ERR_UNSUPPORTED and enqueues nothing (one DiT block at
+ * d = 2048 takes about 76 MB at 2048 tokens and 84 MB at 4096).  Every
+ * call on a device shares that device's array: calls that may overlap on
+ * one device (different streams, or graph replays concurrent with other
+ * calls) race and must be ordered by the caller; calls on one stream are
+ * ordered by the stream.  The array keeps the last call's contents; the
+ * kernels clear what must start at zero themselves.  Other arguments,
+ * checks and errors as qlinear_block_forward_ep; QL_ERR_HIP if the array's
+ * device address cannot be looked up. */
+int qlinear_block_forward_ep_noalloc(const ql_linear_ep *lin, int n_lin, hipStream_t stream);
+
 /* ---- W8A8: int8 activations against int8 weights -------------------------
  *
  * The paper's 8-bit-arithmetic mode (Methodology; Table II): activations are

@@ -106,7 +106,7 @@ hipMemPool_t workspace_pool()
             return nullptr;
         uint64_t keep = UINT64_MAX;
         if (hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess) {
-            hipMemPoolDestroy(p);
+            (void)hipMemPoolDestroy(p);  // already failing; nothing to report
             return nullptr;
         }
         pools[dev] = p;
@@ -178,12 +178,36 @@ bool take_workspace(size_t bytes, hipStream_t stream, Workspace &w)
     if (hipMallocFromPoolAsync(&p, grow, pool, stream) != hipSuccess)
         return false;
     if (e->ptr && !e->captured && hipFreeAsync(e->ptr, stream) != hipSuccess) {
-        hipFreeAsync(p, stream);
+        (void)hipFreeAsync(p, stream);  // already failing; nothing to report
         return false;
     }
     *e = Entry{dev, stream, p, grow, false};
     w = Workspace{(uint8_t *)p, false};
     return true;
+}
+
+// Where a call's workspace comes from: the per-stream buffer above, or a
+// fixed region (the no-allocation entry point's static scratch).  A dry run
+// enqueues nothing: it only records the largest workspace the call takes.
+struct WsSource {
+    uint8_t *fixed;  // device address of the fixed region, or nullptr: pool
+    size_t cap;      // bytes of the fixed region
+    bool dry_run;
+    size_t need;     // out: largest single request
+};
+
+WsSource pool_source() { return WsSource{nullptr, 0, false, 0}; }
+
+bool get_workspace(WsSource &wsrc, size_t bytes, hipStream_t stream, Workspace &w)
+{
+    wsrc.need = std::max(wsrc.need, bytes);
+    if (wsrc.fixed) {
+        if (bytes > wsrc.cap)
+            return false;
+        w = Workspace{wsrc.fixed, false};
+        return true;
+    }
+    return take_workspace(bytes, stream, w);
 }
 
 int device_cus()
@@ -415,10 +439,12 @@ bool wide_fits(const ql_linear &l)
            (l.fmt == QL_FMT_F16 || aligned(l.scales, 16));
 }
 
-int launch_rows(const ql_linear_ep *const *ls, int n, int forced, hipStream_t stream)
+int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc,
+                hipStream_t stream)
 {
     LinDesc ds[QL_MAX_GROUP];
     RowPath path[QL_MAX_GROUP];
+    StreamPlan plan[QL_MAX_GROUP];
     for (int i = 0; i < n; ++i) {
         LinDesc &d = ds[i];
         d = LinDesc{};
@@ -450,7 +476,17 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, hipStream_t st
             path[i] = gemv_ok(d) ? RowPath::GEMV
                     : stream_fits(d) ? RowPath::STREAM : RowPath::SKINNY;
         }
+        if (path[i] == RowPath::STREAM) {
+            plan[i] = stream_plan(ls[i]->lin.fmt, d, device_cus());
+            d.ksplit = plan[i].S;
+            d.psteps = plan[i].psteps;
+            if (plan[i].S > 1)
+                wsrc.need = std::max(wsrc.need, round256((size_t)plan[i].S * d.M * d.N * 4));
+        }
     }
+    // layers run in stream order, so each split layer reuses the workspace
+    if (wsrc.dry_run || (wsrc.fixed && wsrc.need > wsrc.cap))
+        return wsrc.dry_run ? QL_OK : QL_ERR_UNSUPPORTED;
     for (int i = 0; i < n; ++i) {
         LinDesc &d = ds[i];
         const int fmt = ls[i]->lin.fmt;
@@ -458,12 +494,10 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, hipStream_t st
         if (path[i] == RowPath::GEMV) {
             e = launch_qgemv(fmt, d, stream);
         } else if (path[i] == RowPath::STREAM) {
-            const StreamPlan p = stream_plan(fmt, d, device_cus());
-            d.ksplit = p.S;
-            d.psteps = p.psteps;
+            const StreamPlan &p = plan[i];
             Workspace ws{};
             if (p.S > 1) {
-                if (!take_workspace(round256((size_t)p.S * d.M * d.N * 4), stream, ws))
+                if (!get_workspace(wsrc, round256((size_t)p.S * d.M * d.N * 4), stream, ws))
                     return QL_ERR_HIP;
                 d.part = (float *)ws.ptr;
             }
@@ -486,7 +520,7 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, hipStream_t st
 }
 
 // One grouped launch over layers that share fmt and xdt (M > 0 each).
-int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
+int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream_t stream)
 {
     if (n == 0)
         return QL_OK;
@@ -504,7 +538,7 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
     if (per_layer && xf32)
         return QL_ERR_UNSUPPORTED;  // the few-row kernels take bf16 activations
     if (per_layer)
-        return launch_rows(ls, n, forced, stream);
+        return launch_rows(ls, n, forced, wsrc, stream);
     if (forced == QL_PATH_WIDE)
         for (int i = 0; i < n; ++i)
             if (!wide_fits(ls[i]->lin))
@@ -566,8 +600,11 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
-    if (!wide)
+    if (!wide) {
+        if (wsrc.dry_run)
+            return QL_OK;  // no workspace
         return launch_qgemm(ord[0]->lin.fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
+    }
 
     // Workspace: one exact, row-shifted fp16 copy per distinct activation
     // tensor (layers reading the same X share it)
@@ -615,9 +652,13 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
         ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
     }
     bytes += round256((size_t)ncnt * 4);
+    if (wsrc.dry_run) {
+        wsrc.need = std::max(wsrc.need, bytes);
+        return QL_OK;
+    }
     Workspace ws{};
-    if (!take_workspace(bytes, stream, ws))
-        return QL_ERR_HIP;
+    if (!get_workspace(wsrc, bytes, stream, ws))
+        return wsrc.fixed ? QL_ERR_UNSUPPORTED : QL_ERR_HIP;
     uint8_t *const wsb = ws.ptr;
     for (int i = 0; i < n; ++i)
         if (a.d[i].ksplit > 1 || a.d[i].part_out) {
@@ -661,6 +702,63 @@ int launch_group(const ql_linear_ep *const *ls, int n, hipStream_t stream)
     }
     const hipError_t ef = ws.own_alloc ? hipFreeAsync(ws.ptr, stream) : hipSuccess;
     return e == hipSuccess && ef == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
+// The layers of a block call, partitioned by (fmt, xdt): each class is one
+// launch_group call.
+struct Classes {
+    const ql_linear_ep *cls[6][QL_MAX_GROUP];
+    int cnt[6];
+};
+
+int classify(const ql_linear_ep *lin, int n_lin, Classes &c)
+{
+    if (!lin || n_lin < 1 || n_lin > QL_MAX_GROUP)
+        return QL_ERR_INVALID;
+    for (int i = 0; i < n_lin; ++i) {
+        const int st = check_layer(lin[i]);
+        if (st != QL_OK)
+            return st;
+    }
+    std::fill(c.cnt, c.cnt + 6, 0);
+    for (int i = 0; i < n_lin; ++i) {
+        const ql_linear &l = lin[i].lin;
+        if (l.M == 0)
+            continue;
+        const int f = l.fmt == QL_FMT_Q4 ? 0 : l.fmt == QL_FMT_INT8 ? 1 : 2;
+        const int k = 2 * f + (l.xdt == QL_DT_BF16 ? 1 : 0);
+        c.cls[k][c.cnt[k]++] = &lin[i];
+    }
+    return QL_OK;
+}
+
+// Static scratch of the no-allocation entry point (the fp16 activation
+// copies, row shifts, split partials and arrival counters that the pool
+// workspace holds otherwise).  Each device the library runs on holds its own
+// copy for the life of the process.  Host code must never use the array's
+// name as an address: kernels and copies take the device address that
+// hipGetSymbolAddress returns for the current device (scratch_base).
+constexpr size_t SCRATCH_BYTES = (size_t)96 << 20;
+static __device__ __align__(256) uint8_t scratch[SCRATCH_BYTES];
+
+// Device address of this device's scratch, looked up once per device (with
+// that device current); nullptr if the lookup fails.
+uint8_t *scratch_base()
+{
+    constexpr int MAXDEV = 64;
+    static std::mutex mu;
+    static uint8_t *base[MAXDEV] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV)
+        return nullptr;
+    std::lock_guard<std::mutex> g(mu);
+    if (!base[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+            return nullptr;
+        base[dev] = (uint8_t *)p;
+    }
+    return base[dev];
 }
 
 }  // namespace
@@ -723,7 +821,8 @@ int qlinear_forward_ep(int fmt, const void *X, int xdt, int64_t M, int64_t K, co
     if (st != QL_OK || M == 0)
         return st;
     const ql_linear_ep *p = &l;
-    return launch_group(&p, 1, stream);
+    WsSource src = pool_source();
+    return launch_group(&p, 1, src, stream);
 }
 
 int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K, const void *codes,
@@ -734,27 +833,39 @@ int qlinear_forward(int fmt, const void *X, int xdt, int64_t M, int64_t K, const
 
 int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t stream)
 {
-    if (!lin || n_lin < 1 || n_lin > QL_MAX_GROUP)
-        return QL_ERR_INVALID;
-    for (int i = 0; i < n_lin; ++i) {
-        const int st = check_layer(lin[i]);
-        if (st != QL_OK)
+    Classes c;
+    const int st = classify(lin, n_lin, c);
+    if (st != QL_OK)
+        return st;
+    for (int k = 0; k < 6; ++k) {
+        WsSource src = pool_source();
+        const int s = launch_group(c.cls[k], c.cnt[k], src, stream);
+        if (s != QL_OK)
+            return s;
+    }
+    return QL_OK;
+}
+
+int qlinear_block_forward_ep_noalloc(const ql_linear_ep *lin, int n_lin, hipStream_t stream)
+{
+    Classes c;
+    int st = classify(lin, n_lin, c);
+    if (st != QL_OK)
+        return st;
+    uint8_t *const base = scratch_base();
+    if (!base)
+        return QL_ERR_HIP;
+    // size every class's workspace before anything is enqueued; classes run
+    // in stream order, so each reuses the scratch from its start
+    WsSource dry{base, SCRATCH_BYTES, true, 0};
+    for (int k = 0; k < 6; ++k)
+        if ((st = launch_group(c.cls[k], c.cnt[k], dry, stream)) != QL_OK)
             return st;
-    }
-    // partition the non-empty layers by (fmt, xdt); each class is one launch
-    const ql_linear_ep *cls[6][QL_MAX_GROUP];
-    int cnt[6] = {0, 0, 0, 0, 0, 0};
-    for (int i = 0; i < n_lin; ++i) {
-        const ql_linear &l = lin[i].lin;
-        if (l.M == 0)
-            continue;
-        const int f = l.fmt == QL_FMT_Q4 ? 0 : l.fmt == QL_FMT_INT8 ? 1 : 2;
-        const int c = 2 * f + (l.xdt == QL_DT_BF16 ? 1 : 0);
-        cls[c][cnt[c]++] = &lin[i];
-    }
-    for (int c = 0; c < 6; ++c) {
-        const int st = launch_group(cls[c], cnt[c], stream);
-        if (st != QL_OK)
+    if (dry.need > SCRATCH_BYTES)
+        return QL_ERR_UNSUPPORTED;
+    for (int k = 0; k < 6; ++k) {
+        WsSource src{base, SCRATCH_BYTES, false, 0};
+        if ((st = launch_group(c.cls[k], c.cnt[k], src, stream)) != QL_OK)
             return st;
     }
     return QL_OK;

@@ -32,7 +32,7 @@ EXPORTS = [
     "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
     "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
     "qlinear_steer", "qlinear_attention", "qlinear_status_string",
-    "qlinear_force_path",
+    "qlinear_force_path", "qlinear_block_forward_ep_noalloc",
 ]
 
 PATH_AUTO, PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED, PATH_WIDE = range(6)
@@ -119,6 +119,8 @@ def load():
     lib.qlinear_forward_ep.restype = ci
     lib.qlinear_block_forward_ep.argtypes = [ctypes.POINTER(_LinearEp), ci, vp]
     lib.qlinear_block_forward_ep.restype = ci
+    lib.qlinear_block_forward_ep_noalloc.argtypes = [ctypes.POINTER(_LinearEp), ci, vp]
+    lib.qlinear_block_forward_ep_noalloc.restype = ci
     lib.qlinear_quantize_act.argtypes = [vp, ci, i64, i64, vp, vp, vp]
     lib.qlinear_quantize_act.restype = ci
     lib.qlinear_forward_w8a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp,
@@ -383,6 +385,16 @@ def block_forward_ep(entries, stream=None, group=None):
     scales, N, Y, bias, act, residual) tuples.  Asynchronous."""
     arr = group if group is not None else make_group_ep(entries)
     _check(load().qlinear_block_forward_ep(arr, len(arr), _stream(stream)))
+    return [e[5] for e in entries] if entries is not None else None
+
+
+def block_forward_ep_noalloc(entries, stream=None, group=None):
+    """block_forward_ep through the entry point that allocates nothing: its
+    workspace is the library's static scratch (96 MiB per device).  Calls
+    that may overlap on one device must be ordered by the caller.
+    Asynchronous."""
+    arr = group if group is not None else make_group_ep(entries)
+    _check(load().qlinear_block_forward_ep_noalloc(arr, len(arr), _stream(stream)))
     return [e[5] for e in entries] if entries is not None else None
 
 

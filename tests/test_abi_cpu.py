@@ -45,7 +45,7 @@ def test_header_declares_the_boundary():
         "qlinear_forward", "qlinear_block_forward", "qlinear_forward_ep",
         "qlinear_block_forward_ep", "qlinear_quantize_act", "qlinear_forward_w8a8",
         "qlinear_steer", "qlinear_attention", "qlinear_status_string",
-        "qlinear_force_path"])
+        "qlinear_force_path", "qlinear_block_forward_ep_noalloc"])
 
 
 def test_force_path_values(lib):
