@@ -323,14 +323,17 @@ def attention_bench(torch, ql, si, step):
 
 
 def dit_step(torch, ql, si, step):
-    """A sequential DiT denoising step in one HIP graph: per block, QKV
-    linear (+ bias -> bf16), attention (-> bf16), out projection added in
-    place into the fp32 residual stream, FFN-up (+ bias -> GELU -> bf16)
-    feeding FFN-down, added in place, with the steering injection at one
-    block (strength re-read at every replay).  The normalization before the
-    attention and the feed-forward is not built: FFN-up reads a fixed bf16
-    activation tensor in its place.  Same q4 weights as the step."""
-    import numpy as np
+    """A chained DiT denoising step in one HIP graph, the blocks feeding one
+    another through the residual stream: per block, QKV linear (+ bias ->
+    bf16) on the bf16 copy of the residual stream h, attention (-> bf16),
+    out projection (+ bias) added in place into h (fp32) with a bf16 copy of
+    h written by the same kernel, FFN-up (+ bias -> GELU -> bf16) on that
+    copy, FFN-down (+ bias) added in place into h with its bf16 copy (the
+    next block's input), and the steering injection at one block (strength
+    re-read at every replay).  The first block reads a fixed h0 (out of
+    place), so every replay computes the same step.  The block's
+    normalizations and modulation are not part of this library.  Same q4
+    weights as the step."""
     dev = torch.device("cuda")
     M, d = step.M, si.D_MODEL
     B, T, H = 2, M // 2, d // 64
@@ -340,7 +343,10 @@ def dit_step(torch, ql, si, step):
     qkv = torch.empty((M, 3 * d), dtype=torch.bfloat16, device=dev)
     att = torch.empty((M, d), dtype=torch.bfloat16, device=dev)
     up = torch.empty((M, 4 * d), dtype=torch.bfloat16, device=dev)
-    h = torch.zeros((M, d), dtype=torch.float32, device=dev)
+    h0 = torch.randn((M, d), device=dev, generator=g)
+    hb0 = h0.to(torch.bfloat16)  # input preparation, outside the graph
+    h = torch.empty((M, d), dtype=torch.float32, device=dev)
+    hb = torch.empty((M, d), dtype=torch.bfloat16, device=dev)
     direction = torch.randn(d, device=dev, generator=g)
     direction /= direction.norm()
     strength = torch.zeros(1, dtype=torch.float32, device=dev)
@@ -351,12 +357,12 @@ def dit_step(torch, ql, si, step):
         (f0, _, c0, s0, N0, _), (f1, _, c1, s1, N1, _), (f2, _, c2, s2, N2, _), \
             (f3, _, c3, s3, N3, _) = ents
         st = (direction, 30.0, strength) if blk == steer_block else None
+        x_in, h_prev = (hb0, h0) if blk == 0 else (hb, h)
         calls.append((
-            ql.make_group_ep([(f0, step.xa, c0, s0, N0, qkv, bias[0], ql.ACT_NONE, None)]),
-            ql.make_group_ep([(f1, att.view(torch.int16), c1, s1, N1, h, bias[1], ql.ACT_NONE, h)]),
-            ql.make_group_ep([(f2, step.xa, c2, s2, N2, up, bias[2], ql.ACT_GELU, None)]),
-            ql.make_group_ep([(f3, up.view(torch.int16), c3, s3, N3, h, bias[3], ql.ACT_NONE, h,
-                               st)]),
+            ql.make_group_ep([(f0, x_in, c0, s0, N0, qkv, bias[0], ql.ACT_NONE, None)]),
+            ql.make_group_ep([(f1, att, c1, s1, N1, h, bias[1], ql.ACT_NONE, h_prev, None, hb)]),
+            ql.make_group_ep([(f2, hb, c2, s2, N2, up, bias[2], ql.ACT_GELU, None)]),
+            ql.make_group_ep([(f3, up, c3, s3, N3, h, bias[3], ql.ACT_NONE, h, st, hb)]),
             bias))
     qv = qkv.view(torch.int16)
 
@@ -374,10 +380,11 @@ def dit_step(torch, ql, si, step):
     strength.zero_()
     lin_flops = step.flops
     att_flops = 4.0 * B * H * T * T * 64 * len(step.blocks)
-    return {"note": "24 sequential DiT blocks (QKV+bias->bf16, attention, out-proj+bias into the "
-                    "fp32 residual, FFN-up+bias->GELU->bf16, FFN-down+bias into the residual, "
-                    "steering at one block) captured as one HIP graph; the normalizations "
-                    "are not built (FFN-up reads a fixed bf16 tensor)",
+    return {"note": "24 chained DiT blocks (QKV+bias->bf16 on the bf16 copy of the residual "
+                    "stream, attention, out-proj+bias added in place into the fp32 residual with "
+                    "its bf16 copy, FFN-up+bias->GELU->bf16, FFN-down+bias into the residual "
+                    "with its bf16 copy, steering at one block) captured as one HIP graph; "
+                    "the block's normalizations are not part of the library",
             "ms_per_step": round(t0, 4), "ms_per_step_steering_on": round(t1, 4),
             "TFLOPs": round((lin_flops + att_flops) / (t0 * 1e-3) / 1e12, 1),
             "attention_flop_share": round(att_flops / (lin_flops + att_flops), 4)}

@@ -197,6 +197,12 @@ typedef struct {
     const float *steer_dir;
     float steer_norm;
     const float *steer_strength;  /* device fp32 scalar; required with steer_dir */
+    /* Optional bf16 copy of the output (fp32 Y only): y_bf16_copy[m][n] =
+     * Y[m][n] rounded to nearest even, bf16 bit patterns [M][N], 2-byte
+     * aligned (8-byte for the vector store paths), aliasing no other
+     * argument; NULL for none.  With Y the residual stream this is the next
+     * linear layer's bf16 input, written by the same kernel. */
+    uint16_t *y_bf16_copy;
 } ql_epilogue;
 
 /* qlinear_forward with an epilogue (ep == NULL: none, fp32 Y).  Y is fp32 or

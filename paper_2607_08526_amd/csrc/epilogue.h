@@ -11,8 +11,10 @@
 //
 // act the identity or the GELU in its exact (erf) form x * Phi(x) =
 // x * (1 + erf(x / sqrt 2)) / 2, then stored as fp32 or as bf16 (round to
-// nearest even, NaN kept quiet).  Elements are addressed by their flat
-// index idx = m * N + n and their column n.
+// nearest even, NaN kept quiet); an fp32 output may also be stored as a
+// bf16 copy (the next linear layer's input, when Y is a residual stream).
+// Elements are addressed by their flat index idx = m * N + n and their
+// column n.
 #pragma once
 
 #include "internal.h"
@@ -69,6 +71,8 @@ __device__ inline void epi_store(const Epilogue &e, float *Y, int64_t idx, int n
         reinterpret_cast<uint16_t *>(Y)[idx] = (uint16_t)epi_bf16(v);
     else
         Y[idx] = v;
+    if (e.ycopy)
+        e.ycopy[idx] = (uint16_t)epi_bf16(v);
 }
 
 // Whether four consecutive elements of a row (n % 4 == 0, n + 3 < N) can be
@@ -78,7 +82,29 @@ __host__ __device__ inline bool epi_vec_ok(const Epilogue &e, const float *Y, in
 {
     return (N & 3) == 0 && ((uintptr_t)Y & (e.ybf16 ? 7 : 15)) == 0 &&
            ((uintptr_t)e.bias & 15) == 0 && ((uintptr_t)e.resid & 15) == 0 &&
-           ((uintptr_t)e.steer & 15) == 0;
+           ((uintptr_t)e.steer & 15) == 0 && ((uintptr_t)e.ycopy & 7) == 0;
+}
+
+// bf16 bit patterns of four fp32 values, packed in two words
+typedef uint32_t epi_u32x2 __attribute__((ext_vector_type(2)));
+template <typename V4>
+__device__ inline epi_u32x2 epi_bf16x4(V4 v)
+{
+    return epi_u32x2{epi_bf16(v[0]) | (epi_bf16(v[1]) << 16),
+                     epi_bf16(v[2]) | (epi_bf16(v[3]) << 16)};
+}
+
+// the bf16 copy of four finished fp32 elements idx .. idx + 3 (a no-op
+// without a copy)
+__device__ inline void epi_copy4(const Epilogue &e, int64_t idx, epi_u32x2 b, bool nt)
+{
+    if (e.ycopy) {
+        epi_u32x2 *dst = reinterpret_cast<epi_u32x2 *>(e.ycopy + idx);
+        if (nt)
+            __builtin_nontemporal_store(b, dst);
+        else
+            *dst = b;
+    }
 }
 
 // the steering term of four consecutive columns n .. n + 3 (zero, and not
@@ -190,7 +216,10 @@ __device__ inline void epi_store4(const Epilogue &e, float *Y, int64_t idx, int 
         r4 = *reinterpret_cast<const V4 *>(e.resid + idx);
     float alpha;
     const V4 s4 = epi_steer4<V4>(e, n, alpha);
-    epi_put4(e, Y, idx, epi_apply4(e, v, b4, r4, s4, alpha), nt);
+    const V4 y = epi_apply4(e, v, b4, r4, s4, alpha);
+    epi_put4(e, Y, idx, y, nt);
+    if (e.ycopy)
+        epi_copy4(e, idx, epi_bf16x4(y), nt);
 }
 
 }  // namespace qlk

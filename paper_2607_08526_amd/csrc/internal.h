@@ -11,7 +11,8 @@ namespace qlk {
 
 // A layer's epilogue as the kernels see it (see epilogue.h): Y[m][n] =
 // act(P + bias[n]) + resid[m][n] (+ alpha * hnorm * steer[n] when
-// alpha = *strength is not 0), stored as fp32 or (ybf16) bf16.
+// alpha = *strength is not 0), stored as fp32 or (ybf16) bf16, and with
+// ycopy also as bf16 into ycopy[m][n] (fp32 Y only).
 struct Epilogue {
     const float *bias;      // [N] or nullptr
     const float *resid;     // [M][N] or nullptr
@@ -20,12 +21,13 @@ struct Epilogue {
     float hnorm;            // the layer's mean residual norm
     int act;                // QL_ACT_NONE / QL_ACT_GELU
     int ybf16;              // Y holds bf16 bit patterns
+    uint16_t *ycopy;        // bf16 copy of Y [M][N] or nullptr
 };
 
 // an epilogue beyond the plain fp32 store
 __host__ __device__ inline bool epi_active(const Epilogue &e)
 {
-    return e.bias || e.resid || e.steer || e.act || e.ybf16;
+    return e.bias || e.resid || e.steer || e.act || e.ybf16 || e.ycopy;
 }
 
 // Activations and packed codes of one linear layer as the kernels see it.

@@ -654,16 +654,23 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         // read them, so reusing them for the next row's patch read would
         // wait out each store's whole latency
         f32x4 w[4];
+        epi_u32x2 cp[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t)
             w[t] = *reinterpret_cast<const f32x4 *>(patch + (8 * t + (lane >> 3)) * 32 + 4 * cq);
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-            w[t] = epi_pack4(d.ep, epi_apply4(d.ep, w[t], b4, r[t], s4, alpha));
+        for (int t = 0; t < 4; ++t) {
+            const f32x4 y = epi_apply4(d.ep, w[t], b4, r[t], s4, alpha);
+            if (d.ep.ycopy)
+                cp[t] = epi_bf16x4(y);
+            w[t] = epi_pack4(d.ep, y);
+        }
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-            if (col_ok && mb + 8 * t < M)
+            if (col_ok && mb + 8 * t < M) {
                 epi_store_packed4(d.ep, d.Y, (int64_t)(mb + 8 * t) * N + n, w[t], true);
+                epi_copy4(d.ep, (int64_t)(mb + 8 * t) * N + n, cp[t], true);
+            }
     };
 
     if (S > 1 && d.cnt) {

@@ -45,7 +45,8 @@ int check_linear(int fmt, const void *X, int xdt, int64_t M, int64_t K, const vo
     return QL_OK;
 }
 
-const ql_epilogue NO_EPILOGUE = {nullptr, QL_ACT_NONE, nullptr, QL_DT_F32, nullptr, 0.0f, nullptr};
+const ql_epilogue NO_EPILOGUE = {nullptr, QL_ACT_NONE, nullptr, QL_DT_F32, nullptr, 0.0f, nullptr,
+                                 nullptr};
 
 // an epilogue's enums, aliasing and alignment (before check_linear, which
 // takes its ydt)
@@ -59,7 +60,11 @@ int check_epilogue(const ql_epilogue &ep, const void *Y)
         return QL_ERR_INVALID;
     if (ep.steer_dir && !ep.steer_strength)
         return QL_ERR_INVALID;
-    if (!aligned(ep.bias, 4) || !aligned(ep.residual, 4) ||
+    // the bf16 copy is of an fp32 output, and is an output of its own
+    if (ep.y_bf16_copy && (ep.ydt != QL_DT_F32 || (const void *)ep.y_bf16_copy == Y ||
+                           (const void *)ep.y_bf16_copy == ep.residual))
+        return QL_ERR_INVALID;
+    if (!aligned(ep.bias, 4) || !aligned(ep.residual, 4) || !aligned(ep.y_bf16_copy, 2) ||
         (ep.steer_dir && (!aligned(ep.steer_dir, 4) || !aligned(ep.steer_strength, 4))))
         return QL_ERR_ALIGN;
     return QL_OK;
@@ -82,7 +87,8 @@ Epilogue to_epilogue(const ql_epilogue &e)
                     e.steer_dir ? e.steer_strength : nullptr,
                     e.steer_norm,
                     e.act,
-                    e.ydt == QL_DT_BF16 ? 1 : 0};
+                    e.ydt == QL_DT_BF16 ? 1 : 0,
+                    e.y_bf16_copy};
 }
 
 // Stream-ordered pool (one per device) that the per-stream workspaces below

@@ -67,6 +67,7 @@ class _Epilogue(ctypes.Structure):
         ("steer_dir", ctypes.c_void_p),
         ("steer_norm", ctypes.c_float),
         ("steer_strength", ctypes.c_void_p),
+        ("y_bf16_copy", ctypes.c_void_p),
     ]
 
 
@@ -223,6 +224,14 @@ def _require_ep(bias, residual, M, N):
         _require(residual, "residual", (torch.float32,), (M, N))
 
 
+def _require_ycopy(ycopy, Y, M, N):
+    if ycopy is None:
+        return
+    _require(ycopy, "ycopy", _BF16_BITS, (M, N))
+    if Y.dtype != torch.float32:
+        raise ValueError("a bf16 copy is taken of an fp32 output only")
+
+
 def _require_steer(steer, N):
     if steer is None:
         return
@@ -299,25 +308,26 @@ def _ydt(Y):
     raise TypeError(f"outputs must be float32 or bfloat16, not {Y.dtype}")
 
 
-def _epilogue(Y, bias, act, residual, steer=None):
+def _epilogue(Y, bias, act, residual, steer=None, ycopy=None):
     """steer: None, or (direction fp32 [N], hnorm float, strength: a device
-    fp32 tensor of one element, re-read by every launch)."""
+    fp32 tensor of one element, re-read by every launch); ycopy: None, or a
+    bf16 [M][N] tensor that receives a bf16 copy of the (fp32) output."""
     if steer is None:
-        return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y), None, 0.0, None)
+        return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y), None, 0.0, None, _ptr(ycopy))
     d, hnorm, strength = steer
     return _Epilogue(_ptr(bias), act, _ptr(residual), _ydt(Y), _ptr(d), float(hnorm),
-                     _ptr(strength))
+                     _ptr(strength), _ptr(ycopy))
 
 
 def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residual=None,
-               ydtype=torch.float32, steer=None, stream=None):
+               ydtype=torch.float32, steer=None, stream=None, ycopy=None):
     """forward() with the layer epilogue fused into the output store:
     Y = act(X . W^T + bias) + residual (+ alpha * hnorm * d), Y fp32 or bf16
     (ydtype, or Y's dtype when Y is given).  bias fp32 [N], residual fp32
     [M][N] (may be Y itself for fp32 Y), each optional; steer = (d fp32 [N],
     hnorm, strength) adds the steering term with alpha = strength[0] read on
-    the device by the launch (skipped exactly when alpha is 0).
-    Asynchronous."""
+    the device by the launch (skipped exactly when alpha is 0); ycopy (bf16
+    [M][N]) receives a bf16 copy of an fp32 Y.  Asynchronous."""
     M, K = _require_x(X)
     _require_weights(fmt, codes, scales, N, K)
     if Y is None:
@@ -325,8 +335,9 @@ def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residu
     _require_y(Y, M, N, (torch.float32, torch.bfloat16))
     _require_ep(bias, residual, M, N)
     _require_steer(steer, N)
-    ep = _epilogue(Y, bias, act, residual, steer)
-    _on_device(X, codes, scales, Y, bias, residual, *(steer[::2] if steer else ()))
+    _require_ycopy(ycopy, Y, M, N)
+    ep = _epilogue(Y, bias, act, residual, steer, ycopy)
+    _on_device(X, codes, scales, Y, bias, residual, ycopy, *(steer[::2] if steer else ()))
     _check(load().qlinear_forward_ep(fmt, _ptr(X), _xdt(X), M, K, _ptr(codes), _ptr(scales), N,
                                      _ptr(Y), ctypes.byref(ep), _stream(stream)))
     return Y
@@ -359,24 +370,26 @@ def block_forward(entries, stream=None, group=None):
 
 def make_group_ep(entries):
     """ctypes array for block_forward_ep from (fmt, X, codes, scales, N, Y,
-    bias, act, residual[, steer]) tuples (bias/residual/steer None for none;
-    Y fp32 or bf16).  The tensors must outlive every use of the returned
-    array."""
+    bias, act, residual[, steer[, ycopy]]) tuples (bias/residual/steer/ycopy
+    None for none; Y fp32 or bf16; ycopy a bf16 [M][N] copy of an fp32 Y).
+    The tensors must outlive every use of the returned array."""
     if not 1 <= len(entries) <= MAX_GROUP:
         raise ValueError(f"a group holds 1 to {MAX_GROUP} linears, not {len(entries)}")
     arr = (_LinearEp * len(entries))()
     for i, e in enumerate(entries):
         fmt, X, codes, scales, N, Y, bias, act, residual = e[:9]
         steer = e[9] if len(e) > 9 else None
+        ycopy = e[10] if len(e) > 10 else None
         M, K = _require_x(X)
         _require_weights(fmt, codes, scales, N, K)
         _require_y(Y, M, N, (torch.float32, torch.bfloat16))
         _require_ep(bias, residual, M, N)
         _require_steer(steer, N)
-        _on_device(X, codes, scales, Y, bias, residual, *(steer[::2] if steer else ()))
+        _require_ycopy(ycopy, Y, M, N)
+        _on_device(X, codes, scales, Y, bias, residual, ycopy, *(steer[::2] if steer else ()))
         lin = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                       scales.data_ptr() if scales is not None else 0, Y.data_ptr())
-        arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual, steer))
+        arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual, steer, ycopy))
     return arr
 
 

@@ -15,7 +15,7 @@ HIP_INCLUDE = "/opt/rocm/include"
 STRUCTS = {
     "ql_linear": ["fmt", "X", "xdt", "M", "K", "N", "codes", "scales", "Y"],
     "ql_epilogue": ["bias", "act", "residual", "ydt", "steer_dir", "steer_norm",
-                    "steer_strength"],
+                    "steer_strength", "y_bf16_copy"],
     "ql_linear_ep": ["lin", "ep"],
 }
 

@@ -257,3 +257,37 @@ def test_block_forward_ep_routed_layers(gpu, orc):
         torch.cuda.synchronize()
         for e, (P, Yr, bias) in zip(entries, refs):
             check(host_y(torch, e[5]), P, Yr, bias, O.DT_BF16, False, (fmt, e[4]))
+
+
+@pytest.mark.parametrize("fmt,xdt,M,N,K", PATHS)
+def test_epilogue_bf16_copy_every_path(gpu, orc, fmt, xdt, M, N, K):
+    """The bf16 copy of an fp32 output (the residual stream's copy that the
+    next linear reads), on every store path: an in-place residual add with
+    bias and the copy; the fp32 output within the epilogue bound, and the
+    copy equal to the round-to-nearest-even bf16 of the fp32 output, bit for
+    bit (NaN-filled beforehand, so every element is written).  A copy of a
+    bf16 output, or one aliasing Y or the residual, is refused."""
+    torch, ql = gpu
+    W, X = si.small_case(3500 + M + N + K + fmt, M, N, K, xdt)
+    cd, sd = ql.quantize(fmt, dev_f32(torch, W))
+    cr, sr = orc.quantize(fmt, W)
+    Pr = orc.forward(fmt, X, xdt, cr, sr, N)
+    rng = np.random.default_rng(3600 + M + N)
+    bias = (rng.standard_normal(N) * 0.5).astype(np.float32)
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    Xd = dev_x(torch, X, xdt)
+    Y = dev_f32(torch, resid)
+    copy = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    ql.forward_ep(fmt, Xd, cd, sd, N, Y=Y, bias=dev_f32(torch, bias), residual=Y, ycopy=copy)
+    torch.cuda.synchronize()
+    Yg = host_y(torch, Y)
+    check(Yg, Pr, orc.epilogue(Pr, bias, O.ACT_NONE, resid), bias, xdt, False, (M, N, K))
+    want = si.f32_to_bf16_bits(Yg.astype(np.float32))
+    assert np.array_equal(copy.view(torch.int16).cpu().numpy().view(np.uint16), want)
+    Yb = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):  # a copy of a bf16 output
+        ql.forward_ep(fmt, Xd, cd, sd, N, Y=Yb, ycopy=copy)
+    alias = Y.view(-1).view(torch.bfloat16)[:M * N].view(M, N)  # same address as Y
+    with pytest.raises(ql.QLinearError) as err:
+        ql.forward_ep(fmt, Xd, cd, sd, N, Y=Y, residual=Y, ycopy=alias)
+    assert err.value.status == 1
