@@ -520,6 +520,56 @@ def skinny_sweep(torch, ql, si):
     return out
 
 
+def block_few_rows(torch, ql, si):
+    """One d = 2048 block's four linears (the int8 block workload's weights,
+    quantized as int8 and as q4) at M in {1, 8, 32}: the grouped call (one
+    launch streams all four matrices) against the four layers called one by
+    one, each as a HIP graph over R copies of the weights (R x footprint >=
+    512 MB, past the last-level cache)."""
+    import numpy as np
+    dev = torch.device("cuda")
+    out = []
+    Ws = [si.block_int8_weight(i) for i in range(4)]
+    for fmt in (ql.FMT_INT8, ql.FMT_Q4):
+        q = [ql.quantize(fmt, torch.from_numpy(W).to(dev)) for W in Ws]
+        wbytes = sum(c.numel() + 2 * s_.numel() for c, s_ in q)
+        R = max(1, -(-ROT_BYTES // wbytes))
+        copies = [q] + [[(c.clone(), s_.clone()) for c, s_ in q] for _ in range(R - 1)]
+        for M in (1, 8, 32):
+            rng = np.random.default_rng(500 + M)
+            xa = torch.from_numpy(si.activations(rng, M, 2048, si.DT_BF16).view("int16")).to(dev)
+            xb = torch.from_numpy(si.activations(rng, M, 8192, si.DT_BF16).view("int16")).to(dev)
+            Ys = [torch.empty((M, W.shape[0]), dtype=torch.float32, device=dev) for W in Ws]
+            groups, singles = [], []
+            for qq in copies:
+                ents = [(fmt, xb if W.shape[1] == 8192 else xa, c, s_, W.shape[0], Y)
+                        for (c, s_), W, Y in zip(qq, Ws, Ys)]
+                groups.append(ql.make_group(ents))
+                singles.append([ql.make_group([e]) for e in ents])
+
+            def grouped():
+                for g in groups:
+                    ql.block_forward(None, group=g)
+
+            def one_by_one():
+                for gs in singles:
+                    for g in gs:
+                        ql.block_forward(None, group=g)
+
+            tg = graph_time(torch, grouped)[0] / R * 1e-3
+            ts = graph_time(torch, one_by_one)[0] / R * 1e-3
+            algo = wbytes + M * (2048 * 3 + 8192) * 2 + 4 * M * sum(W.shape[0] for W in Ws)
+            out.append({"fmt": "int8" if fmt == ql.FMT_INT8 else "q4", "d": 2048, "M": M,
+                        "us_grouped": round(tg * 1e6, 2), "us_per_layer_calls": round(ts * 1e6, 2),
+                        "weight_GBps": round(wbytes / tg / 1e9, 1),
+                        "hbm_frac": round(algo / tg / 1e9 / HBM_PEAK_GBPS, 4),
+                        "weight_MB": round(wbytes / 1e6, 2), "copies": R})
+            log(f"block_few_rows {out[-1]}")
+        del copies, groups, singles
+        torch.cuda.empty_cache()
+    return out
+
+
 def block_int8(torch, ql, si):
     dev = torch.device("cuda")
     xa, xb = si.block_activations()
@@ -724,6 +774,7 @@ def main():
 
     if args.sweeps_only:
         print(json.dumps({"skinny": skinny_sweep(torch, ql, si),
+                          "block_few_rows": block_few_rows(torch, ql, si),
                           "block_int8": block_int8(torch, ql, si),
                           "block_w8a8": block_w8a8(torch, ql, si),
                           "paper_widths": paper_widths(torch, ql, si)}), flush=True)
@@ -793,6 +844,7 @@ def main():
     res["dit_step"] = dit_step(torch, ql, si, step)
     if not args.no_sweeps:
         res["skinny"] = skinny_sweep(torch, ql, si)
+        res["block_few_rows"] = block_few_rows(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)
         res["block_w8a8"] = block_w8a8(torch, ql, si)
         res["paper_widths"] = paper_widths(torch, ql, si)

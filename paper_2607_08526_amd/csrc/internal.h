@@ -169,20 +169,33 @@ hipError_t launch_qgemm_skinny(int fmt, const LinDesc &d, hipStream_t stream);
 // Wavefront-reduction GEMV for M <= 4 (bf16 activations): codes and scales
 // in registers, activations staged in LDS; gemv_ok() states its shape limits.
 bool gemv_ok(const LinDesc &d);
-hipError_t launch_qgemv(int fmt, const LinDesc &d, hipStream_t stream);
 
 int stream_max_m();
 // longest reduction the streaming kernel takes: its per-lane 32-bit load
 // offsets span up to 64 weight rows (64 K bytes) and 32 activation rows
 int stream_max_k();
 // mx: activation rows staged (4, 8, 16, 32); rw: weight rows per workgroup;
-// kw: wavefronts per workgroup; S, psteps: K parts of psteps 32-blocks each
-// (S > 1: LinDesc::part receives plain partial outputs [S][M][N])
+// kw: wavefronts per workgroup (common to a group); S: the largest layer's
+// K parts, psteps: the common part length in 32-blocks.  Per layer the
+// LinDesc carries ksplit and psteps (ksplit > 1: LinDesc::part receives
+// plain partial outputs [ksplit][M][N]).
 struct StreamPlan {
     int mx, rw, kw, S, psteps;
 };
-StreamPlan stream_plan(int fmt, const LinDesc &d, int cus);
-hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LinDesc &d,
+// the plan of a group of n layers (one format, one M); S[i], psteps[i]
+// receive each layer's parts and part length
+StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *psteps);
+// n layers of one format in one launch of a few-row kernel: layer i on the
+// workgroups begin[i] .. begin[i + 1] - 1 (streaming kernel: ceil(N / rw) *
+// ksplit of them; GEMV: ceil(N / rows per workgroup))
+struct LayerGroup {
+    LinDesc d[QL_MAX_GROUP];
+    int begin[QL_MAX_GROUP + 1];
+    int n;
+};
+// The GEMV over a group of layers with one row count M (gemv_ok for each).
+hipError_t launch_qgemv(int fmt, const LayerGroup &g, hipStream_t stream);
+hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LayerGroup &g,
                                hipStream_t stream);
 
 }  // namespace qlk

@@ -33,6 +33,13 @@
 // second MFMA against a constant -OFF matrix fed in as the C operand; the
 // block's fp16 scale is then applied to the fp32 partial.
 //
+// Grouping.  One launch takes up to QL_MAX_GROUP layers of one format and
+// row count (a DiT block's four linears): layer i owns the workgroups
+// begin[i] .. begin[i + 1] - 1 of the grid, each layer with its own K parts;
+// the template shape (rows per workgroup, wavefronts, activation stage) is
+// common to the group.  All of a block's weights then stream in one launch,
+// and its split layers share one sum launch.
+//
 // Requirements (checked by the host): K % 256 == 0, 16-byte aligned codes,
 // scales and X.
 #include <algorithm>
@@ -141,8 +148,12 @@ __device__ inline int cswz(int j, int p)
     return FMT == QL_FMT_INT8 ? (p ^ ((j >> 1) & 7)) : (p ^ ((j >> 2) & 3));
 }
 
+// The kernel body for workgroup wg of layer d (the single-layer and the
+// grouped kernel below differ only in how they find d: a single layer's
+// descriptor is the whole kernel argument, so its fields load at once; a
+// group's layer is looked up first)
 template <int FMT, int RW, int MX, int KW>
-__global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
+__device__ __forceinline__ void stream_body(const LinDesc &d, const int wg)
 {
     using G = SGeo<FMT, RW, MX>;
     __shared__ __align__(16) uint8_t lds[KW * G::WAVE];
@@ -152,8 +163,8 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
     const int M = d.M, N = d.N, K = d.K, nb = K >> 5;
     // consecutive workgroups take the parts of one row group: with the
     // round-robin XCD dispatch, part p's activation range stays on few XCDs
-    const int S = d.ksplit, part = (int)blockIdx.x % S;
-    const int n0 = (int)blockIdx.x / S * RW;
+    const int S = d.ksplit, part = wg % S;
+    const int n0 = wg / S * RW;
     const int crow_bytes = FMT == QL_FMT_INT8 ? K : K / 2;
 
     uint8_t *const ring = lds + wave * G::WAVE;
@@ -335,48 +346,69 @@ __global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
 }
 
 template <int FMT, int RW, int MX, int KW>
-hipError_t launch_kw(const LinDesc &d, hipStream_t s)
+__global__ __launch_bounds__(64 * KW) void qgemm_stream_kernel(const LinDesc d)
+{
+    stream_body<FMT, RW, MX, KW>(d, (int)blockIdx.x);
+}
+
+template <int FMT, int RW, int MX, int KW>
+__global__ __launch_bounds__(64 * KW) void qgemm_stream_group_kernel(const LayerGroup grp)
+{
+    // this workgroup's layer (wave-uniform) and its index within the layer
+    int li = 0;
+    while (li + 1 < grp.n && (int)blockIdx.x >= grp.begin[li + 1])
+        ++li;
+    stream_body<FMT, RW, MX, KW>(grp.d[li], (int)blockIdx.x - grp.begin[li]);
+}
+
+template <int FMT, int RW, int MX, int KW>
+hipError_t launch_kw(const LayerGroup &g, hipStream_t s)
 {
     if constexpr (KW * SGeo<FMT, RW, MX>::WAVE > 160 * 1024) {
         return hipErrorInvalidValue;  // does not fit the LDS; never chosen
     } else {
-        const dim3 grid((unsigned)((d.N + RW - 1) / RW * d.ksplit));
-        hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, KW>), grid, dim3(64 * KW), 0, s, d);
+        const dim3 grid((unsigned)g.begin[g.n]);
+        if (g.n == 1)
+            hipLaunchKernelGGL((qgemm_stream_kernel<FMT, RW, MX, KW>), grid, dim3(64 * KW), 0, s,
+                               g.d[0]);
+        else
+            hipLaunchKernelGGL((qgemm_stream_group_kernel<FMT, RW, MX, KW>), grid, dim3(64 * KW),
+                               0, s, g);
         return hipGetLastError();
     }
 }
 
 template <int FMT, int RW, int MX>
-hipError_t launch_rw(int kw, const LinDesc &d, hipStream_t s)
+hipError_t launch_rw(int kw, const LayerGroup &g, hipStream_t s)
 {
     switch (kw) {
-    case 2: return launch_kw<FMT, RW, MX, 2>(d, s);
-    case 4: return launch_kw<FMT, RW, MX, 4>(d, s);
-    case 8: return launch_kw<FMT, RW, MX, 8>(d, s);
+    case 2: return launch_kw<FMT, RW, MX, 2>(g, s);
+    case 4: return launch_kw<FMT, RW, MX, 4>(g, s);
+    case 8: return launch_kw<FMT, RW, MX, 8>(g, s);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <int FMT, int MX>
-hipError_t launch_mx(int rw, int kw, const LinDesc &d, hipStream_t s)
+hipError_t launch_mx(int rw, int kw, const LayerGroup &g, hipStream_t s)
 {
     switch (rw) {
-    case 8: return launch_rw<FMT, 8, MX>(kw, d, s);
-    case 16: return launch_rw<FMT, 16, MX>(kw, d, s);
-    case 32: return launch_rw<FMT, 32, MX>(kw, d, s);
-    case 64: return launch_rw<FMT, 64, MX>(kw, d, s);
+    case 8: return launch_rw<FMT, 8, MX>(kw, g, s);
+    case 16: return launch_rw<FMT, 16, MX>(kw, g, s);
+    case 32: return launch_rw<FMT, 32, MX>(kw, g, s);
+    case 64: return launch_rw<FMT, 64, MX>(kw, g, s);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <int FMT>
-hipError_t launch_fmt(const StreamPlan &p, const LinDesc &d, hipStream_t s)
+hipError_t launch_fmt(const StreamPlan &p, const LayerGroup &g, hipStream_t s)
 {
     switch (p.mx) {
-    case 4: return launch_mx<FMT, 4>(p.rw, p.kw, d, s);
-    case 8: return launch_mx<FMT, 8>(p.rw, p.kw, d, s);
-    case 16: return launch_mx<FMT, 16>(p.rw, p.kw, d, s);
-    case 32: return launch_mx<FMT, 32>(p.rw, p.kw, d, s);
+    case 4: return launch_mx<FMT, 4>(p.rw, p.kw, g, s);
+    case 8: return launch_mx<FMT, 8>(p.rw, p.kw, g, s);
+    case 16: return launch_mx<FMT, 16>(p.rw, p.kw, g, s);
+    case 32: return launch_mx<FMT, 32>(p.rw, p.kw, g, s);
     default: return hipErrorInvalidValue;
     }
 }
@@ -412,23 +444,37 @@ int stream_geo(int fmt, int mx, int rw, int &stage, int &ring)
 int stream_max_m() { return 32; }
 int stream_max_k() { return 1 << 24; }
 
-// Choice of rows per workgroup, wavefronts and K parts.  Each wavefront
-// keeps R - 1 chunks of loads in flight, so a workgroup streams its bytes
-// (activations MX * Kp * 2, codes RW * Kp * cb for its part's Kp) in about
-// bytes / (KW (R - 1) STAGE) memory round trips; the launch takes as many
-// workgroup rounds as the grid needs over the CUs, and a split adds the
-// partial round trip and the sum launch.  The plan minimizes that estimate.
-StreamPlan stream_plan(int fmt, const LinDesc &d, int cus)
+// Choice of rows per workgroup, wavefronts and K parts for a group of
+// layers (one format, one row count M).  Each wavefront keeps R - 1 chunks
+// of loads in flight, so a workgroup streams its bytes (activations
+// MX * Kp * 2, codes RW * Kp * cb for its part's Kp) in about
+// bytes / (KW (R - 1) STAGE) memory round trips.  Every layer is cut into
+// parts of about one common length (so that its workgroups take about as
+// long as the others'); the launch takes as many workgroup rounds as the
+// grid needs over the CUs, and a split adds the partial round trip and the
+// sum launch.  The plan minimizes that estimate over the rows per
+// workgroup, the wavefronts and the part length.
+StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *psteps)
 {
     constexpr double RT = 2.0;           // us per memory round trip under load
     constexpr double SUM_LAUNCH = 3.0;   // us: split_sum launch and its gap
     constexpr double SUM_RATE = 4.0e6;   // bytes per us the sum launch moves
     constexpr double PART_COST = 0.3;    // us per part (fitted to a sweep of configurations)
-    const int mx = d.M <= 4 ? 4 : d.M <= 8 ? 8 : d.M <= 16 ? 16 : 32;
-    const int nb = d.K / 32;
+    constexpr int MAXS = 16;
+    int M = 0, nbmax = 0;
+    for (int i = 0; i < n; ++i) {
+        M = std::max(M, ds[i].M);
+        nbmax = std::max(nbmax, ds[i].K / 32);
+    }
+    const int mx = M <= 4 ? 4 : M <= 8 ? 8 : M <= 16 ? 16 : 32;
     const double cb = fmt == QL_FMT_INT8 ? 1.0 : 0.5;
-    StreamPlan best{mx, 16, 4, 1, nb};
+    StreamPlan best{mx, 16, 4, 1, nbmax};
     double best_t = 1e30;
+    int bS[QL_MAX_GROUP], bP[QL_MAX_GROUP];
+    for (int i = 0; i < n; ++i) {
+        bS[i] = 1;
+        bP[i] = ds[i].K / 32;
+    }
     for (int rw : {8, 16, 32, 64}) {
         int stage = 0, ring = 0;
         const int wave = stream_geo(fmt, mx, rw, stage, ring);
@@ -436,35 +482,60 @@ StreamPlan stream_plan(int fmt, const LinDesc &d, int cus)
             if (kw * wave > 160 * 1024)
                 continue;
             const int per_cu = std::min(160 * 1024 / (kw * wave), 2048 / (64 * kw));
-            for (int S : {1, 2, 4, 8, 16}) {
-                // parts of whole 8-block groups, at least 8 blocks per wavefront
-                const int pb = ((nb + S - 1) / S + 7) & ~7;
-                const int Se = (nb + pb - 1) / pb;
-                if (Se != S || pb < 8 * kw)
+            // part lengths (blocks): whole 8-block groups, >= 8 per
+            // wavefront, doubling up to the longest layer's whole K
+            int lens[16], nl = 0;
+            for (int L = 8 * kw; L < nbmax && nl < 15; L *= 2)
+                lens[nl++] = L;
+            lens[nl++] = (nbmax + 7) & ~7;
+            for (int li = 0; li < nl; ++li) {
+                const int L = lens[li];
+                int Si[QL_MAX_GROUP], Pi[QL_MAX_GROUP], Smax = 1;
+                int64_t wgs = 0;
+                double sum_bytes = 0.0, trips_max = 0.0;
+                bool ok = true;
+                for (int i = 0; i < n && ok; ++i) {
+                    const int nb = ds[i].K / 32;
+                    int S = std::max(1, std::min(MAXS, (nb + L - 1) / L));
+                    const int pb = ((nb + S - 1) / S + 7) & ~7;
+                    S = (nb + pb - 1) / pb;
+                    if (pb < 8 * kw)
+                        ok = false;
+                    Si[i] = S;
+                    Pi[i] = pb;
+                    Smax = std::max(Smax, S);
+                    wgs += (int64_t)((ds[i].N + rw - 1) / rw) * S;
+                    const double bytes = (double)pb * 32 * (mx * 2 + rw * cb);
+                    trips_max = std::max(trips_max,
+                                         std::ceil(bytes / ((double)kw * (ring - 1) * stage)) + 1);
+                    if (S > 1)
+                        sum_bytes += (double)(S + 1) * ds[i].M * ds[i].N * 4;
+                }
+                if (!ok)
                     continue;
-                const int64_t wgs = (int64_t)((d.N + rw - 1) / rw) * S;
-                const double bytes = (double)pb * 32 * (mx * 2 + rw * cb);
-                const double trips = std::ceil(bytes / ((double)kw * (ring - 1) * stage)) + 1;
                 const double rounds = std::ceil((double)wgs / ((double)cus * per_cu));
-                double t = rounds * trips * RT;
-                if (S > 1)
-                    t += RT + SUM_LAUNCH + (double)(S + 1) * d.M * d.N * 4 / SUM_RATE +
-                         PART_COST * S;
+                double t = rounds * trips_max * RT;
+                if (Smax > 1)
+                    t += RT + SUM_LAUNCH + sum_bytes / SUM_RATE + PART_COST * Smax;
                 if (t < best_t * 0.97) {
                     best_t = t;
-                    best = StreamPlan{mx, rw, kw, S, pb};
+                    best = StreamPlan{mx, rw, kw, Smax, L};
+                    std::copy(Si, Si + n, bS);
+                    std::copy(Pi, Pi + n, bP);
                 }
             }
         }
     }
+    std::copy(bS, bS + n, S);
+    std::copy(bP, bP + n, psteps);
     return best;
 }
 
-hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LinDesc &d,
+hipError_t launch_qgemm_stream(int fmt, const StreamPlan &p, const LayerGroup &g,
                                hipStream_t stream)
 {
-    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(p, d, stream)
-                              : launch_fmt<QL_FMT_Q4>(p, d, stream);
+    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(p, g, stream)
+                              : launch_fmt<QL_FMT_Q4>(p, g, stream);
 }
 
 }  // namespace qlk

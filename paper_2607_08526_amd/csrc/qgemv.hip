@@ -18,8 +18,17 @@
 // with one fp32 FMA; the lane partials are then summed across the wavefront
 // by DPP steps in a fixed order (deterministic).
 //
+// Grouping.  One launch takes up to QL_MAX_GROUP layers of one format and
+// one row count (a DiT block's four linears): layer i owns the workgroups
+// begin[i] .. begin[i + 1] - 1.  The blocks per lane (a template bound) are
+// those of the longest K.  A layer with fewer blocks still issues every
+// load, so that they all go out at once: its lanes past the row's end all
+// load the row's last block (one line per wavefront) and skip it.
+//
 // Requirements (checked by the host): M <= 4, K % 256 == 0, M * K <= 32768
 // (the activation stage fits LDS), 16-byte aligned codes and X.
+#include <algorithm>
+
 #include "epilogue.h"
 #include "internal.h"
 
@@ -111,16 +120,19 @@ __device__ inline float wave_sum(float v)
     return v;
 }
 
+// The kernel body for workgroup wg of layer d (see the single-layer and
+// grouped kernels below)
 template <int FMT, int MM, int RPW, int BPL>
-__global__ __launch_bounds__(64 * WAVES) void qgemv_kernel(const LinDesc d)
+__device__ __forceinline__ void gemv_body(const LinDesc &d, const int wg)
 {
     // dynamic LDS, sized at launch (M K bf16, then q4's M K / 32 fp32 block
-    // sums) so that small activations leave room for many workgroups per CU
+    // sums, for the group's largest K) so that small activations leave room
+    // for many workgroups per CU
     extern __shared__ __align__(16) uint16_t xs[];
     float *const xsum = reinterpret_cast<float *>(xs + d.M * d.K);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int N = d.N, K = d.K, nb = K >> 5;
-    const int n0 = ((int)blockIdx.x * WAVES + wave) * RPW;
+    const int n0 = (wg * WAVES + wave) * RPW;
     constexpr int CB = FMT == QL_FMT_INT8 ? 32 : 16;  // code bytes per block
     const int crow = FMT == QL_FMT_INT8 ? K : K / 2;
 
@@ -227,33 +239,73 @@ __global__ __launch_bounds__(64 * WAVES) void qgemv_kernel(const LinDesc d)
                     epi_store(d.ep, d.Y, (int64_t)m * N + n0 + r, n0 + r, acc[r][m]);
 }
 
-template <int FMT, int MM, int RPW>
-hipError_t launch_bpl(const LinDesc &d, hipStream_t s)
+template <int FMT, int MM, int RPW, int BPL>
+__global__ __launch_bounds__(64 * WAVES) void qgemv_kernel(const LinDesc d)
 {
-    const int nb = d.K / 32, bpl = (nb + 63) / 64;
-    const dim3 grid((unsigned)((d.N + WAVES * RPW - 1) / (WAVES * RPW))), block(64 * WAVES);
-    const size_t lds = (size_t)d.M * d.K * 2 + (FMT == QL_FMT_Q4 ? (size_t)d.M * nb * 4 : 0);
-    switch (bpl) {
-    case 1: hipLaunchKernelGGL((qgemv_kernel<FMT, MM, RPW, 1>), grid, block, lds, s, d); break;
-    case 2: hipLaunchKernelGGL((qgemv_kernel<FMT, MM, RPW, 2>), grid, block, lds, s, d); break;
-    case 3: hipLaunchKernelGGL((qgemv_kernel<FMT, MM, RPW, 3>), grid, block, lds, s, d); break;
-    case 4: hipLaunchKernelGGL((qgemv_kernel<FMT, MM, RPW, 4>), grid, block, lds, s, d); break;
+    gemv_body<FMT, MM, RPW, BPL>(d, (int)blockIdx.x);
+}
+
+template <int FMT, int MM, int RPW, int BPL>
+__global__ __launch_bounds__(64 * WAVES) void qgemv_group_kernel(const LayerGroup grp)
+{
+    // this workgroup's layer (wave-uniform) and its index within the layer
+    int li = 0;
+    while (li + 1 < grp.n && (int)blockIdx.x >= grp.begin[li + 1])
+        ++li;
+    gemv_body<FMT, MM, RPW, BPL>(grp.d[li], (int)blockIdx.x - grp.begin[li]);
+}
+
+template <int FMT, int MM, int RPW, int BPL>
+void launch_one(const LayerGroup &g, dim3 grid, size_t lds, hipStream_t s)
+{
+    if (g.n == 1)
+        hipLaunchKernelGGL((qgemv_kernel<FMT, MM, RPW, BPL>), grid, dim3(64 * WAVES), lds, s,
+                           g.d[0]);
+    else
+        hipLaunchKernelGGL((qgemv_group_kernel<FMT, MM, RPW, BPL>), grid, dim3(64 * WAVES), lds,
+                           s, g);
+}
+
+template <int FMT, int MM, int RPW>
+hipError_t launch_bpl(const LayerGroup &g0, hipStream_t s)
+{
+    LayerGroup g = g0;
+    int nbmax = 0;
+    size_t lds = 0;
+    g.begin[0] = 0;
+    for (int i = 0; i < g.n; ++i) {
+        const LinDesc &d = g.d[i];
+        const int nb = d.K / 32;
+        nbmax = std::max(nbmax, nb);
+        lds = std::max(lds, (size_t)d.M * d.K * 2 +
+                                (FMT == QL_FMT_Q4 ? (size_t)d.M * nb * 4 : 0));
+        g.begin[i + 1] = g.begin[i] + (d.N + WAVES * RPW - 1) / (WAVES * RPW);
+    }
+    const dim3 grid((unsigned)g.begin[g.n]);
+    switch ((nbmax + 63) / 64) {
+    case 1: launch_one<FMT, MM, RPW, 1>(g, grid, lds, s); break;
+    case 2: launch_one<FMT, MM, RPW, 2>(g, grid, lds, s); break;
+    case 3: launch_one<FMT, MM, RPW, 3>(g, grid, lds, s); break;
+    case 4: launch_one<FMT, MM, RPW, 4>(g, grid, lds, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 template <int FMT>
-hipError_t launch_fmt(const LinDesc &d, hipStream_t s)
+hipError_t launch_fmt(const LayerGroup &g, hipStream_t s)
 {
     // two weight rows per wavefront while that still leaves two workgroups
     // per CU, one otherwise
-    const bool two = (d.N + 2 * WAVES - 1) / (2 * WAVES) >= 512;
-    switch (d.M) {
-    case 1: return two ? launch_bpl<FMT, 1, 2>(d, s) : launch_bpl<FMT, 1, 1>(d, s);
-    case 2: return two ? launch_bpl<FMT, 2, 2>(d, s) : launch_bpl<FMT, 2, 1>(d, s);
-    case 3: return two ? launch_bpl<FMT, 3, 2>(d, s) : launch_bpl<FMT, 3, 1>(d, s);
-    case 4: return two ? launch_bpl<FMT, 4, 2>(d, s) : launch_bpl<FMT, 4, 1>(d, s);
+    int64_t rows = 0;
+    for (int i = 0; i < g.n; ++i)
+        rows += g.d[i].N;
+    const bool two = (rows + 2 * WAVES - 1) / (2 * WAVES) >= 512;
+    switch (g.d[0].M) {
+    case 1: return two ? launch_bpl<FMT, 1, 2>(g, s) : launch_bpl<FMT, 1, 1>(g, s);
+    case 2: return two ? launch_bpl<FMT, 2, 2>(g, s) : launch_bpl<FMT, 2, 1>(g, s);
+    case 3: return two ? launch_bpl<FMT, 3, 2>(g, s) : launch_bpl<FMT, 3, 1>(g, s);
+    case 4: return two ? launch_bpl<FMT, 4, 2>(g, s) : launch_bpl<FMT, 4, 1>(g, s);
     default: return hipErrorInvalidValue;
     }
 }
@@ -265,10 +317,13 @@ bool gemv_ok(const LinDesc &d)
     return d.M >= 1 && d.M <= 4 && d.K % 256 == 0 && d.K <= 8192 && (int64_t)d.M * d.K <= XMAX;
 }
 
-hipError_t launch_qgemv(int fmt, const LinDesc &d, hipStream_t stream)
+hipError_t launch_qgemv(int fmt, const LayerGroup &g, hipStream_t stream)
 {
-    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(d, stream)
-                              : launch_fmt<QL_FMT_Q4>(d, stream);
+    for (int i = 1; i < g.n; ++i)
+        if (g.d[i].M != g.d[0].M)
+            return hipErrorInvalidValue;  // one row count per launch
+    return fmt == QL_FMT_INT8 ? launch_fmt<QL_FMT_INT8>(g, stream)
+                              : launch_fmt<QL_FMT_Q4>(g, stream);
 }
 
 }  // namespace qlk

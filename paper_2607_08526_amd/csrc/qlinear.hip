@@ -448,9 +448,9 @@ bool wide_fits(const ql_linear &l)
 int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc,
                 hipStream_t stream)
 {
+    const int fmt = ls[0]->lin.fmt;
     LinDesc ds[QL_MAX_GROUP];
     RowPath path[QL_MAX_GROUP];
-    StreamPlan plan[QL_MAX_GROUP];
     for (int i = 0; i < n; ++i) {
         LinDesc &d = ds[i];
         d = LinDesc{};
@@ -462,6 +462,7 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc
         d.M = (int)ls[i]->lin.M;
         d.N = (int)ls[i]->lin.N;
         d.K = (int)ls[i]->lin.K;
+        d.ksplit = 1;
         switch (forced) {
         case QL_PATH_GEMV:
             if (!gemv_ok(d))
@@ -482,46 +483,77 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc
             path[i] = gemv_ok(d) ? RowPath::GEMV
                     : stream_fits(d) ? RowPath::STREAM : RowPath::SKINNY;
         }
-        if (path[i] == RowPath::STREAM) {
-            plan[i] = stream_plan(ls[i]->lin.fmt, d, device_cus());
-            d.ksplit = plan[i].S;
-            d.psteps = plan[i].psteps;
-            if (plan[i].S > 1)
-                wsrc.need = std::max(wsrc.need, round256((size_t)plan[i].S * d.M * d.N * 4));
+    }
+    // the streaming layers: one launch over all of them, their K parts
+    // planned together; the split layers' partials side by side in the
+    // workspace, summed by one more launch
+    LayerGroup sg{};
+    StreamPlan sp{};
+    size_t part_off[QL_MAX_GROUP], part_bytes = 0;
+    for (int i = 0; i < n; ++i)
+        if (path[i] == RowPath::STREAM)
+            sg.d[sg.n++] = ds[i];
+    if (sg.n > 0) {
+        int S[QL_MAX_GROUP], P[QL_MAX_GROUP];
+        sp = stream_plan(fmt, sg.d, sg.n, device_cus(), S, P);
+        sg.begin[0] = 0;
+        for (int j = 0; j < sg.n; ++j) {
+            LinDesc &d = sg.d[j];
+            d.ksplit = S[j];
+            d.psteps = P[j];
+            sg.begin[j + 1] = sg.begin[j] + (d.N + sp.rw - 1) / sp.rw * S[j];
+            part_off[j] = part_bytes;
+            if (S[j] > 1)
+                part_bytes += round256((size_t)S[j] * d.M * d.N * 4);
         }
     }
-    // layers run in stream order, so each split layer reuses the workspace
-    if (wsrc.dry_run || (wsrc.fixed && wsrc.need > wsrc.cap))
+    wsrc.need = std::max(wsrc.need, part_bytes);
+    if (wsrc.dry_run || (wsrc.fixed && part_bytes > wsrc.cap))
         return wsrc.dry_run ? QL_OK : QL_ERR_UNSUPPORTED;
+
+    // the GEMV layers: one launch per distinct row count
+    bool done[QL_MAX_GROUP] = {};
     for (int i = 0; i < n; ++i) {
-        LinDesc &d = ds[i];
-        const int fmt = ls[i]->lin.fmt;
-        hipError_t e = hipSuccess;
-        if (path[i] == RowPath::GEMV) {
-            e = launch_qgemv(fmt, d, stream);
-        } else if (path[i] == RowPath::STREAM) {
-            const StreamPlan &p = plan[i];
-            Workspace ws{};
-            if (p.S > 1) {
-                if (!get_workspace(wsrc, round256((size_t)p.S * d.M * d.N * 4), stream, ws))
-                    return QL_ERR_HIP;
-                d.part = (float *)ws.ptr;
+        if (path[i] != RowPath::GEMV || done[i])
+            continue;
+        LayerGroup g{};
+        for (int j = i; j < n; ++j)
+            if (path[j] == RowPath::GEMV && !done[j] && ds[j].M == ds[i].M) {
+                g.d[g.n++] = ds[j];
+                done[j] = true;
             }
-            e = launch_qgemm_stream(fmt, p, d, stream);
-            if (e == hipSuccess && p.S > 1) {
-                const SplitSum q{d.part, p.S, d.M, d.N, d.Y, d.ep};
-                e = launch_split_sum(&q, 1, stream);
-            }
-            if (ws.own_alloc) {
-                const hipError_t ef = hipFreeAsync(ws.ptr, stream);
-                e = e == hipSuccess ? ef : e;
-            }
-        } else {
-            e = launch_qgemm_skinny(fmt, d, stream);
+        if (launch_qgemv(fmt, g, stream) != hipSuccess)
+            return QL_ERR_HIP;
+    }
+    if (sg.n > 0) {
+        Workspace ws{};
+        if (part_bytes > 0) {
+            if (!get_workspace(wsrc, part_bytes, stream, ws))
+                return QL_ERR_HIP;
+            for (int j = 0; j < sg.n; ++j)
+                if (sg.d[j].ksplit > 1)
+                    sg.d[j].part = (float *)(ws.ptr + part_off[j]);
+        }
+        hipError_t e = launch_qgemm_stream(fmt, sp, sg, stream);
+        if (e == hipSuccess && part_bytes > 0) {
+            SplitSum sums[QL_MAX_GROUP];
+            int ns = 0;
+            for (int j = 0; j < sg.n; ++j)
+                if (sg.d[j].ksplit > 1)
+                    sums[ns++] = SplitSum{sg.d[j].part, sg.d[j].ksplit, sg.d[j].M, sg.d[j].N,
+                                          sg.d[j].Y, sg.d[j].ep};
+            e = launch_split_sum(sums, ns, stream);
+        }
+        if (ws.own_alloc) {
+            const hipError_t ef = hipFreeAsync(ws.ptr, stream);
+            e = e == hipSuccess ? ef : e;
         }
         if (e != hipSuccess)
             return QL_ERR_HIP;
     }
+    for (int i = 0; i < n; ++i)
+        if (path[i] == RowPath::SKINNY && launch_qgemm_skinny(fmt, ds[i], stream) != hipSuccess)
+            return QL_ERR_HIP;
     return QL_OK;
 }
 

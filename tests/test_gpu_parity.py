@@ -724,3 +724,67 @@ def test_forced_path_fp32_activations(gpu, orc):
         assert rel_err(Yg.cpu().numpy(), orc.forward(O.FMT_INT8, X, O.DT_F32, codes, scales, N)) <= 1e-5
     finally:
         ql.load().qlinear_force_path(ql.PATH_AUTO)
+
+
+# --------------------------------------------------------------------------
+# few-row grouped launches: a whole block's weights in one launch
+# --------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def skinny_block():
+    """The four d = 2048 linears of the int8 block workload's weights (seeds
+    2..5) and their q4 codes from the same draws."""
+    return [si.block_int8_weight(i) for i in range(4)]
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+@pytest.mark.parametrize("M", [1, 3, 8, 32])
+def test_block_forward_few_rows_grouped(gpu, orc, skinny_block, fmt, M):
+    """One block's four linears (QKV 2048->6144, out, FFN-up 2048->8192,
+    FFN-down 8192->2048) at the few-row sizes: the GEMV (M <= 4) and the
+    streaming kernel (M <= 32) each take the four layers in one launch, the
+    streaming kernel's K-split layers share one sum launch.  Every output
+    NaN-filled beforehand, every row against the oracle; a second call
+    repeats the first bit for bit."""
+    torch, ql = gpu
+    rng = np.random.default_rng(7300 + M + fmt)
+    xa = si.activations(rng, M, 2048, si.DT_BF16)
+    xb = si.activations(rng, M, 8192, si.DT_BF16)
+    entries, host = [], []
+    for W in skinny_block:
+        N, K = W.shape
+        cd, sd = ql.quantize(fmt, dev_w(torch, W))
+        X = xb if K == 8192 else xa
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        entries.append((fmt, dev_x(torch, X, O.DT_BF16), cd, sd, N, Y))
+        host.append((X, host_codes(cd), host_scales(sd), N))
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    first = [e[5].clone() for e in entries]
+    ql.block_forward(entries)
+    torch.cuda.synchronize()
+    for e, Y1, (X, cr, sr, N) in zip(entries, first, host):
+        assert torch.equal(e[5], Y1)
+        Yr = orc.forward(fmt, X, O.DT_BF16, cr, sr, N)
+        assert rel_err(e[5].cpu().numpy(), Yr) <= 1e-5, (M, N)
+
+
+def test_block_forward_few_rows_mixed_m(gpu, orc):
+    """One call whose layers have different row counts: GEMV layers of two
+    row counts (two launches), streaming layers of two row counts in one
+    launch (activation stage of the larger), some with K parts."""
+    torch, ql = gpu
+    specs = [(1, 300, 2048), (4, 257, 8192), (1, 64, 512), (9, 500, 8192), (30, 129, 1024),
+             (4, 1000, 256)]
+    for fmt in (O.FMT_INT8, O.FMT_Q4):
+        entries, refs = [], []
+        for i, (M, N, K) in enumerate(specs):
+            W, X = si.small_case(7400 + i + fmt, M, N, K)
+            cd, sd = ql.quantize(fmt, dev_w(torch, W))
+            Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+            entries.append((fmt, dev_x(torch, X, O.DT_BF16), cd, sd, N, Y))
+            refs.append(orc.forward(fmt, X, O.DT_BF16, host_codes(cd), host_scales(sd), N))
+        ql.block_forward(entries)
+        torch.cuda.synchronize()
+        for (M, N, K), e, Yr in zip(specs, entries, refs):
+            assert rel_err(e[5].cpu().numpy(), Yr) <= 1e-5, (fmt, M, N, K)
