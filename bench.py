@@ -68,6 +68,16 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle's timed sample")
+    ap.add_argument("--counter-points", action="store_true",
+                    help="run every measured configuration a few times eagerly, each point "
+                         "bracketed by marker dispatches, for rocprofv3 --pmc runs (see "
+                         "--summarize-points), then exit")
+    ap.add_argument("--summarize-points", nargs="+", metavar="DIR",
+                    help="turn rocprofv3 --pmc runs of --counter-points (one directory per "
+                         "counter set) into a per-point table and exit")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="per-point kernel durations of a rocprofv3 --kernel-trace run of "
+                         "--counter-points, then exit")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain device copy of known size (counter calibration)")
     ap.add_argument("--summarize-stats", metavar="DIR",
@@ -150,6 +160,281 @@ def summarize_traffic(fetch_dir, write_dir):
         "write_calibration": round(wcal, 4),
         "gemm_dispatches": len(gf),
     }
+
+
+# ---- counter runs ------------------------------------------------------------
+#
+# rocprofv3 --pmc records counters per dispatch.  The counter mode runs every
+# measured configuration (a "point") a few times eagerly, on distinct weight
+# copies (so that no call finds its weights in the L2 or last-level cache of
+# an earlier one), with a marker dispatch of `id` workgroups (libqlbench's
+# mark_kernel) before and after the point's calls; the summary splits the
+# dispatch list at the markers.  FETCH_SIZE and WRITE_SIZE are scaled by what
+# they read for a pure 1 GiB read (read_ceiling_kernel) and a pure 1 GiB
+# write (fill_kernel) of the same run.
+
+CALIB_BYTES = 1 << 30
+POINT_CALLS = 3
+
+
+def counter_point_list(torch, ql, si):
+    """(name, algorithmic bytes, flops, calls) per point: each call a
+    closure on its own copy of the weights.  Everything is allocated before
+    the first point runs."""
+    import numpy as np
+    dev = torch.device("cuda")
+    pts = []
+
+    def q(fmt, W, copies):
+        Wd = torch.from_numpy(W).to(dev)
+        c, s_ = ql.quantize(fmt, Wd)
+        return [(c, s_)] + [(c.clone(), s_.clone()) for _ in range(copies - 1)]
+
+    def xdev(X):
+        return torch.from_numpy(X if X.dtype == np.float32 else X.view("int16")).to(dev)
+
+    # cfg1, cfg2: the single-linear workloads
+    for name in ("single_int8", "single_q4"):
+        cfg = getattr(si, name)()
+        fmt, W, X = cfg["fmt"], cfg["W"], xdev(cfg["X"])
+        N, K = W.shape
+        M = X.shape[0]
+        Y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        cps = q(fmt, W, POINT_CALLS)
+        wb = cps[0][0].numel() + 2 * cps[0][1].numel()
+        calls = [(lambda c=c, s_=s_, X=X, Y=Y, fmt=fmt, N=N: ql.forward(fmt, X, c, s_, N, Y))
+                 for c, s_ in cps]
+        pts.append((f"{name} {N}x{K} M={M}", wb + X.numel() * X.element_size() + M * N * 4,
+                    2.0 * M * N * K, calls))
+    # cfg5: the few-row sweep
+    for v, fmt, N, K in si.skinny_variants():
+        cps = q(fmt, si.skinny_weight(v, N, K), POINT_CALLS)
+        wb = cps[0][0].numel() + 2 * cps[0][1].numel()
+        for M in si.SKINNY_M:
+            X = xdev(si.skinny_activations(M, K))
+            Y = torch.empty((M, N), dtype=torch.float32, device=dev)
+            calls = [(lambda c=c, s_=s_, X=X, Y=Y, fmt=fmt, N=N: ql.forward(fmt, X, c, s_, N, Y))
+                     for c, s_ in cps]
+            pts.append((f"skinny {'int8' if fmt == ql.FMT_INT8 else 'q4'} {N}x{K} M={M}",
+                        wb + M * K * 2 + M * N * 4, 2.0 * M * N * K, calls))
+
+    # one DiT block (d = 2048) per call: grouped few-row calls, the int8
+    # block and the q4 step's block at 2048 tokens, the paper's widths
+    def block_point(label, fmt, Wfn, d, M, copies, seed):
+        rng = np.random.default_rng(seed)
+        xa = xdev(si.activations(rng, M, d, si.DT_BF16))
+        xb = xdev(si.activations(rng, M, 4 * d, si.DT_BF16))
+        lin = si.block_linears(d)
+        Ys = [torch.empty((M, N), dtype=torch.float32, device=dev) for _, N, _ in lin]
+        calls, wb = [], 0
+        for cpy in range(copies):
+            ents = []
+            for i, (_, N, K) in enumerate(lin):
+                c, s_ = ql.quantize(fmt, torch.from_numpy(Wfn(cpy, i)).to(dev))
+                ents.append((fmt, xb if K == 4 * d else xa, c, s_, N, Ys[i]))
+                if cpy == 0:
+                    wb += c.numel() + 2 * s_.numel()
+            g = ql.make_group(ents)
+            calls.append(lambda g=g, ents=ents: ql.block_forward(None, group=g))
+        act = M * (3 * d + 4 * d) * 2 + M * sum(N for _, N, _ in lin) * 4
+        pts.append((label, wb + act, sum(2.0 * M * N * K for _, N, K in lin), calls))
+
+    for fmt in (ql.FMT_INT8, ql.FMT_Q4):
+        for M in (1, 8, 32):
+            block_point(f"block d=2048 {'int8' if fmt == ql.FMT_INT8 else 'q4'} M={M} (grouped)",
+                        fmt, lambda cpy, i: si.block_int8_weight(i), 2048, M, 2, 500 + M)
+    block_point("block d=2048 int8 M=2048", ql.FMT_INT8, lambda cpy, i: si.block_int8_weight(i),
+                2048, 2048, 2, 6)
+    block_point("step block d=2048 q4 M=2048", ql.FMT_Q4, lambda cpy, i: si.step_q4_weight(cpy, i),
+                2048, 2048, 2, 6)
+    for w, (name, d, nblk) in enumerate(si.PAPER_WIDTHS):
+        block_point(f"paper width {name} d={d} q4 M={si.PAPER_TOKENS}", ql.FMT_Q4,
+                    lambda cpy, i, w=w: si.paper_weight(w, cpy, i), d, si.PAPER_TOKENS, 2,
+                    900 + w)
+    return pts
+
+
+def counter_points(torch, ql, si):
+    import ctypes
+    from paper_2607_08526_amd import build as B
+    lib = ctypes.CDLL(B.BENCH_LIB)
+    lib.qlbench_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.qlbench_fill.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32, ctypes.c_void_p]
+    lib.qlbench_mark.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    stream = lambda: ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    pts = counter_point_list(torch, ql, si)
+    torch.cuda.synchronize()
+    buf = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+    for _ in range(2):
+        if lib.qlbench_fill(ctypes.c_void_p(buf.data_ptr()), CALIB_BYTES, 1, stream()) or \
+                lib.qlbench_read(ctypes.c_void_p(buf.data_ptr()), CALIB_BYTES,
+                                 ctypes.c_void_p(sink.data_ptr()), stream()):
+            raise RuntimeError("calibration launch failed")
+    torch.cuda.synchronize()
+    del buf
+    for pid, (name, abytes, flops, calls) in enumerate(pts, start=1):
+        if lib.qlbench_mark(pid, ctypes.c_void_p(sink.data_ptr()), stream()):
+            raise RuntimeError("marker launch failed")
+        for call in calls:
+            call()
+        if lib.qlbench_mark(pid, ctypes.c_void_p(sink.data_ptr()), stream()):
+            raise RuntimeError("marker launch failed")
+        torch.cuda.synchronize()
+        log(f"point {pid}: {name}, {len(calls)} calls")
+    with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "gpurun_out",
+                           "counter_points.json"), "w") as f:
+        json.dump([{"id": i, "name": n, "algo_bytes": b, "flops": fl, "calls": len(c)}
+                   for i, (n, b, fl, c) in enumerate(pts, start=1)], f)
+
+
+def _dispatches(d):
+    """Per-dispatch counter records of a rocprofv3 --pmc run, in dispatch
+    order: [(dispatch id, kernel, grid size, {counter: value})]."""
+    import csv, collections
+    recs = collections.OrderedDict()
+    for p in _csvs(d, "counter_collection.csv"):
+        for r in csv.DictReader(open(p)):
+            key = int(r["Dispatch_Id"])
+            if key not in recs:
+                recs[key] = (key, r["Kernel_Name"], int(r["Grid_Size"]), {})
+            recs[key][3][r["Counter_Name"]] = recs[key][3].get(r["Counter_Name"], 0.0) + \
+                float(r["Counter_Value"])
+    return [recs[k] for k in sorted(recs)]
+
+
+def _split_points(disp):
+    """{point id: [dispatches between its two markers]} and the calibration
+    dispatches (before the first marker)."""
+    out, calib, cur = {}, [], None
+    for rec in disp:
+        _, kern, grid, _ = rec
+        if "mark_kernel" in kern:
+            pid = grid // 64
+            cur = None if cur == pid else pid
+            if cur is not None:
+                out[cur] = []
+            continue
+        if cur is not None:
+            out[cur].append(rec)
+        elif not out:
+            calib.append(rec)
+    return out, calib
+
+
+SIMDS, XCDS = 1024, 8  # 256 CUs x 4 SIMDs; GRBM_GUI_ACTIVE is summed over the 8 XCDs
+
+
+def _mfma_busy(c):
+    """Fraction of the dispatch's cycles the matrix cores were busy, over
+    every SIMD: SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs; 32 per
+    32x32x16 f16 MFMA, the full issue time at the dense peak) over 1024 x
+    the dispatch's cycles (GRBM_GUI_ACTIVE, summed over the 8 XCDs)."""
+    busy, gui = c.get("SQ_VALU_MFMA_BUSY_CYCLES"), c.get("GRBM_GUI_ACTIVE")
+    if not busy or not gui:
+        return float("nan")
+    return busy / (SIMDS * gui / XCDS)
+
+
+def summarize_trace(d):
+    """Per point of a --kernel-trace run of --counter-points: each kernel's
+    average duration per call, and the wall time from the first kernel's
+    start to the last one's end, per call."""
+    import csv, collections
+    rows = []
+    for p in _csvs(d, "kernel_trace.csv"):
+        rows += list(csv.DictReader(open(p)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    meta_p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gpurun_out",
+                          "counter_points.json")
+    meta = {m["id"]: m for m in json.load(open(meta_p))}
+    cur, groups = None, collections.OrderedDict()
+    for r in rows:
+        grid = int(r.get("Grid_Size_X", r.get("Grid_Size", "0")))
+        if "mark_kernel" in r["Kernel_Name"]:
+            pid = grid // 64
+            cur = None if cur == pid else pid
+            if cur is not None:
+                groups[cur] = []
+            continue
+        if cur is not None:
+            groups[cur].append(r)
+    out = [f"{'id':>3} {'point':<44} {'us/call':>8} {'kernels (avg us per call)'}"]
+    for pid, rs in groups.items():
+        calls = meta[pid]["calls"]
+        per = collections.OrderedDict()
+        for r in rs:
+            k = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            k = k.replace("void ", "").replace("qlk::", "")
+            per[k] = per.get(k, 0.0) + (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        span = (int(rs[-1]["End_Timestamp"]) - int(rs[0]["Start_Timestamp"])) / 1e3 / calls
+        out.append(f"{pid:3d} {meta[pid]['name'][:44]:<44} {span:8.2f} " +
+                   "  ".join(f"{k} {v / calls:.2f}" for k, v in per.items()))
+    return "\n".join(out)
+
+
+def summarize_points(dirs):
+    import collections
+    meta_p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gpurun_out",
+                          "counter_points.json")
+    meta = {m["id"]: m for m in json.load(open(meta_p))}
+    vals = collections.defaultdict(lambda: collections.defaultdict(float))
+    kern = collections.defaultdict(lambda: collections.defaultdict(
+        lambda: collections.defaultdict(float)))
+    cal = {}
+    for d in dirs:
+        pts, calib = _split_points(_dispatches(d))
+        for _, k, _, c in calib:
+            for cn, v in c.items():
+                if cn in ("FETCH_SIZE", "WRITE_SIZE"):
+                    tag = "read" if "read_ceiling" in k else "fill" if "fill_kernel" in k else None
+                    if tag:
+                        cal[(tag, cn)] = max(cal.get((tag, cn), 0.0), v * 1024.0)
+        for pid, recs in pts.items():
+            calls = meta[pid]["calls"]
+            for _, k, _, c in recs:
+                short = k.replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
+                for cn, v in c.items():
+                    vals[pid][cn] += v / calls
+                    kern[pid][short][cn] += v / calls
+    fcal = cal.get(("read", "FETCH_SIZE"), 0.0) / CALIB_BYTES
+    wcal = cal.get(("fill", "WRITE_SIZE"), 0.0) / CALIB_BYTES
+    lines = [f"calibration: FETCH_SIZE of a pure 1 GiB read = {fcal:.4f} x its bytes; "
+             f"WRITE_SIZE of a pure 1 GiB write = {wcal:.4f} x its bytes",
+             f"(read of the fill: FETCH {cal.get(('fill', 'FETCH_SIZE'), 0) / CALIB_BYTES:.4f}, "
+             f"write of the read: WRITE {cal.get(('read', 'WRITE_SIZE'), 0) / CALIB_BYTES:.4f})", ""]
+    hdr = (f"{'id':>3} {'point':<44} {'algo_MB':>8} {'fetch_MB':>9} {'write_MB':>9} "
+           f"{'hbm/algo':>8} {'mfma_busy':>9} {'valu/mfma':>9}")
+    lines.append(hdr)
+    rows = []
+    for pid in sorted(vals):
+        m, v = meta[pid], vals[pid]
+        fb = v.get("FETCH_SIZE", float("nan")) * 1024 / fcal if fcal else float("nan")
+        wb = v.get("WRITE_SIZE", float("nan")) * 1024 / wcal if wcal else float("nan")
+        mf = v.get("SQ_INSTS_MFMA", 0.0)
+        mb = _mfma_busy(v)
+        vpm = (v.get("SQ_INSTS_VALU", float("nan")) - mf) / mf if mf > 0 else float("nan")
+        rows.append({"id": pid, "point": m["name"], "algo_bytes": m["algo_bytes"],
+                     "fetch_bytes": fb, "write_bytes": wb, "mfma_busy": mb, "valu_per_mfma": vpm,
+                     "counters": {k: round(x, 1) for k, x in v.items()}})
+        lines.append(f"{pid:3d} {m['name'][:44]:<44} {m['algo_bytes'] / 1e6:8.2f} {fb / 1e6:9.2f} "
+                     f"{wb / 1e6:9.2f} {(fb + wb) / m['algo_bytes']:8.2f} {mb:9.3f} {vpm:9.2f}")
+    lines.append("")
+    lines.append("per kernel (per call):")
+    for pid in sorted(kern):
+        for k, c in kern[pid].items():
+            fb = c.get("FETCH_SIZE", float("nan")) * 1024 / fcal / 1e6 if fcal else float("nan")
+            wb = c.get("WRITE_SIZE", float("nan")) * 1024 / wcal / 1e6 if wcal else float("nan")
+            mf = c.get("SQ_INSTS_MFMA", 0.0)
+            extra = ""
+            if mf > 0:
+                extra = (f"  mfma_busy {_mfma_busy(c):.3f}  valu/mfma "
+                         f"{(c.get('SQ_INSTS_VALU', 0.0) - mf) / mf:.2f}")
+            lines.append(f"{pid:3d} {k[:60]:<60} fetch {fb:8.2f} MB  write {wb:8.2f} MB{extra}  " +
+                         " ".join(f"{cn}={x:.0f}" for cn, x in sorted(c.items())
+                                  if cn not in ("FETCH_SIZE", "WRITE_SIZE")))
+    return "\n".join(lines) + "\n\nJSON " + json.dumps(
+        {"fetch_calibration": fcal, "write_calibration": wcal, "points": rows})
 
 
 class Step:
@@ -752,6 +1037,12 @@ def main():
     if args.summarize_traffic:
         print(json.dumps(summarize_traffic(*args.summarize_traffic), indent=1))
         return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_points:
+        print(summarize_points(args.summarize_points))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "single-GPU benchmark: --gpus must be 1 (the multi-GPU "
                                    "sharding is a design, not implemented)"}))
@@ -771,6 +1062,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         del a, b
+
+    if args.counter_points:
+        counter_points(torch, ql, si)
+        return
 
     if args.sweeps_only:
         print(json.dumps({"skinny": skinny_sweep(torch, ql, si),

@@ -226,12 +226,13 @@ int qlinear_block_forward_ep(const ql_linear_ep *lin, int n_lin, hipStream_t str
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc).  The same kernels and results, bit for bit, but the
  * workspace (fp16 activation copies, row shifts, split partials and arrival
- * counters) lives in a static device array of the library, 96 MiB
- * (100663296 bytes) per device, held from the first call on a device until
+ * counters) lives in a static device array of the library, 128 MiB
+ * (134217728 bytes) per device, held from the first call on a device until
  * the process ends.  The call allocates and frees nothing, through HIP or
  * any allocating library.  A call whose workspace would exceed the array
- * returns QL_ERR_UNSUPPORTED and enqueues nothing (one DiT block at
- * d = 2048 takes about 76 MB at 2048 tokens and 84 MB at 4096).  Every
+ * returns QL_ERR_UNSUPPORTED and enqueues nothing (at d = 2048 and 2048
+ * tokens one block's grouped call takes about 76 MB, the FFN-down layer
+ * alone about 101 MB; a block at 4096 tokens about 84 MB).  Every
  * call on a device shares that device's array: calls that may overlap on
  * one device (different streams, or graph replays concurrent with other
  * calls) race and must be ordered by the caller; calls on one stream are

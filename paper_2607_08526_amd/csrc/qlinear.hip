@@ -776,7 +776,7 @@ int classify(const ql_linear_ep *lin, int n_lin, Classes &c)
 // copy for the life of the process.  Host code must never use the array's
 // name as an address: kernels and copies take the device address that
 // hipGetSymbolAddress returns for the current device (scratch_base).
-constexpr size_t SCRATCH_BYTES = (size_t)96 << 20;
+constexpr size_t SCRATCH_BYTES = (size_t)128 << 20;
 static __device__ __align__(256) uint8_t scratch[SCRATCH_BYTES];
 
 // Device address of this device's scratch, looked up once per device (with

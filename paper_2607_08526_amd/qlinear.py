@@ -403,7 +403,7 @@ def block_forward_ep(entries, stream=None, group=None):
 
 def block_forward_ep_noalloc(entries, stream=None, group=None):
     """block_forward_ep through the entry point that allocates nothing: its
-    workspace is the library's static scratch (96 MiB per device).  Calls
+    workspace is the library's static scratch (128 MiB per device).  Calls
     that may overlap on one device must be ordered by the caller.
     Asynchronous."""
     arr = group if group is not None else make_group_ep(entries)

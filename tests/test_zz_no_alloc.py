@@ -18,7 +18,7 @@ from oracle import oracle as O
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-3
-SCRATCH_BYTES = 96 << 20
+SCRATCH_BYTES = 128 << 20
 
 
 @pytest.fixture(scope="module")
@@ -107,11 +107,11 @@ def test_no_alloc_matches_pool_entry_two_calls(gpu, orc):
 
 
 def test_no_alloc_refuses_oversized_workspace(gpu, orc):
-    """A layer whose fp16 activation copy alone (8192 x 8192 x 2 bytes =
-    128 MiB) exceeds the scratch: QL_ERR_UNSUPPORTED, nothing enqueued (Y
+    """A layer whose fp16 activation copy alone (8192 x 10240 x 2 bytes =
+    160 MiB) exceeds the scratch: QL_ERR_UNSUPPORTED, nothing enqueued (Y
     keeps its NaN fill); the same call through the pool entry point works."""
     torch, ql = gpu
-    M, N, K = 8192, 64, 8192
+    M, N, K = 8192, 64, 10240
     assert M * K * 2 > SCRATCH_BYTES
     X = torch.zeros((M, K), dtype=torch.bfloat16, device="cuda")
     W = torch.zeros((N, K), dtype=torch.float32, device="cuda")
@@ -126,3 +126,29 @@ def test_no_alloc_refuses_oversized_workspace(gpu, orc):
     ql.block_forward_ep(e)
     torch.cuda.synchronize()
     assert bool((Y == 0).all())
+
+
+def test_no_alloc_largest_dit_layer(gpu, orc):
+    """The DiT step's largest single call: FFN-down (8192 -> 2048, q4) alone
+    at 2048 tokens, K cut into parts with partial tiles in the scratch
+    (about 101 MB of workspace): bit for bit the pool path, sampled rows
+    against the oracle."""
+    torch, ql = gpu
+    rng = np.random.default_rng(13)
+    M, N, K = 2048, 2048, 8192
+    W = si.weights(rng, N, K)
+    X = si.activations(rng, M, K, si.DT_BF16)
+    codes, scales = ql.quantize(O.FMT_Q4, torch.from_numpy(W).cuda())
+    Xd = torch.from_numpy(X.view(np.int16)).cuda()
+    Ys = [torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda") for _ in range(2)]
+    ql.block_forward_ep([(O.FMT_Q4, Xd, codes, scales, N, Ys[0], None, O.ACT_NONE, None)])
+    ql.block_forward_ep_noalloc([(O.FMT_Q4, Xd, codes, scales, N, Ys[1], None, O.ACT_NONE, None)])
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(Ys[1]).all())
+    assert torch.equal(Ys[0], Ys[1])
+    rows = np.array([0, 127, 128, 1000, 2047])
+    cr = codes.cpu().numpy().astype(np.uint8)
+    sr = scales.cpu().numpy().view(np.uint16)
+    Yr = orc.forward(O.FMT_Q4, X, O.DT_BF16, cr, sr, N, rows=rows)
+    Yg = Ys[1].cpu().numpy().astype(np.float64)[rows]
+    assert np.max(np.abs(Yg - Yr)) / np.max(np.abs(Yr)) <= TOL
