@@ -232,12 +232,17 @@ int device_cus()
 // Split plan of a grouped fp16-path launch: how many parts each layer's
 // output tiles are cut into along K.  Tiles of different reduction lengths
 // (FFN-down's K = 4d next to K = d) or too few tiles for the GPU leave most
-// workgroup slots idle at the end of the launch; cutting the long
-// reductions into parts evens that out at the price of a partial-tile round
-// trip per part.  The plan is the one with the shortest estimated makespan
-// under the hardware's dispatch: workgroup p runs on XCD p % 8, each XCD
-// takes a contiguous range of every layer's parts (in layer order) and
-// starts them in order on its first free slot (wide_wgs_per_cu(fmt) per CU).
+// CUs idle at the end of the launch; cutting the long reductions into parts
+// evens that out at the price of a partial-tile round trip per part.  The
+// plan is the one with the shortest estimated makespan under the hardware's
+// dispatch: workgroup p runs on XCD p % 8, each XCD takes a contiguous range
+// of every layer's parts (in layer order) and starts them in order on its
+// first free CU.  The model counts one slot per CU: two workgroups resident
+// on one CU finish about as late as the two one after the other (measured
+// on single layers at 2048 tokens: out projection in 2 parts, one per CU,
+// 40 us, in 4 parts, two per CU, 49 us).  A layer with at least as many
+// tiles as there are CUs is not cut (measured: QKV at 2048 tokens, 384
+// tiles, 71 us whole and 91 us in 2 parts).
 //
 // A launch that fits in one wave of workgroup slots has no other work to
 // hide the last parts' in-kernel reduction behind: there the parts may
@@ -257,6 +262,11 @@ constexpr double TAIL_PER_PART = 2.2;    // last arriver's reload of one partial
 constexpr double EXT_GAP = 2.0;          // the extra launch
 constexpr double EXT_BYTES_PER_STEP = 5.0e6;  // bytes the sum launch moves per step
 constexpr int EXT_MAX_SPLIT = 16;
+// an in-kernel reduction whose layer has an epilogue: the last part to
+// arrive also applies it (residual loads, bias, copies) while the rest of
+// the GPU waits (measured: out projection with its residual add and bf16
+// copy, 2 parts, 53 us reduced in the kernel, 48 us by the sum launch)
+constexpr double EPI_TAIL = 12.0;
 
 double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
 {
@@ -284,7 +294,9 @@ double makespan(const LinDesc *d, int n, const SplitPlan &pl, int slots)
 
 SplitPlan plan_splits(int fmt, const LinDesc *d, int n)
 {
-    const int slots = std::max(1, wide_wgs_per_cu(fmt) * device_cus() / XCDS);
+    (void)fmt;
+    const int cus = device_cus();
+    const int slots = std::max(1, cus / XCDS);
     SplitPlan best{};
     double best_t = 0.0;
     int best_parts = 0;
@@ -299,9 +311,10 @@ SplitPlan plan_splits(int fmt, const LinDesc *d, int n)
         int total_parts = 0;
         for (int i = 0; i < n; ++i) {
             const int ns = d[i].K / 64;
-            // parts of a multiple of 4 steps (whole scale chunks), >= 8 steps
+            // parts of a multiple of 4 steps (whole scale chunks), >= 8 steps;
+            // a layer with a tile for every CU stays whole
             int ps = ns;
-            if (L < ns) {
+            if (L < ns && (int64_t)d[i].tiles_m * d[i].tiles_n < cus) {
                 ps = std::max(8, (L + 3) & ~3);
                 ps = std::min(ps, ns);
             }
@@ -334,7 +347,8 @@ SplitPlan plan_splits(int fmt, const LinDesc *d, int n)
     best_t = 0.0;
     for (int i = 0; i < n; ++i)
         best_t = std::max(best_t, best.psteps[i] + TILE_OVH +
-                                      (best.S[i] > 1 ? PART_STORE + TAIL_PER_PART * best.S[i]
+                                      (best.S[i] > 1 ? PART_STORE + TAIL_PER_PART * best.S[i] +
+                                                           (epi_active(d[i].ep) ? EPI_TAIL : 0.0)
                                                      : 0.0));
     std::vector<int> lens;
     for (int i = 0; i < n; ++i)
@@ -348,7 +362,8 @@ SplitPlan plan_splits(int fmt, const LinDesc *d, int n)
         double sum_bytes = 0.0;
         for (int i = 0; i < n; ++i) {
             const int ns = d[i].K / 64;
-            int ps = std::min(ns, std::max(4, (L + 3) & ~3));
+            int ps = (int64_t)d[i].tiles_m * d[i].tiles_n < cus
+                         ? std::min(ns, std::max(4, (L + 3) & ~3)) : ns;
             int S = (ns + ps - 1) / ps;
             if (S > EXT_MAX_SPLIT) {
                 ps = ((ns + EXT_MAX_SPLIT - 1) / EXT_MAX_SPLIT + 3) & ~3;
