@@ -29,13 +29,14 @@
  * roundings).  bf16 activations at larger M take the fp16 path: X is copied
  * exactly to fp16 with a power-of-two shift per row, each weight enters the
  * matrix cores as fp16(c * fp16(s * 2^f)) with one shift f per weight row
- * (Q * max_b s * 2^f in [2^14, 2^15)), so the one extra rounding is that of
- * c * s to 11 significant bits: relative error at most 2^-11 per weight for
- * every block whose scale is at least Q * 2^-28 of its row's largest scale
- * (2^-21 for int8, 2^-25 for q4).  Smaller blocks' scaled scales are fp16
- * subnormals; their weights are off by less than 2^-31 of the row's largest
- * dequantized weight.  Measured: about 2e-4 of max |Y| at transformer
- * shapes.
+ * and K part (the library may cut a long reduction into parts; Q * max_b s
+ * * 2^f in [2^14, 2^15) over the row's blocks in the part), so the one extra
+ * rounding is that of c * s to 11 significant bits: relative error at most
+ * 2^-11 per weight for every block whose scale is at least Q * 2^-28 of the
+ * largest scale of its row in its part, a fortiori of its row (2^-21 for
+ * int8, 2^-25 for q4).  Smaller blocks' scaled scales are fp16 subnormals;
+ * their weights are off by less than 2^-31 of the row's largest dequantized
+ * weight.  Measured: about 2e-4 of max |Y| at transformer shapes.
  *
  * Data formats (all buffers are DEVICE memory owned by the caller):
  *   W       fp32 [N][K]

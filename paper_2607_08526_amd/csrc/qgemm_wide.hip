@@ -8,9 +8,10 @@
 //   X'[m][k] = X[m][k] * 2^-e[m]                       (fp16, exact; xprep.hip)
 //   W'[n][k] = fp16(c[n][k] * fp16(s[n][b] * 2^f[n]))   (one rounding)
 //
-// with the whole K accumulated in fp32 by v_mfma_f32_32x32x16_f16.  f[n] is
-// chosen per weight row from the row's largest scale so that every |W'| is
-// below 2^15: c is made exact in fp16 by a magic-number add (the fp16 bit
+// with the whole K (or one K part of a split reduction) accumulated in fp32
+// by v_mfma_f32_32x32x16_f16.  f[n] is chosen per weight row (and K part)
+// from the largest scale of the row's blocks in the part, so that every
+// |W'| is below 2^15: c is made exact in fp16 by a magic-number add (the fp16 bit
 // pattern 0x6400 | u is 1024 + u) and one packed fp16 multiply by the scaled
 // scale rounds c * s to 11 significant bits.  No per-block work remains on
 // the accumulators, which is what made the exact per-block form
@@ -464,11 +465,15 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         if (q < ns)
             issue_stage<FMT>(c, ring + q * G::STAGE, q);
 
-    // Row shifts, behind the first stages so their latency overlaps: lane
-    // (l32, g) scans half of the scales of each of its NSUB weight rows
-    // (16-byte chunks g, g + 2, ...; K % 256 == 0 and 16-byte aligned scales,
-    // checked by the host); the two halves are then combined.  fp16 bit
-    // patterns of non-negative values order as integers.
+    // Row shifts, behind the first stages so their latency overlaps.  Each
+    // K part takes the shift of each weight row from the largest scale of
+    // its own blocks (its partial outputs are scaled back exactly before
+    // they are stored or added up, so parts may differ): lane (l32, g)
+    // scans half of this part's scale chunks of each of its NSUB weight
+    // rows (16-byte chunks q0 + g, q0 + g + 2, ...; K % 256 == 0 and
+    // 16-byte aligned scales, checked by the host); the two halves are then
+    // combined.  fp16 bit patterns of non-negative values order as integers.
+    const int q0 = s0 / G::SGROUP, q1 = (s0 + ns) / G::SGROUP;
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
         if constexpr (FMT == QL_FMT_F16) {
@@ -479,7 +484,7 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
         uint32_t mx = 0;
 #pragma unroll 4
-        for (int q = c.g; q < nb / 8; q += 2) {
+        for (int q = q0 + c.g; q < q1; q += 2) {
             const u32x4 v = srow[q];
 #pragma unroll
             for (int t = 0; t < 4; ++t)
