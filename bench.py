@@ -34,9 +34,6 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_step_q4.txt")
 # valid for the sources it was measured on
 KERNEL_SOURCES = ["paper_2607_08526_amd/csrc/qgemm_wide.hip", "paper_2607_08526_amd/csrc/xprep.hip",
                   "paper_2607_08526_amd/csrc/internal.h", "paper_2607_08526_amd/csrc/qlinear.hip"]
-GEMM_KERNEL = "qgemm_wide_kernel<4, false>"  # q4, no epilogue
-PREP_KERNEL = "xprep_kernel"
-COPY_BYTES = 1 << 30  # the calibration copy: 1 GiB read + 1 GiB written
 
 
 def kernel_source_hash():
@@ -75,16 +72,14 @@ def parse():
     ap.add_argument("--summarize-points", nargs="+", metavar="DIR",
                     help="turn rocprofv3 --pmc runs of --counter-points (one directory per "
                          "counter set) into a per-point table and exit")
+    ap.add_argument("--write-traffic", action="store_true",
+                    help="with --summarize-points: also write the step launch's HBM traffic "
+                         "record (the bench line's roofline.traffic)")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="per-point kernel durations of a rocprofv3 --kernel-trace run of "
                          "--counter-points, then exit")
-    ap.add_argument("--calib-copy", action="store_true",
-                    help="also run a plain device copy of known size (counter calibration)")
     ap.add_argument("--summarize-stats", metavar="DIR",
                     help="print a kernel summary of a rocprofv3 --stats output dir and exit")
-    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
-                         "'bench.py --calib-copy' into the traffic record and exit")
     return ap.parse_args()
 
 
@@ -108,58 +103,6 @@ def summarize_stats(d):
                    f"{float(r['MinNs']) / 1e3:10.2f} {float(r['MaxNs']) / 1e3:10.2f} "
                    f"{float(r['TotalDurationNs']) / 1e6:10.3f} {float(r['Percentage']):6.2f}  {short}")
     return "\n".join(out)
-
-
-def _counter_avg(d, counter):
-    """Per-dispatch average of one counter, by kernel (KiB for FETCH/WRITE_SIZE)."""
-    import csv, collections
-    acc = collections.defaultdict(list)
-    for p in _csvs(d, "counter_collection.csv"):
-        for r in csv.DictReader(open(p)):
-            if r["Counter_Name"] == counter:
-                acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
-    return acc
-
-
-def summarize_traffic(fetch_dir, write_dir):
-    """HBM bytes of one step launch (the pre-pass dispatches and the GEMM of
-    one block call), each counter scaled by what it reads for a plain copy of
-    COPY_BYTES."""
-    f = _counter_avg(fetch_dir, "FETCH_SIZE")
-    w = _counter_avg(write_dir, "WRITE_SIZE")
-
-    def pick(acc, key, pred=None):
-        ks = [k for k in acc if key in k and (pred is None or pred(acc[k]))]
-        if not ks:
-            raise SystemExit(f"no dispatches of {key} in the counter output")
-        vals = [v for k in ks for v in acc[k]]
-        return vals
-
-    # the calibration copy: the largest single dispatch of a copy kernel
-    def copy_val(acc):
-        ks = [k for k in acc if "copy" in k.lower()]
-        if not ks:
-            raise SystemExit("no copy kernel in the counter output (run with --calib-copy)")
-        return max(v for k in ks for v in acc[k])
-
-    fcal = copy_val(f) * 1024 / COPY_BYTES
-    wcal = copy_val(w) * 1024 / COPY_BYTES
-    gf, gw = pick(f, GEMM_KERNEL), pick(w, GEMM_KERNEL)
-    pf, pw = pick(f, PREP_KERNEL), pick(w, PREP_KERNEL)
-    # each block call runs one GEMM dispatch and one pre-pass per distinct X
-    prep_per_call = len(pf) / len(gf)
-    gemm_b = (sum(gf) / len(gf) * 1024 / fcal) + (sum(gw) / len(gw) * 1024 / wcal)
-    prep_b = prep_per_call * ((sum(pf) / len(pf) * 1024 / fcal) + (sum(pw) / len(pw) * 1024 / wcal))
-    return {
-        "kernel_source_sha256": kernel_source_hash(),
-        "hbm_bytes_per_launch": round(gemm_b + prep_b),
-        "gemm_bytes_per_dispatch": round(gemm_b),
-        "prep_bytes_per_call": round(prep_b),
-        "prep_dispatches_per_call": prep_per_call,
-        "fetch_calibration": round(fcal, 4),
-        "write_calibration": round(wcal, 4),
-        "gemm_dispatches": len(gf),
-    }
 
 
 # ---- counter runs ------------------------------------------------------------
@@ -373,7 +316,19 @@ def summarize_trace(d):
     return "\n".join(out)
 
 
-def summarize_points(dirs):
+STEP_POINT = "step block d=2048 q4 M=2048"
+TRAFFIC_COMMANDS = [
+    "cd /tmp && export TMPDIR=/tmp",
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pmc_fetch -o fetch -- "
+    "python3 $R/bench.py --counter-points",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pmc_write -o write -- "
+    "python3 $R/bench.py --counter-points",
+    "python3 $R/bench.py --summarize-points $R/gpurun_out/pmc_fetch $R/gpurun_out/pmc_write "
+    "--write-traffic   (R = repository root)",
+]
+
+
+def summarize_points(dirs, write_traffic=False):
     import collections
     meta_p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gpurun_out",
                           "counter_points.json")
@@ -433,6 +388,36 @@ def summarize_points(dirs):
             lines.append(f"{pid:3d} {k[:60]:<60} fetch {fb:8.2f} MB  write {wb:8.2f} MB{extra}  " +
                          " ".join(f"{cn}={x:.0f}" for cn, x in sorted(c.items())
                                   if cn not in ("FETCH_SIZE", "WRITE_SIZE")))
+    if write_traffic:
+        step = [r for r in rows if r["point"] == STEP_POINT]
+        if not step or not (step[0]["fetch_bytes"] == step[0]["fetch_bytes"]) or \
+                not (step[0]["write_bytes"] == step[0]["write_bytes"]):
+            raise SystemExit("the step point needs both FETCH_SIZE and WRITE_SIZE runs")
+        st = step[0]
+        pid = st["id"]
+        rec = {
+            "kernel_source_sha256": kernel_source_hash(),
+            "hbm_bytes_per_launch": round(st["fetch_bytes"] + st["write_bytes"]),
+            "fetch_bytes_per_launch": round(st["fetch_bytes"]),
+            "write_bytes_per_launch": round(st["write_bytes"]),
+            "algorithmic_bytes_per_launch": st["algo_bytes"],
+            "per_kernel": {k: {"fetch_bytes": round(c.get("FETCH_SIZE", 0) * 1024 / fcal),
+                               "write_bytes": round(c.get("WRITE_SIZE", 0) * 1024 / wcal)}
+                           for k, c in kern[pid].items()},
+            "fetch_calibration": round(fcal, 4),
+            "write_calibration": round(wcal, 4),
+            "commands": TRAFFIC_COMMANDS,
+            "notes": "One launch = one block call of the q4 step (d = 2048, 2048 tokens): the "
+                     "activation pre-pass (both activation tensors, one dispatch) and the "
+                     "grouped large-M GEMM, averaged over calls on two blocks' distinct weights. "
+                     "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are divided by what they read "
+                     "for a pure 1 GiB read (read_ceiling_kernel: FETCH_SIZE = 0.5 x the bytes, "
+                     "the counter's request unit) and a pure 1 GiB write (fill_kernel: "
+                     "WRITE_SIZE = 1.0 x) in the same run.",
+        }
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
     return "\n".join(lines) + "\n\nJSON " + json.dumps(
         {"fetch_calibration": fcal, "write_calibration": wcal, "points": rows})
 
@@ -984,6 +969,206 @@ def paper_widths(torch, ql, si):
     return out
 
 
+def single_configs(torch, ql, si):
+    """The two single-linear workloads (int8 1024x1024 with fp32 X 64x1024;
+    q4 FFN-up 6144x1536 with bf16 X 256x1536), each as a HIP graph over R
+    copies of the weights (R x footprint >= 512 MB, past the last-level
+    cache), with the roofline time max(flops / peak, bytes / 8 TB/s).  fp32
+    activations are contracted as three bf16 planes, so their MFMA peak is a
+    third of the bf16 one."""
+    dev = torch.device("cuda")
+    out = []
+    for name in ("single_int8", "single_q4"):
+        cfg = getattr(si, name)()
+        fmt, W, Xh, xdt = cfg["fmt"], cfg["W"], cfg["X"], cfg["xdt"]
+        N, K = W.shape
+        M = Xh.shape[0]
+        X = torch.from_numpy(Xh if xdt == si.DT_F32 else Xh.view("int16")).to(dev)
+        Y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        c, s_ = ql.quantize(fmt, torch.from_numpy(W).to(dev))
+        wbytes = c.numel() + 2 * s_.numel()
+        R = max(1, -(-ROT_BYTES // wbytes))
+        copies = [(c, s_)] + [(c.clone(), s_.clone()) for _ in range(R - 1)]
+        groups = [ql.make_group([(fmt, X, cc, ss, N, Y)]) for cc, ss in copies]
+
+        def fn():
+            for g in groups:
+                ql.block_forward(None, group=g)
+
+        t = graph_time(torch, fn)[0] / R * 1e-3
+        flops = 2.0 * M * N * K
+        abytes = wbytes + X.numel() * X.element_size() + M * N * 4
+        peak = BF16_MFMA_PEAK_TFLOPS / (3.0 if xdt == si.DT_F32 else 1.0)
+        t_roof = max(flops / (peak * 1e12), abytes / (HBM_PEAK_GBPS * 1e9))
+        out.append({"workload": name, "fmt": "int8" if fmt == ql.FMT_INT8 else "q4",
+                    "M": M, "N": N, "K": K, "x": "fp32" if xdt == si.DT_F32 else "bf16",
+                    "us_per_call": round(t * 1e6, 3), "TFLOPs": round(flops / t / 1e12, 2),
+                    "hbm_GBps": round(abytes / t / 1e9, 1),
+                    "roofline_us": round(t_roof * 1e6, 3),
+                    "roofline_bound": "mfma" if flops / (peak * 1e12) >= abytes / (
+                        HBM_PEAK_GBPS * 1e9) else "hbm",
+                    "roofline_frac": round(t_roof / t, 4), "copies": R})
+        log(f"single {out[-1]}")
+        del copies, groups
+    return out
+
+
+def host_info():
+    """The host's CPU model and the cores the process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)),
+            "os_cpu_count": os.cpu_count()}
+
+
+class ClockSampler:
+    """Samples the GPU's current graphics (shader) clock in a thread while a
+    workload runs (amd-smi's Python interface, else rocm-smi)."""
+
+    def __init__(self, period=0.02):
+        import threading
+        self.period, self.samples, self.source = period, [], None
+        self._stop = threading.Event()
+        self._read = self._setup()
+        self._thread = threading.Thread(target=self._loop, daemon=True)
+
+    def _setup(self):
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            h = amdsmi.amdsmi_get_processor_handles()[0]
+            gfx = amdsmi.AmdSmiClkType.GFX
+
+            def read():
+                return float(amdsmi.amdsmi_get_clock_info(h, gfx)["clk"])
+            read()
+            self.source = "amdsmi gfx clock"
+            return read
+        except Exception:
+            pass
+        import re
+        import subprocess
+
+        def read_smi():
+            out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                                 timeout=5).stdout
+            m = re.search(r"sclk clock level:\s*\d+:\s*\((\d+)Mhz\)", out)
+            return float(m.group(1)) if m else None
+        try:
+            if read_smi() is not None:
+                self.source = "rocm-smi sclk"
+                self.period = 0.2
+                return read_smi
+        except Exception:
+            pass
+        return None
+
+    def _loop(self):
+        while not self._stop.is_set():
+            try:
+                v = self._read()
+                if v:
+                    self.samples.append(v)
+            except Exception:
+                pass
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self._read:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._read:
+            self._thread.join()
+        return False
+
+    def summary(self):
+        if not self.samples:
+            return {"sclk_mhz": None, "samples": 0, "source": self.source}
+        v = sorted(self.samples)
+        return {"sclk_mhz": v[len(v) // 2], "sclk_mhz_min": v[0], "sclk_mhz_max": v[-1],
+                "samples": len(v), "source": self.source}
+
+
+def step_clock(torch, step, seconds=0.6):
+    """The shader clock while the step runs back to back for ~0.6 s (the
+    step's GEMMs run power-limited below the 2.4 GHz peak clock)."""
+    import time as _t
+    step.run()
+    torch.cuda.synchronize()
+    with ClockSampler() as cs:
+        t0 = _t.perf_counter()
+        while _t.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                step.run()
+            torch.cuda.synchronize()
+    return cs.summary()
+
+
+def oracle_timings(step, si):
+    """The fp64 oracle timed per workload, quantization and forward apart,
+    on the host cores the process may run on: the single linears and the
+    few-row sweep in full, one int8 block at 2048 tokens in full, and the
+    24-block q4 step as 24 x one block (quantization of block 0's weights,
+    forward rate of the cpu_baseline sample), labelled extrapolated."""
+    import numpy as np
+    from oracle import oracle as O
+    orc = O.default()
+    out = {"threads": orc.num_threads(), **host_info()}
+
+    def timed(f):
+        t = time.perf_counter()
+        r = f()
+        return r, time.perf_counter() - t
+
+    rows = []
+    for name in ("single_int8", "single_q4"):
+        cfg = getattr(si, name)()
+        (cr, sr), tq = timed(lambda: orc.quantize(cfg["fmt"], cfg["W"]))
+        N, K = cfg["W"].shape
+        _, tf = timed(lambda: orc.forward(cfg["fmt"], cfg["X"], cfg["xdt"], cr, sr, N))
+        fl = 2.0 * cfg["X"].shape[0] * N * K
+        rows.append({"workload": name, "quantize_s": round(tq, 4), "forward_s": round(tf, 4),
+                     "forward_GFLOPs": round(fl / tf / 1e9, 3)})
+    sk_q, sk_f, sk_fl = 0.0, 0.0, 0.0
+    for v, fmt, N, K in si.skinny_variants():
+        W = si.skinny_weight(v, N, K)
+        (cr, sr), tq = timed(lambda: orc.quantize(fmt, W))
+        sk_q += tq
+        for M in si.SKINNY_M:
+            X = si.skinny_activations(M, K)
+            _, tf = timed(lambda: orc.forward(fmt, X, O.DT_BF16, cr, sr, N))
+            sk_f += tf
+            sk_fl += 2.0 * M * N * K
+    rows.append({"workload": "skinny sweep (4 weights x M in 1, 8, 32, 128)",
+                 "quantize_s": round(sk_q, 4), "forward_s": round(sk_f, 4),
+                 "forward_GFLOPs": round(sk_fl / sk_f / 1e9, 3)})
+    xa, xb = step.xa_host, step.xb_host
+    bq, bf, bfl = 0.0, 0.0, 0.0
+    for i, (_, N, K) in enumerate(si.block_linears()):
+        W = si.block_int8_weight(i)
+        (cr, sr), tq = timed(lambda: orc.quantize(O.FMT_INT8, W))
+        X = xb if K == 4 * si.D_MODEL else xa
+        _, tf = timed(lambda: orc.forward(O.FMT_INT8, X, O.DT_BF16, cr, sr, N))
+        bq, bf, bfl = bq + tq, bf + tf, bfl + 2.0 * X.shape[0] * N * K
+    rows.append({"workload": "block_int8 (one d=2048 block, 2048 tokens, in full)",
+                 "quantize_s": round(bq, 3), "forward_s": round(bf, 3),
+                 "forward_GFLOPs": round(bfl / bf / 1e9, 3)})
+    q4q = sum(timed(lambda W=W: orc.quantize(O.FMT_Q4, W))[1] for W in step.W0)
+    out["rows"] = rows
+    out["q4_block0_quantize_s"] = round(q4q, 3)
+    return out
+
+
 def cpu_baseline(step, si, target_s):
     """The fp64 oracle on a bounded sample of the same workload: rows of
     block 0's four linears (all N), after the oracle's own quantization."""
@@ -1012,7 +1197,7 @@ def cpu_baseline(step, si, target_s):
         t = run(rows)
     flops = rows * sum(2.0 * N * K for _, N, K in lin)
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", **host_info(), "forward_s_per_row": t / rows,
             "sample": f"fp64 oracle forward of {rows} of 2048 token rows through block 0's four "
                       f"q4 linears (all outputs), {t:.1f}s; the oracle's own quantization of "
                       f"those 50.3M weights took {tq:.2f}s (not in the rate)"}
@@ -1034,14 +1219,11 @@ def main():
     if args.summarize_stats:
         print(summarize_stats(args.summarize_stats))
         return
-    if args.summarize_traffic:
-        print(json.dumps(summarize_traffic(*args.summarize_traffic), indent=1))
-        return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
         return
     if args.summarize_points:
-        print(summarize_points(args.summarize_points))
+        print(summarize_points(args.summarize_points, args.write_traffic))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "single-GPU benchmark: --gpus must be 1 (the multi-GPU "
@@ -1055,20 +1237,13 @@ def main():
         sys.exit("bench.py needs a GPU")
     ql.load()
 
-    if args.calib_copy:
-        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
-
     if args.counter_points:
         counter_points(torch, ql, si)
         return
 
     if args.sweeps_only:
-        print(json.dumps({"skinny": skinny_sweep(torch, ql, si),
+        print(json.dumps({"single_configs": single_configs(torch, ql, si),
+                          "skinny": skinny_sweep(torch, ql, si),
                           "block_few_rows": block_few_rows(torch, ql, si),
                           "block_int8": block_int8(torch, ql, si),
                           "block_w8a8": block_w8a8(torch, ql, si),
@@ -1088,6 +1263,8 @@ def main():
     achieved = step.flops_per_block / (avg_launch_ms * 1e-3) / 1e12
     log(f"step: {ms_per_step:.3f} ms, {tflops:.1f} TFLOP/s; grouped launch avg {avg_launch_ms:.4f} ms "
         f"-> {achieved:.1f} TFLOP/s; host wall {wall:.2f}s")
+    clock = step_clock(torch, step)
+    log(f"shader clock while the step runs: {clock}")
 
     res = {
         "metric": "quantized-linear TFLOP/s, one DiT denoising step's linear stack "
@@ -1121,6 +1298,7 @@ def main():
             "flops_per_launch": step.flops_per_block,
             "avg_launch_ms": round(avg_launch_ms, 5),
         },
+        "sclk": clock,
     }
     if args.step_only:
         print(json.dumps(res), flush=True)
@@ -1138,6 +1316,7 @@ def main():
     res["attention"] = attention_bench(torch, ql, si, step)
     res["dit_step"] = dit_step(torch, ql, si, step)
     if not args.no_sweeps:
+        res["single_configs"] = single_configs(torch, ql, si)
         res["skinny"] = skinny_sweep(torch, ql, si)
         res["block_few_rows"] = block_few_rows(torch, ql, si)
         res["block_int8"] = block_int8(torch, ql, si)
@@ -1145,6 +1324,14 @@ def main():
         res["paper_widths"] = paper_widths(torch, ql, si)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(step, si, args.cpu_seconds)
+        ot = oracle_timings(step, si)
+        per_block_fwd = res["cpu_baseline"]["forward_s_per_row"] * step.M
+        ot["step_q4_extrapolated"] = {
+            "note": "24 x one q4 block: the block-0 quantization time and the forward rate of "
+                    "the cpu_baseline sample scaled to 2048 token rows (extrapolated, not run)",
+            "quantize_s": round(24 * ot["q4_block0_quantize_s"], 2),
+            "forward_s": round(24 * per_block_fwd, 1)}
+        res["oracle_timings"] = ot
     print(json.dumps(res), flush=True)
 
 
