@@ -34,7 +34,9 @@
 // HBM straight into registers one step ahead.  Workgroups are assigned to
 // tiles XCD-aware: the 8 XCDs take contiguous ranges of the logical tile
 // order (row tiles fastest), so workgroups sharing a weight strip share an
-// L2.
+// L2.  A long reduction with too few tiles for the GPU is cut into K parts
+// (LinDesc::ksplit parts of psteps 64-k steps): each part stores a plain
+// fp32 partial output and the split-sum launch adds them in part order.
 #include <type_traits>
 
 #include "epilogue.h"
@@ -196,9 +198,12 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
         if (t < args.n && p < args.d[t].tile_begin && end == args.total_tiles)
             end = args.d[t].tile_begin;
     }
+    // a split layer's logical tiles walk its K parts fastest
     const int local = logical_tile(p - d.tile_begin, end - d.tile_begin);
-    const int tm = local % d.tiles_m;
-    const int tn = local / d.tiles_m;
+    const int S = d.ksplit, part = local % S;
+    const int tile = local / S;
+    const int tm = tile % d.tiles_m;
+    const int tn = tile / d.tiles_m;
     const int M = d.M, N = d.N, K = d.K;
     const int nb = K >> 5;
     const int m0 = tm * BM;
@@ -301,15 +306,17 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
         for (int j = 0; j < NSUB; ++j)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nsteps = (nb + 1) >> 1;
-    load_codes(0, cr, sr);
-    load_x(0);
+    // this part's 64-k steps [s0, s1)
+    const int s0 = part * d.psteps;
+    const int s1 = min((nb + 1) >> 1, s0 + d.psteps);
+    load_codes(s0, cr, sr);
+    load_x(s0);
     store_x(0);
     __syncthreads();
 
-    for (int step = 0; step < nsteps; ++step) {
-        const int buf = step & 1;
-        const bool more = step + 1 < nsteps;
+    for (int step = s0; step < s1; ++step) {
+        const int buf = (step - s0) & 1;
+        const bool more = step + 1 < s1;
         if (more) {
             load_x(step + 1);
             load_codes(step + 1, cn, sn);
@@ -375,7 +382,10 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
         __syncthreads();
     }
 
-    // ---- epilogue: lane holds rows 4*lg + r of each 16-row subtile ---------
+    // ---- epilogue: lane holds rows 4*lg + r of each 16-row subtile; a part
+    // of a split layer stores its plain partial output (the sum launch adds
+    // the parts and applies the epilogue) --------------------------------
+    float *const Yp = S > 1 ? d.part + (int64_t)part * M * N : nullptr;
 #pragma unroll
     for (int i = 0; i < MSUB; ++i)
 #pragma unroll
@@ -384,8 +394,12 @@ __global__ __launch_bounds__(256) void qgemm_kernel(const GroupArgs args)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int m = m0 + i * 16 + lg * 4 + r;
-                if (m < M && n < N)
-                    epi_store(d.ep, d.Y, (int64_t)m * N + n, n, acc[i][j][r]);
+                if (m < M && n < N) {
+                    if (S > 1)
+                        Yp[(int64_t)m * N + n] = acc[i][j][r];
+                    else
+                        epi_store(d.ep, d.Y, (int64_t)m * N + n, n, acc[i][j][r]);
+                }
             }
         }
 }

@@ -572,6 +572,66 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc
     return QL_OK;
 }
 
+// The tiled exact kernel over a group (LinDescs set up with ksplit = 1).
+// A group with too few tiles for two workgroups per CU has its reductions
+// cut into parts of one common length (at least 4 steps of 64 k), each
+// layer into ceil(steps / length) parts; the parts' plain partial outputs
+// are added, in part order, by the split-sum launch, which also applies
+// the layers' epilogues.
+int launch_tiled(int fmt, bool xf32, TileCfg t, GroupArgs &a, WsSource &wsrc,
+                 hipStream_t stream)
+{
+    const int n = a.n;
+    const int64_t target = 2 * (int64_t)device_cus();
+    int64_t work = 0;
+    for (int i = 0; i < n; ++i)
+        work += (int64_t)a.d[i].tiles_m * a.d[i].tiles_n * ((a.d[i].K / 32 + 1) / 2);
+    const int64_t L = std::max<int64_t>(4, (work + target - 1) / target);
+    int64_t total = 0;
+    size_t part_off[QL_MAX_GROUP], bytes = 0;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        const int ns = (d.K / 32 + 1) / 2;  // 64-k steps, the last one possibly half
+        int S = (int)std::min<int64_t>(EXT_MAX_SPLIT, (ns + L - 1) / L);
+        d.psteps = (ns + S - 1) / S;
+        d.ksplit = S = (ns + d.psteps - 1) / d.psteps;
+        d.tile_begin = (int)total;
+        total += (int64_t)d.tiles_m * d.tiles_n * S;
+        part_off[i] = bytes;
+        if (S > 1)
+            bytes += round256((size_t)S * d.M * d.N * 4);
+    }
+    if (total >= I31)
+        return QL_ERR_UNSUPPORTED;
+    a.total_tiles = (int)total;
+    wsrc.need = std::max(wsrc.need, bytes);
+    if (wsrc.dry_run)
+        return QL_OK;
+    Workspace ws{};
+    if (bytes > 0) {
+        if (!get_workspace(wsrc, bytes, stream, ws))
+            return wsrc.fixed ? QL_ERR_UNSUPPORTED : QL_ERR_HIP;
+        for (int i = 0; i < n; ++i)
+            if (a.d[i].ksplit > 1)
+                a.d[i].part = (float *)(ws.ptr + part_off[i]);
+    }
+    hipError_t e = launch_qgemm(fmt, xf32, t, a, stream);
+    if (e == hipSuccess && bytes > 0) {
+        SplitSum sums[QL_MAX_GROUP];
+        int ns = 0;
+        for (int i = 0; i < n; ++i)
+            if (a.d[i].ksplit > 1)
+                sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
+                                      a.d[i].ep};
+        e = launch_split_sum(sums, ns, stream);
+    }
+    if (ws.own_alloc) {
+        const hipError_t ef = hipFreeAsync(ws.ptr, stream);
+        e = e == hipSuccess ? ef : e;
+    }
+    return e == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
 // One grouped launch over layers that share fmt and xdt (M > 0 each).
 int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream_t stream)
 {
@@ -653,11 +713,8 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         return QL_ERR_UNSUPPORTED;
     a.n = n;
     a.total_tiles = (int)total;
-    if (!wide) {
-        if (wsrc.dry_run)
-            return QL_OK;  // no workspace
-        return launch_qgemm(ord[0]->lin.fmt, xf32, t, a, stream) == hipSuccess ? QL_OK : QL_ERR_HIP;
-    }
+    if (!wide)
+        return launch_tiled(ord[0]->lin.fmt, xf32, t, a, wsrc, stream);
 
     // Workspace: one exact, row-shifted fp16 copy per distinct activation
     // tensor (layers reading the same X share it)

@@ -788,3 +788,45 @@ def test_block_forward_few_rows_mixed_m(gpu, orc):
         torch.cuda.synchronize()
         for (M, N, K), e, Yr in zip(specs, entries, refs):
             assert rel_err(e[5].cpu().numpy(), Yr) <= 1e-5, (fmt, M, N, K)
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_tiled_kernel_k_parts(gpu, orc, fmt):
+    """The tiled exact kernel cuts long reductions into K parts when a call
+    has too few tiles for the GPU (partials added by the sum launch): fp32
+    activations at the single-linear workload's shape (64 x 1024 x 1024),
+    an odd block count (the last 64-k step is half a step) in the last
+    part, bf16 mid-M shapes forced onto the tiled kernel, and a split layer
+    with its epilogue applied by the sum launch.  Results repeat bit for
+    bit."""
+    torch, ql = gpu
+    cases = [(64, 1024, 1024, O.DT_F32), (40, 512, 2080, O.DT_F32), (7, 300, 4128, O.DT_F32),
+             (128, 2048, 8192, O.DT_BF16), (214, 1024, 4096, O.DT_BF16),
+             (256, 1536, 6144, O.DT_BF16)]
+    try:
+        for (M, N, K, xdt) in cases:
+            W, X = si.small_case(7500 + M + N + K + fmt, M, N, K, xdt)
+            codes, scales = quantize_both(gpu, orc, fmt, W)
+            ql.load().qlinear_force_path(ql.PATH_TILED if xdt == O.DT_BF16 else ql.PATH_AUTO)
+            Yg = forward_gpu(gpu, fmt, X, xdt, codes, scales, N)
+            Yr = orc.forward(fmt, X, xdt, codes, scales, N)
+            assert rel_err(Yg, Yr) <= (1e-5 if xdt == O.DT_F32 else 2e-6), (M, N, K, rel_err(Yg, Yr))
+            assert np.array_equal(Yg, forward_gpu(gpu, fmt, X, xdt, codes, scales, N))
+        # a split layer with bias, GELU and a residual, applied after the sum
+        M, N, K = 64, 1024, 1024
+        W, X = si.small_case(7600 + fmt, M, N, K, O.DT_F32)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        rng = np.random.default_rng(7601)
+        bias = (rng.standard_normal(N) * 0.5).astype(np.float32)
+        resid = rng.standard_normal((M, N)).astype(np.float32)
+        Y = torch.from_numpy(resid.copy()).cuda()
+        ql.forward_ep(fmt, dev_x(torch, X, O.DT_F32), torch.from_numpy(codes).cuda(),
+                      torch.from_numpy(scales.view(np.int16)).cuda(), N, Y=Y,
+                      bias=torch.from_numpy(bias).cuda(), act=ql.ACT_GELU, residual=Y)
+        torch.cuda.synchronize()
+        P = orc.forward(fmt, X, O.DT_F32, codes, scales, N)
+        Yr = orc.epilogue(P, bias, O.ACT_GELU, resid)
+        lim = 1.13 * 1e-5 * np.max(np.abs(P)) + 1e-6 * (np.abs(Yr) + np.max(np.abs(P)))
+        assert np.all(np.abs(Y.cpu().numpy().astype(np.float64) - Yr) <= lim)
+    finally:
+        ql.load().qlinear_force_path(ql.PATH_AUTO)
