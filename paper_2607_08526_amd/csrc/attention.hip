@@ -45,7 +45,12 @@ constexpr int KROW = DH + PAD;     // Ks row: one key
 // Vt row: one value channel, 34 words (= 2 mod 32 banks), so that the 16
 // rows of one phase of 8-byte operand reads land on distinct banks
 constexpr int VROW = BKEY + 4;
-constexpr int STAGE = (BKEY * KROW + DH * VROW) * 2;  // bytes
+constexpr int KBYTES = BKEY * KROW * 2, VBYTES = DH * VROW * 2;
+// The running maximum m may trail the true one: it moves only when a tile's
+// scores exceed it by more than 2^LAZY in the exponent (so p <= 2^LAZY), and
+// then the accumulators are rescaled; the quotient O / l is the same for any
+// m, and fp32 holds 2^LAZY * T easily.
+constexpr float LAZY = 8.0f;
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -56,15 +61,29 @@ __device__ inline uint32_t pack_bf16(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-__global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
+
+// Software pipeline over key tiles: while the softmax of tile j runs on the
+// VALU, the matrix cores form the scores of tile j + 1 (their K rows are
+// already in LDS), then take tile j's value product.  K and V tiles have
+// two LDS buffers each, filled one tile apart: during step j the K buffer
+// of tile j (read in step j - 1) receives tile j + 2 and the V buffer of
+// tile j - 1 receives tile j + 1, so one barrier per step suffices.
+__global__ __launch_bounds__(THREADS, 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attention_kernel(const AttnArgs a)
 {
-    __shared__ __align__(16) uint8_t lds[2 * STAGE];
+    __shared__ __align__(16) uint8_t lds[2 * KBYTES + 2 * VBYTES];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hf = lane >> 5;
     const int bh = blockIdx.y, b = bh / a.H, h = bh - b * a.H;
     const int T = a.T;
     const int64_t seq = (int64_t)b * T;  // first row of this sequence
     const int q = blockIdx.x * BQ + wave * 32 + l32;  // this lane's query
+    auto kbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + i * KBYTES); };
+    auto vbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + 2 * KBYTES + i * VBYTES); };
 
     // the query's B operands: head-dim chunk s, elements 16 s + 8 hf .. + 7
     bf16x8 qb[4];
@@ -82,37 +101,75 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
     // tile, elements 8 (t / 32) .. + 7.  V is written transposed, the two
     // keys of a row pair packed into one 32-bit word; with 32 row pairs per
     // wavefront those writes spread over the LDS banks (8 row pairs per
-    // wavefront put every write of an instruction into 8 banks)
+    // wavefront put every write of an instruction into 8 banks).  Keys at or
+    // beyond T repeat key T - 1 (their probabilities are set to 0).
     const int pr = tid >> 3, c8 = 8 * (tid & 7);
     const int vpr = tid & 31, vc8 = 8 * (tid >> 5);
     u32x4 pk[2], pv[2];
-    auto fetch = [&](int kt) {
+    const uint16_t *const kp = a.k + (seq + 2 * pr) * a.ldk + h * DH + c8;
+    const uint16_t *const vp = a.v + (seq + 2 * vpr) * a.ldv + h * DH + vc8;
+    // (a full tile's rows are the thread's first rows advanced by whole
+    // tiles; only the last tile's are clamped)
+    auto fetch_k = [&](int kt) {
+        if ((kt + 1) * BKEY <= T) {
+            const uint16_t *p = kp + (int64_t)kt * BKEY * a.ldk;
+            pk[0] = *reinterpret_cast<const u32x4 *>(p);
+            pk[1] = *reinterpret_cast<const u32x4 *>(p + a.ldk);
+        } else {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int key = kt * BKEY + 2 * pr + i;
-            u32x4 zk = {0u, 0u, 0u, 0u}, zv = zk;
-            if (key < T) {
-                zk = *reinterpret_cast<const u32x4 *>(a.k + (seq + key) * a.ldk + h * DH + c8);
+            for (int i = 0; i < 2; ++i) {
+                const int key = min(kt * BKEY + 2 * pr + i, T - 1) - 2 * pr;
+                pk[i] = *reinterpret_cast<const u32x4 *>(kp + (int64_t)key * a.ldk);
             }
-            const int vkey = kt * BKEY + 2 * vpr + i;
-            if (vkey < T)
-                zv = *reinterpret_cast<const u32x4 *>(a.v + (seq + vkey) * a.ldv + h * DH + vc8);
-            pk[i] = zk;
-            pv[i] = zv;
         }
     };
-    auto put = [&](int buf) {
-        uint16_t *ks = reinterpret_cast<uint16_t *>(lds + buf * STAGE);
-        uint16_t *vt = ks + BKEY * KROW;
+    auto fetch_v = [&](int kt) {
+        if ((kt + 1) * BKEY <= T) {
+            const uint16_t *p = vp + (int64_t)kt * BKEY * a.ldv;
+            pv[0] = *reinterpret_cast<const u32x4 *>(p);
+            pv[1] = *reinterpret_cast<const u32x4 *>(p + a.ldv);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int key = min(kt * BKEY + 2 * vpr + i, T - 1) - 2 * vpr;
+                pv[i] = *reinterpret_cast<const u32x4 *>(vp + (int64_t)key * a.ldv);
+            }
+        }
+    };
+    auto put_k = [&](uint16_t *ks) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
             *reinterpret_cast<u32x4 *>(ks + (2 * pr + i) * KROW + c8) = pk[i];
+    };
+    auto put_v = [&](uint16_t *vt) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const uint32_t lo = (pv[0][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
             const uint32_t hi = (pv[1][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
             *reinterpret_cast<uint32_t *>(vt + (vc8 + e) * VROW + 2 * vpr) = lo | (hi << 16);
         }
+    };
+    // scores of this lane's query against keys 32 sub + 8 (r / 4) + 4 hf + r % 4
+    // (all eight K fragments are read before the first MFMA)
+    auto scores = [&](const uint16_t *ks, f32x16 (&sc)[2]) {
+        bf16x8 ka[4][2];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int sub = 0; sub < 2; ++sub)
+                ka[s][sub] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4 *>(ks + (32 * sub + l32) * KROW +
+                                                             16 * s + 8 * hf));
+        const f32x16 zero = {};
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+            sc[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0][sub], qb[0], zero, 0, 0, 0);
+#pragma unroll
+        for (int s = 1; s < 4; ++s)
+#pragma unroll
+            for (int sub = 0; sub < 2; ++sub)
+                sc[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s][sub], qb[s], sc[sub], 0,
+                                                                  0, 0);
     };
 
     f32x16 oacc[2];
@@ -122,55 +179,49 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
         for (int r = 0; r < 16; ++r)
             oacc[t][r] = 0.0f;
     float mrun = -INFINITY, lrun = 0.0f;
+    const float c = a.scale_log2e;  // p = 2^(s c - m c), c >= 0
 
-    const int nkt = (T + BKEY - 1) / BKEY;
-    fetch(0);
-    put(0);
-    __syncthreads();
-    for (int kt = 0; kt < nkt; ++kt) {
-        if (kt + 1 < nkt)
-            fetch(kt + 1);
-        const uint16_t *ks = reinterpret_cast<const uint16_t *>(lds + (kt & 1) * STAGE);
-        const uint16_t *vt = ks + BKEY * KROW;
-
-        // scores of this lane's query against keys 32 sub + 8 (r / 4) + 4 hf + r % 4
-        f32x16 sc[2];
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-            f32x16 acc;
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                acc[r] = 0.0f;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const bf16x8 ka = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4 *>(ks + (32 * sub + l32) * KROW +
-                                                             16 * s + 8 * hf));
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[s], acc, 0, 0, 0);
-            }
-            sc[sub] = acc;
-        }
-        // running maximum of the raw scores (keys beyond T excluded; the
-        // scale c = scale * log2 e >= 0 is applied inside the exponent:
-        // p = 2^(s c - m c))
-        const bool tail = (kt + 1) * BKEY > T;
+    // Softmax of one tile's scores and its value product, in two parts so
+    // that the next tile's score MFMAs can be placed between them.  TAIL:
+    // the last, partial tile (keys at or beyond T get p = 0).
+    float alpha = 0.0f;
+    auto tile_max = [&](auto tailc, int kt, const f32x16 (&sc)[2]) {
+        constexpr bool TAIL = decltype(tailc)::value;
         auto valid = [&](int sub, int r) {
-            return kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3) < T;
+            return !TAIL || kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3) < T;
         };
-        float mt = -INFINITY;
+        // tile maximum: four independent chains (the compiler forms v_max3)
+        float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                mt = fmaxf(mt, !tail || valid(sub, r) ? sc[sub][r] : -INFINITY);
+                mx[r & 3] = fmaxf(mx[r & 3], valid(sub, r) ? sc[sub][r] : -INFINITY);
+        float mt = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
         mt = fmaxf(mt, __shfl_xor(mt, 32));
-        const float c = a.scale_log2e;
-        const float mnew = fmaxf(mrun, mt);
-        const float alpha = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mrun - mnew) * c);
+        // move the maximum only when some lane of the wavefront needs it
+        const bool up = mrun == -INFINITY || (mt - mrun) * c > LAZY;
+        const bool any_up = __ballot(up) != 0;
+        const float mnew = any_up ? fmaxf(mrun, mt) : mrun;
+        alpha = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((mrun - mnew) * c);
         mrun = mnew;
-        const float mc = mnew * c;
-        float ls = 0.0f;
-        u32x4 pb[2][2];  // P^T operands: [sub][chunk c], 8 bf16 each
+        lrun *= alpha;
+        if (any_up) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    oacc[t][r] *= alpha;
+        }
+    };
+    auto tile_pv = [&](auto tailc, int kt, const f32x16 (&sc)[2], const uint16_t *vt) {
+        constexpr bool TAIL = decltype(tailc)::value;
+        auto valid = [&](int sub, int r) {
+            return !TAIL || kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3) < T;
+        };
+        const float mc = mrun * c;
+        float ls[4];
+        u32x4 pb[2][2];  // P^T operands: [sub][chunk], 8 bf16 each
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
@@ -181,26 +232,21 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
                     const int r0 = 8 * ch + 2 * e;
                     float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][r0], c, -mc));
                     float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][r0 + 1], c, -mc));
-                    if (tail) {
+                    if (TAIL) {
                         p0 = valid(sub, r0) ? p0 : 0.0f;
                         p1 = valid(sub, r0 + 1) ? p1 : 0.0f;
                     }
-                    ls += p0 + p1;
+                    ls[e] = sub == 0 && ch == 0 ? p0 + p1 : ls[e] + (p0 + p1);
                     w[e] = pack_bf16(p0, p1);
                 }
                 pb[sub][ch] = u32x4{w[0], w[1], w[2], w[3]};
             }
-        lrun = lrun * alpha + ls;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                oacc[t][r] *= alpha;
+        lrun += (ls[0] + ls[1]) + (ls[2] + ls[3]);
         // O^T += V^T P^T over the four 16-key chunks
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int kc = 0; kc < 4; ++kc)
 #pragma unroll
-            for (int kc = 0; kc < 4; ++kc) {
+            for (int t = 0; t < 2; ++t) {
                 const uint16_t *row = vt + (32 * t + l32) * VROW + 16 * kc + 4 * hf;
                 const u32x2 lo = *reinterpret_cast<const u32x2 *>(row);
                 const u32x2 hi = *reinterpret_cast<const u32x2 *>(row + 8);
@@ -208,9 +254,55 @@ __global__ __launch_bounds__(THREADS, 2) void attention_kernel(const AttnArgs a)
                 oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     va, __builtin_bit_cast(bf16x8, pb[kc >> 1][kc & 1]), oacc[t], 0, 0, 0);
             }
-        if (kt + 1 < nkt)
-            put((kt + 1) & 1);
-        __syncthreads();
+    };
+
+    const int nkt = (T + BKEY - 1) / BKEY;
+    fetch_k(0);
+    fetch_v(0);
+    put_k(kbuf(0));
+    put_v(vbuf(0));
+    if (nkt > 1) {
+        fetch_k(1);
+        put_k(kbuf(1));
+    }
+    __syncthreads();
+    // one step: tile kt, whose scores are in cur (it is full, and tile kt + 1
+    // exists); the scores of tile kt + 1 go to nxt
+    auto step = [&](int kt, const f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+        __syncthreads();  // K of tile kt + 1 and V of tile kt are in LDS
+        if (kt + 2 < nkt)
+            fetch_k(kt + 2);
+        fetch_v(kt + 1);
+        tile_max(Flag<false>{}, kt, cur);
+        scores(kbuf((kt + 1) & 1), nxt);
+        tile_pv(Flag<false>{}, kt, cur, vbuf(kt & 1));
+        if (kt + 2 < nkt)
+            put_k(kbuf(kt & 1));
+        put_v(vbuf((kt + 1) & 1));
+    };
+    auto last = [&](int kt, const f32x16 (&cur)[2]) {
+        __syncthreads();  // V of the last tile is in LDS
+        if (nkt * BKEY > T) {
+            tile_max(Flag<true>{}, kt, cur);
+            tile_pv(Flag<true>{}, kt, cur, vbuf(kt & 1));
+        } else {
+            tile_max(Flag<false>{}, kt, cur);
+            tile_pv(Flag<false>{}, kt, cur, vbuf(kt & 1));
+        }
+    };
+    // two score buffers in turn (no copies between steps)
+    f32x16 sa[2], sb[2];
+    scores(kbuf(0), sa);
+    int kt = 0;
+    for (; kt + 2 < nkt; kt += 2) {
+        step(kt, sa, sb);
+        step(kt + 1, sb, sa);
+    }
+    if (kt + 1 < nkt) {
+        step(kt, sa, sb);
+        last(kt + 1, sb);
+    } else {
+        last(kt, sa);
     }
 
     // normalize and store: channel 32 t + 8 (r / 4) + 4 hf + r % 4 of query q
