@@ -20,9 +20,11 @@
 //
 // Grouping.  One launch takes up to QL_MAX_GROUP layers of one format and
 // one row count (a DiT block's four linears): layer i owns the workgroups
-// begin[i] .. begin[i + 1] - 1.  The blocks per lane (a template bound) are
-// those of the longest K.  A layer with fewer blocks still issues every
-// load, so that they all go out at once: its lanes past the row's end all
+// begin[i] .. begin[i + 1] - 1 (the host lists the longest rows first).  The
+// blocks per lane (a template bound) are those of the longest K.  A layer
+// whose rows fit one block per lane runs a one-block body with twice the
+// rows per wavefront instead; a layer in between still issues every load of
+// the bound, so that they all go out at once: its lanes past the row's end
 // load the row's last block (one line per wavefront) and skip it.
 //
 // Requirements (checked by the host): M <= 4, K % 256 == 0, M * K <= 32768
@@ -245,14 +247,29 @@ __global__ __launch_bounds__(64 * WAVES) void qgemv_kernel(const LinDesc d)
     gemv_body<FMT, MM, RPW, BPL>(d, (int)blockIdx.x);
 }
 
+// rows per wavefront for a layer of the group: a layer whose rows fit one
+// block per lane takes twice the group's rows per wavefront (the same
+// registers as the longer layers' blocks, and half the workgroups)
+template <int RPW, int BPL>
+__host__ __device__ inline int group_rpw(int K)
+{
+    return BPL > 1 && K / 32 <= 64 ? 2 * RPW : RPW;
+}
+
 template <int FMT, int MM, int RPW, int BPL>
 __global__ __launch_bounds__(64 * WAVES) void qgemv_group_kernel(const LayerGroup grp)
 {
-    // this workgroup's layer (wave-uniform) and its index within the layer
+    // this workgroup's layer (wave-uniform) and its index within the layer;
+    // a layer of one block per lane runs the one-block body (its loads and
+    // registers only)
     int li = 0;
     while (li + 1 < grp.n && (int)blockIdx.x >= grp.begin[li + 1])
         ++li;
-    gemv_body<FMT, MM, RPW, BPL>(grp.d[li], (int)blockIdx.x - grp.begin[li]);
+    const int wg = (int)blockIdx.x - grp.begin[li];
+    if (group_rpw<RPW, BPL>(grp.d[li].K) != RPW)
+        gemv_body<FMT, MM, 2 * RPW, 1>(grp.d[li], wg);
+    else
+        gemv_body<FMT, MM, RPW, BPL>(grp.d[li], wg);
 }
 
 template <int FMT, int MM, int RPW, int BPL>
@@ -272,17 +289,22 @@ hipError_t launch_bpl(const LayerGroup &g0, hipStream_t s)
     LayerGroup g = g0;
     int nbmax = 0;
     size_t lds = 0;
-    g.begin[0] = 0;
     for (int i = 0; i < g.n; ++i) {
         const LinDesc &d = g.d[i];
         const int nb = d.K / 32;
         nbmax = std::max(nbmax, nb);
         lds = std::max(lds, (size_t)d.M * d.K * 2 +
                                 (FMT == QL_FMT_Q4 ? (size_t)d.M * nb * 4 : 0));
-        g.begin[i + 1] = g.begin[i] + (d.N + WAVES * RPW - 1) / (WAVES * RPW);
+    }
+    const int bpl = (nbmax + 63) / 64;
+    // workgroups per layer: rows per wavefront as the group kernel takes them
+    g.begin[0] = 0;
+    for (int i = 0; i < g.n; ++i) {
+        const int rpw = g.n > 1 && bpl > 1 && g.d[i].K / 32 <= 64 ? 2 * RPW : RPW;
+        g.begin[i + 1] = g.begin[i] + (g.d[i].N + WAVES * rpw - 1) / (WAVES * rpw);
     }
     const dim3 grid((unsigned)g.begin[g.n]);
-    switch ((nbmax + 63) / 64) {
+    switch (bpl) {
     case 1: launch_one<FMT, MM, RPW, 1>(g, grid, lds, s); break;
     case 2: launch_one<FMT, MM, RPW, 2>(g, grid, lds, s); break;
     case 3: launch_one<FMT, MM, RPW, 3>(g, grid, lds, s); break;

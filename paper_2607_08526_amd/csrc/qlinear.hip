@@ -537,6 +537,10 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc
                 g.d[g.n++] = ds[j];
                 done[j] = true;
             }
+        // longest rows first: their workgroups carry the most bytes, and
+        // the short ones then fill the launch's tail
+        std::stable_sort(g.d, g.d + g.n,
+                         [](const LinDesc &x, const LinDesc &y) { return x.K > y.K; });
         if (launch_qgemv(fmt, g, stream) != hipSuccess)
             return QL_ERR_HIP;
     }
