@@ -345,7 +345,10 @@ def forward_ep(fmt, X, codes, scales, N, Y=None, bias=None, act=ACT_NONE, residu
 
 def make_group(entries):
     """ctypes array for block_forward from (fmt, X, codes, scales, N, Y) tuples.
-    The tensors must outlive every use of the returned array."""
+    The array holds the device addresses of the tensors and keeps references
+    to the tensors themselves, so they live as long as the array (a freed
+    tensor's memory may be returned to the driver, e.g. when a graph capture
+    empties torch's cache, and a later launch would then fault)."""
     if not 1 <= len(entries) <= MAX_GROUP:
         raise ValueError(f"a group holds 1 to {MAX_GROUP} linears, not {len(entries)}")
     arr = (_Linear * len(entries))()
@@ -356,6 +359,7 @@ def make_group(entries):
         _on_device(X, codes, scales, Y)
         arr[i] = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                          scales.data_ptr() if scales is not None else 0, Y.data_ptr())
+    arr._tensors = [tuple(e) for e in entries]
     return arr
 
 
@@ -372,7 +376,8 @@ def make_group_ep(entries):
     """ctypes array for block_forward_ep from (fmt, X, codes, scales, N, Y,
     bias, act, residual[, steer[, ycopy]]) tuples (bias/residual/steer/ycopy
     None for none; Y fp32 or bf16; ycopy a bf16 [M][N] copy of an fp32 Y).
-    The tensors must outlive every use of the returned array."""
+    The array keeps references to every tensor it points to (see
+    make_group)."""
     if not 1 <= len(entries) <= MAX_GROUP:
         raise ValueError(f"a group holds 1 to {MAX_GROUP} linears, not {len(entries)}")
     arr = (_LinearEp * len(entries))()
@@ -390,6 +395,7 @@ def make_group_ep(entries):
         lin = _Linear(fmt, X.data_ptr(), _xdt(X), M, K, N, codes.data_ptr(),
                       scales.data_ptr() if scales is not None else 0, Y.data_ptr())
         arr[i] = _LinearEp(lin, _epilogue(Y, bias, act, residual, steer, ycopy))
+    arr._tensors = [tuple(e) for e in entries]
     return arr
 
 

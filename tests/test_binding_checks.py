@@ -141,3 +141,28 @@ def test_attention_rejects():
         ql.attention(qkv[:, ::3], k, v, B, T, H)
     with pytest.raises(ValueError):  # host tensors
         ql.attention(q, k, v, B, T, H)
+
+
+def test_groups_keep_their_tensors(monkeypatch):
+    """A group array holds only device addresses; it must also keep the
+    tensors alive, or a tensor dropped by the caller could have its memory
+    handed back to the driver (torch empties its cache when a graph capture
+    begins) while the group still points at it.  Host tensors stand in for
+    device ones here: the device check is switched off and nothing is
+    launched."""
+    import gc
+    import weakref
+    monkeypatch.setattr(ql, "_on_device", lambda *a: None)
+    codes, scales = weights()
+    X, Y = x_bf16(), torch.zeros((M, N), dtype=torch.float32)
+    bias, strength, d = torch.zeros(N), torch.zeros(1), torch.zeros(N)
+    refs = [weakref.ref(t) for t in (codes, scales, X, Y, bias, strength, d)]
+    g = ql.make_group([(ql.FMT_INT8, X, codes, scales, N, Y)])
+    ge = ql.make_group_ep([(ql.FMT_INT8, X, codes, scales, N, Y, bias, ql.ACT_NONE, None,
+                            (d, 3.0, strength))])
+    del codes, scales, X, Y, bias, strength, d
+    gc.collect()
+    assert all(r() is not None for r in refs)
+    del g, ge
+    gc.collect()
+    assert all(r() is None for r in refs)
