@@ -184,9 +184,9 @@ def test_epilogue_gelu_special_values(gpu, orc):
 
 def test_block_forward_ep_grouped(gpu, orc):
     """One grouped call with a different epilogue per layer: the fp16 path's
-    grouped launch with K parts summed by the last part to arrive (mixed
-    reduction lengths over two activations), and a small-M group on the
-    streaming kernels."""
+    grouped launch with K parts (mixed reduction lengths over two
+    activations; summed by the separate launch, which applies the
+    epilogues), and a small-M group on the streaming kernels."""
     torch, ql = gpu
     for M, shapes in ((384, [(700, 512), (256, 4096), (1000, 512)]),
                       (24, [(3072, 1024), (1024, 4096), (4096, 1024)])):
@@ -291,3 +291,69 @@ def test_epilogue_bf16_copy_every_path(gpu, orc, fmt, xdt, M, N, K):
     with pytest.raises(ql.QLinearError) as err:
         ql.forward_ep(fmt, Xd, cd, sd, N, Y=Y, residual=Y, ycopy=alias)
     assert err.value.status == 1
+
+
+def test_block_forward_ep_in_kernel_reduction(gpu, orc):
+    """A DiT block at d = 1024 and 768 tokens, the shape class (a few hundred
+    to ~1500 tokens) whose split plan adds the K parts inside the large-M
+    kernel: more parts than one wave of workgroups (FFN-down in 4 parts of
+    16 steps, the other layers in 2 of 8), each part stores its partial
+    tile, and the last part to arrive adds them in part order and applies
+    the layer's epilogue (QKV + bias -> bf16; out-projection + bias + a
+    residual; FFN-up + bias -> GELU -> bf16; FFN-down + bias added in place
+    into its residual with a bf16 copy).  Every output starts NaN-filled and
+    must be finite everywhere; 64 rows (one in every 128-row tile) x all
+    columns against the oracle; the copy equals the rounded fp32 output bit
+    for bit; a second call repeats the first bit for bit."""
+    torch, ql = gpu
+    M, d = 768, 1024
+    rng = np.random.default_rng(3500)
+    rows = np.array(sorted({0, M - 1} | {int(rng.integers(t, t + 128)) for t in range(0, M, 128)}
+                           | set(rng.choice(M, 56, replace=False).tolist())), dtype=np.int64)
+    _, xa = si.small_case(3501, M, 1, d)
+    _, xb = si.small_case(3502, M, 1, 4 * d)
+    for fmt in (O.FMT_Q4, O.FMT_INT8):
+        entries, refs = [], []
+        copy = torch.full((M, d), -1, dtype=torch.int16, device="cuda")
+        for i, (_, N, K) in enumerate(si.block_linears(d)):
+            W, _ = si.small_case(3510 + i, 1, N, K)
+            cd, sd = ql.quantize(fmt, dev_f32(torch, W))
+            cr, sr = orc.quantize(fmt, W)
+            X = xb if K == 4 * d else xa
+            bias = (rng.standard_normal(N) * 0.5).astype(np.float32)
+            act = O.ACT_GELU if i == 2 else O.ACT_NONE
+            resid = rng.standard_normal((M, N)).astype(np.float32) if i in (1, 3) else None
+            ybf16 = i in (0, 2)
+            if i == 3:
+                resid3 = resid
+                Y = dev_f32(torch, resid)  # in place, with its bf16 copy
+                rd, yc = Y, copy.view(torch.bfloat16)
+            else:
+                Y = torch.full((M, N), float("nan"), device="cuda",
+                               dtype=torch.bfloat16 if ybf16 else torch.float32)
+                rd, yc = (None if resid is None else dev_f32(torch, resid)), None
+            entries.append((fmt, dev_x(torch, X, O.DT_BF16), cd, sd, N, Y, dev_f32(torch, bias),
+                            act, rd, None, yc))
+            Pr = orc.forward(fmt, X, O.DT_BF16, cr, sr, N, rows=rows)
+            Yr = orc.epilogue(Pr, bias, act, None if resid is None else resid[rows])
+            refs.append((Pr, Yr, bias, ybf16))
+        g = ql.make_group_ep(entries)
+        ql.block_forward_ep(None, group=g)
+        torch.cuda.synchronize()
+        first = [e[5].clone() for e in entries] + [copy.clone()]
+        for e, (Pr, Yr, bias, yb) in zip(entries, refs):
+            assert bool(torch.isfinite(e[5].float()).all()), (fmt, e[4])
+            check(host_y(torch, e[5])[rows], Pr, Yr, bias, O.DT_BF16, yb, (fmt, e[4]))
+        assert torch.equal(copy.view(torch.bfloat16), entries[3][5].to(torch.bfloat16))
+        # again from the same inputs: NaN-filled outputs, the in-place layer
+        # back at its residual
+        for i, e in enumerate(entries):
+            if i == 3:
+                e[5].copy_(dev_f32(torch, resid3))
+            else:
+                e[5].fill_(float("nan"))
+        copy.fill_(-1)
+        ql.block_forward_ep(None, group=g)
+        torch.cuda.synchronize()
+        again = [e[5] for e in entries] + [copy]
+        assert all(torch.equal(a_, b_) for a_, b_ in zip(first, again)), fmt

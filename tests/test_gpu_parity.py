@@ -312,13 +312,43 @@ def test_forward_stored_extreme_codes_exact(gpu, orc, fmt):
 
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_in_kernel_reduction(gpu, orc, fmt):
+    """Single layers whose split plan adds the K parts inside the large-M
+    kernel (more parts than one wave of workgroups: 700 or 768 tokens x 2048
+    x 2048, 6 x 8 output tiles in 4 parts of 8 steps each; each part stores
+    its partial tile and the last part to arrive adds them in part order).
+    Every output starts NaN-filled; all rows against the oracle (700: a
+    ragged last row tile); a second call repeats the first bit for bit."""
+    torch, ql = gpu
+    N, K = 2048, 2048
+    W, _ = si.small_case(3600 + fmt, 1, N, K)
+    codes, scales = quantize_both(gpu, orc, fmt, W)
+    cd = torch.from_numpy(codes).cuda()
+    sd = torch.from_numpy(scales.view(np.int16)).cuda()
+    for M in (768, 700):
+        _, X = si.small_case(3610 + M, M, 1, K)
+        Xd = dev_x(torch, X, O.DT_BF16)
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        ql.forward(fmt, Xd, cd, sd, N, Y)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(Y).all()), M
+        Yg = Y.cpu().numpy()
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        assert rel_err(Yg, Yr) <= TOL[O.DT_BF16], M
+        Y.fill_(float("nan"))
+        ql.forward(fmt, Xd, cd, sd, N, Y)
+        torch.cuda.synchronize()
+        assert np.array_equal(Y.cpu().numpy(), Yg), M
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forward_split_reduction(gpu, orc, fmt):
     """Large-M shapes with few output tiles and long reductions, which the
-    fp16 path cuts into K parts: single layers that fit in one wave of
-    workgroups (parts summed by a separate launch) and a grouped call mixing
-    reduction lengths (parts summed by the last part to arrive); uneven last
-    parts (K / 64 not a multiple of the part length), ragged tiles; results
-    repeat bit for bit."""
+    fp16 path cuts into K parts summed by a separate launch (the plan when
+    all parts fit in one wave of workgroups): single layers and a grouped
+    call mixing reduction lengths over two activations; uneven last parts
+    (K / 64 not a multiple of the part length), ragged tiles; results repeat
+    bit for bit.  The in-kernel reduction has tests of its own."""
     torch, ql = gpu
     for (M, N, K) in ((300, 520, 4096), (129, 260, 8448), (2048, 64, 2304)):
         W, X = si.small_case(90 + M + N + K + fmt, M, N, K)
