@@ -841,23 +841,32 @@ def block_few_rows(torch, ql, si):
 
 
 def block_int8(torch, ql, si):
+    """One int8 block (d = 2048, 2048 tokens): a HIP graph of R block calls
+    over R copies of the weights (R x 53.5 MB >= 512 MB, past the last-level
+    cache, as the step's distinct blocks are), per call."""
     dev = torch.device("cuda")
     xa, xb = si.block_activations()
     xa_d = torch.from_numpy(xa.view("int16")).to(dev)
     xb_d = torch.from_numpy(xb.view("int16")).to(dev)
-    ents, wbytes = [], 0
+    q, wbytes = [], 0
     for i, (name, N, K) in enumerate(si.block_linears()):
         codes, scales = ql.quantize(ql.FMT_INT8, torch.from_numpy(si.block_int8_weight(i)).to(dev))
         wbytes += codes.numel() + 2 * scales.numel()
-        Y = torch.empty((xa.shape[0], N), dtype=torch.float32, device=dev)
-        ents.append((ql.FMT_INT8, xb_d if K == 4 * si.D_MODEL else xa_d, codes, scales, N, Y))
-    grp = ql.make_group(ents)
-    med, lo, hi = graph_time(torch, lambda: ql.block_forward(None, group=grp))
+        q.append((codes, scales, N, K))
+    R = max(1, -(-ROT_BYTES // wbytes))
+    Ys = [torch.empty((xa.shape[0], N), dtype=torch.float32, device=dev) for _, _, N, _ in q]
+    grps = []
+    for r in range(R):
+        ents = [(ql.FMT_INT8, xb_d if K == 4 * si.D_MODEL else xa_d,
+                 c if r == 0 else c.clone(), s_ if r == 0 else s_.clone(), N, Y)
+                for (c, s_, N, K), Y in zip(q, Ys)]
+        grps.append(ql.make_group(ents))
+    med = graph_time(torch, lambda: [ql.block_forward(None, group=g) for g in grps])[0] / R
     flops = sum(2.0 * xa.shape[0] * N * K for _, N, K in si.block_linears())
     t = med * 1e-3
     return {"us_per_block": round(med * 1e3, 2), "TFLOPs": round(flops / t / 1e12, 1),
             "mfma_frac": round(flops / t / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
-            "weight_GBps": round(wbytes / t / 1e9, 1)}
+            "weight_GBps": round(wbytes / t / 1e9, 1), "copies": R}
 
 
 # non-packed fp32 VALU lane operations per second: 256 CUs x 4 SIMDs x 16
@@ -870,7 +879,8 @@ INT8_MFMA_PEAK_TOPS = 5000.0
 def block_w8a8(torch, ql, si):
     """One DiT block (d = 2048, 2048 tokens) in W8A8: the per-token
     quantization of both activation tensors and the four int8 products, on
-    the same int8 weights and activations as block_int8; graph-timed."""
+    the same int8 weights and activations as block_int8; each part timed as
+    a HIP graph of R calls over R copies of the weights, per call."""
     dev = torch.device("cuda")
     xa, xb = si.block_activations()
     xa_d = torch.from_numpy(xa.view("int16")).to(dev)
@@ -883,23 +893,27 @@ def block_w8a8(torch, ql, si):
         ws.append(ql.quantize(ql.FMT_INT8, torch.from_numpy(si.block_int8_weight(i)).to(dev)))
         Ys.append(torch.empty((xa.shape[0], N), dtype=torch.float32, device=dev))
     wide = [K == 4 * si.D_MODEL for _, _, K in lin]
+    wbytes = sum(c.numel() + 2 * s_.numel() for c, s_ in ws)
+    R = max(1, -(-ROT_BYTES // wbytes))
+    wcopies = [ws] + [[(c.clone(), s_.clone()) for c, s_ in ws] for _ in range(R - 1)]
 
     def quant():
         ql.quantize_act(xa_d, qa, sa)
         ql.quantize_act(xb_d, qb, sb)
 
-    def gemms():
+    def gemms(w):
         for i, (_, N, K) in enumerate(lin):
             q, s_ = (qb, sb) if wide[i] else (qa, sa)
-            ql.forward_w8a8(q, s_, ws[i][0], ws[i][1], N, Y=Ys[i])
+            ql.forward_w8a8(q, s_, w[i][0], w[i][1], N, Y=Ys[i])
 
     def both():
-        quant()
-        gemms()
+        for w in wcopies:
+            quant()
+            gemms(w)
 
-    t_all = graph_time(torch, both)[0]
-    t_q = graph_time(torch, quant)[0]
-    t_g = graph_time(torch, gemms)[0]
+    t_all = graph_time(torch, both)[0] / R
+    t_q = graph_time(torch, lambda: [quant() for _ in range(R)])[0] / R
+    t_g = graph_time(torch, lambda: [gemms(w) for w in wcopies])[0] / R
     M = xa.shape[0]
     mnk = sum(M * N * K for _, N, K in lin)
     valu_floor_us = mnk / 16 / VALU_LANE_OPS * 1e6  # cvt + FMA per output per 32-k block
