@@ -299,7 +299,8 @@ int qlinear_steer(float *h, int64_t M, int64_t N, const float *dir, float hnorm,
  * h * dh (likewise K, V), so the fused [tokens][3 d] output of a QKV linear
  * is read in place (q = qkv, k = qkv + d, v = qkv + 2 d, ld = 3 d).  O: rows
  * of ldo elements, fp32 or bf16 (odt).  Head dimension 64 only
- * (QL_ERR_UNSUPPORTED otherwise); B * H <= 65535.  q, k, v 16-byte aligned
+ * (QL_ERR_UNSUPPORTED otherwise); B * H <= 65535, B * T < 2^31 and
+ * ceil(T / 128) * B * H < 2^31 (likewise).  q, k, v 16-byte aligned
  * with ld % 8 == 0; o 16-byte (fp32) or 8-byte (bf16) aligned with
  * ldo % 4 == 0.  The probabilities enter the value product rounded to bf16
  * (fp32 accumulation).  Asynchronous on `stream`. */

@@ -78,10 +78,17 @@ void attention_kernel(const AttnArgs a)
     __shared__ __align__(16) uint8_t lds[2 * KBYTES + 2 * VBYTES];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hf = lane >> 5;
-    const int bh = blockIdx.y, b = bh / a.H, h = bh - b * a.H;
-    const int T = a.T;
+    // workgroup p runs on XCD p % 8; each XCD takes a contiguous range of
+    // (sequence, head) pairs with all their query blocks, so each pair's
+    // K and V tiles are fetched into one XCD's L2 and re-read there by its
+    // query blocks (round-robin pairs would make every XCD fetch them all)
+    const int T = a.T, nq = (T + BQ - 1) / BQ;
+    const int G = (int)gridDim.x, p = (int)blockIdx.x;
+    const int gq = G >> 3, gr = G & 7, xcd = p & 7, idx = p >> 3;
+    const int L = xcd < gr ? xcd * (gq + 1) + idx : gr * (gq + 1) + (xcd - gr) * gq + idx;
+    const int bh = L / nq, qblk = L - bh * nq, b = bh / a.H, h = bh - b * a.H;
     const int64_t seq = (int64_t)b * T;  // first row of this sequence
-    const int q = blockIdx.x * BQ + wave * 32 + l32;  // this lane's query
+    const int q = qblk * BQ + wave * 32 + l32;  // this lane's query
     auto kbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + i * KBYTES); };
     auto vbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + 2 * KBYTES + i * VBYTES); };
 
@@ -330,7 +337,7 @@ void attention_kernel(const AttnArgs a)
 
 hipError_t launch_attention(const AttnArgs &a, hipStream_t stream)
 {
-    const dim3 grid((unsigned)((a.T + BQ - 1) / BQ), (unsigned)(a.B * a.H));
+    const dim3 grid((unsigned)((int64_t)(a.T + BQ - 1) / BQ * a.B * a.H));
     hipLaunchKernelGGL(attention_kernel, grid, dim3(THREADS), 0, stream, a);
     return hipGetLastError();
 }

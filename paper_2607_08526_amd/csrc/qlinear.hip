@@ -1075,8 +1075,8 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
         ldv < H * dh || ldo < H * dh)
         return QL_ERR_SHAPE;
     if (dh != 64 || B * T >= I31 || B * H > 65535 || ldq >= I31 || ldk >= I31 ||
-        ldv >= I31 || ldo >= I31)
-        return QL_ERR_UNSUPPORTED;
+        ldv >= I31 || ldo >= I31 || (T + 127) / 128 * B * H >= I31)  // one workgroup per
+        return QL_ERR_UNSUPPORTED;                                       // 128 queries
     if (!q || !k || !v || !o || !(scale >= 0.0f) || scale > 3.0e38f)
         return QL_ERR_INVALID;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || ldq % 8 || ldk % 8 ||
