@@ -8,11 +8,13 @@
 // rounded, by at most 2^-25 of the shifted scale.  The forward kernel
 // multiplies its fp32 results back by 2^e[m] exactly.
 //
-// One workgroup per row, the rows of every activation tensor of a call in
-// one launch; rows up to 16384 wide are read once and held in registers
-// between the max-reduction and the convert-and-store.  For the
-// q4 kernel each 8-k group is stored in the slot order of its weight
-// conversion (qgemm_wide.hip).
+// One wavefront per row (four rows per workgroup), the rows of every
+// activation tensor of a call in one launch; rows up to 16384 wide are read
+// once into the wavefront's registers (16-byte chunks, lane l taking chunks
+// l, l + 64, ...), reduced to the row maximum by lane exchanges (no
+// barrier), then converted and stored.  Wider rows take one workgroup per
+// row and two passes.  For the q4 kernel each 8-k group is stored in the
+// slot order of its weight conversion (qgemm_wide.hip).
 #include "internal.h"
 
 namespace qlk {
@@ -24,6 +26,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ inline uint32_t bf16_absmax2(uint32_t v)
 {
     return max(v & 0x7FFFu, (v >> 16) & 0x7FFFu);
+}
+
+// the shift e of a row whose largest |x| has the bf16 bit pattern mx:
+// exponent of the row maximum (bf16: value in [2^(E-127), 2^(E-126)));
+// zero, subnormal-only or non-finite rows keep e = 0
+__device__ inline int shift_of(uint32_t mx)
+{
+    const int E = (int)(mx >> 7);
+    return (E >= 1 && E <= 254) ? (E - 127) - 14 : 0;
 }
 
 // largest |x| of the row, compared as bf16 bit patterns (monotone for
@@ -38,10 +49,7 @@ __device__ inline int row_shift(uint32_t mx, int *rexp, int m)
         wmax[threadIdx.x >> 6] = mx;
     __syncthreads();
     mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
-    // exponent of the row maximum (bf16: value in [2^(E-127), 2^(E-126)));
-    // zero, subnormal-only or non-finite rows keep e = 0
-    const int E = (int)(mx >> 7);
-    const int e = (E >= 1 && E <= 254) ? (E - 127) - 14 : 0;
+    const int e = shift_of(mx);
     if (threadIdx.x == 0)
         rexp[m] = e;
     return e;
@@ -68,13 +76,59 @@ __device__ inline u32x4 to_f16(u32x4 v, int e)
     return __builtin_bit_cast(u32x4, h);
 }
 
-// R > 0: the row (K / 8 16-byte chunks <= 256 * R) is read once into
-// registers.  R == 0: any K, a max pass and a convert pass (the second read
-// of the row hits L2).  Workgroup b converts row b - row_begin[i] of job i
-// (all activation tensors of a call in one launch).
-template <int R, bool SLOTS>
-__global__ __launch_bounds__(256) void xprep_kernel(const XprepArgs a, int *__restrict__ zero,
-                                                    int nzero)
+// C chunks of 16 bytes per lane (K / 8 <= 64 C): wavefront w of workgroup
+// b converts global row 4 b + w, i.e. row r - row_begin[i] of job i (all
+// activation tensors of a call in one launch, rows numbered consecutively).
+template <int C, bool SLOTS>
+__global__ __launch_bounds__(256) void xprep_wave_kernel(const XprepArgs a, int rows,
+                                                         int *__restrict__ zero, int nzero)
+{
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < nzero; i += 256)
+            zero[i] = 0;
+    const int r = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (r >= rows)
+        return;  // the whole wavefront
+    int ji = 0;
+#pragma unroll
+    for (int i = 1; i < QL_MAX_GROUP; ++i)
+        if (i < a.n && r >= a.row_begin[i])
+            ji = i;
+    const XprepJob &jb = a.j[ji];
+    const int m = r - a.row_begin[ji], K = jb.K, n16 = K / 8;
+    const u32x4 *row = reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint16_t *>(jb.X) +
+                                                       (int64_t)m * K);
+    u32x4 *out = reinterpret_cast<u32x4 *>(jb.Xh + (int64_t)m * K);
+    u32x4 v[C];
+    uint32_t mx = 0;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int i = lane + 64 * c;
+        v[c] = i < n16 ? row[i] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            mx = max(mx, bf16_absmax2(v[c][j]));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
+    const int e = shift_of(mx);
+    if (lane == 0)
+        jb.rexp[m] = e;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int i = lane + 64 * c;
+        if (i < n16)
+            out[i] = to_f16<SLOTS>(v[c], e);
+    }
+}
+
+// Rows wider than 16384: one workgroup per row, a max pass and a convert
+// pass (the second read of the row hits L2).  Workgroup b converts row
+// b - row_begin[i] of job i.
+template <bool SLOTS>
+__global__ __launch_bounds__(256) void xprep_row_kernel(const XprepArgs a, int *__restrict__ zero,
+                                                        int nzero)
 {
     const int b = blockIdx.x;
     if (b == 0)
@@ -91,36 +145,16 @@ __global__ __launch_bounds__(256) void xprep_kernel(const XprepArgs a, int *__re
     const u32x4 *row = reinterpret_cast<const u32x4 *>(X + (int64_t)m * K);
     u32x4 *out = reinterpret_cast<u32x4 *>(jb.Xh + (int64_t)m * K);
     const int n16 = K / 8;
-    const int t = threadIdx.x;
     uint32_t mx = 0;
-    if (R > 0) {
-        u32x4 v[R > 0 ? R : 1];
+    for (int i = threadIdx.x; i < n16; i += 256) {
+        const u32x4 v = row[i];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int i = t + r * 256;
-            v[r] = i < n16 ? row[i] : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                mx = max(mx, bf16_absmax2(v[r][j]));
-        }
-        const int e = row_shift(mx, jb.rexp, m);
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int i = t + r * 256;
-            if (i < n16)
-                out[i] = to_f16<SLOTS>(v[r], e);
-        }
-    } else {
-        for (int i = t; i < n16; i += 256) {
-            const u32x4 v = row[i];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                mx = max(mx, bf16_absmax2(v[j]));
-        }
-        const int e = row_shift(mx, jb.rexp, m);
-        for (int i = t; i < n16; i += 256)
-            out[i] = to_f16<SLOTS>(row[i], e);
+        for (int j = 0; j < 4; ++j)
+            mx = max(mx, bf16_absmax2(v[j]));
     }
+    const int e = row_shift(mx, jb.rexp, m);
+    for (int i = threadIdx.x; i < n16; i += 256)
+        out[i] = to_f16<SLOTS>(row[i], e);
 }
 
 template <bool SLOTS>
@@ -128,17 +162,22 @@ void launch_xprep_t(const XprepArgs &a, int rows, int maxK, int *zero, int nzero
                     hipStream_t stream)
 {
     const int n16 = maxK / 8;
-    const dim3 grid((unsigned)rows), block(256);
-    if (n16 <= 256)
-        hipLaunchKernelGGL((xprep_kernel<1, SLOTS>), grid, block, 0, stream, a, zero, nzero);
-    else if (n16 <= 512)
-        hipLaunchKernelGGL((xprep_kernel<2, SLOTS>), grid, block, 0, stream, a, zero, nzero);
-    else if (n16 <= 1024)
-        hipLaunchKernelGGL((xprep_kernel<4, SLOTS>), grid, block, 0, stream, a, zero, nzero);
-    else if (n16 <= 2048)
-        hipLaunchKernelGGL((xprep_kernel<8, SLOTS>), grid, block, 0, stream, a, zero, nzero);
+    const dim3 block(256), wgrid((unsigned)((rows + 3) / 4));
+    if (n16 <= 64 * 4)
+        hipLaunchKernelGGL((xprep_wave_kernel<4, SLOTS>), wgrid, block, 0, stream, a, rows, zero,
+                           nzero);
+    else if (n16 <= 64 * 8)
+        hipLaunchKernelGGL((xprep_wave_kernel<8, SLOTS>), wgrid, block, 0, stream, a, rows, zero,
+                           nzero);
+    else if (n16 <= 64 * 16)
+        hipLaunchKernelGGL((xprep_wave_kernel<16, SLOTS>), wgrid, block, 0, stream, a, rows, zero,
+                           nzero);
+    else if (n16 <= 64 * 32)
+        hipLaunchKernelGGL((xprep_wave_kernel<32, SLOTS>), wgrid, block, 0, stream, a, rows, zero,
+                           nzero);
     else
-        hipLaunchKernelGGL((xprep_kernel<0, SLOTS>), grid, block, 0, stream, a, zero, nzero);
+        hipLaunchKernelGGL((xprep_row_kernel<SLOTS>), dim3((unsigned)rows), block, 0, stream, a,
+                           zero, nzero);
 }
 
 }  // namespace
