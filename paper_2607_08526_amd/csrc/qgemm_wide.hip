@@ -43,8 +43,12 @@
 //
 // Memory pipeline: activations, codes and scales move from global memory to
 // LDS with the gfx950 direct-to-LDS loads (no VGPRs, no VALU), through a ring
-// of NST stages of 64 k each (two scale blocks); a stage is issued NST - 1
-// steps before it is consumed.  Each lane's offset within the tile is
+// of NST stages of 64 k each (two scale blocks).  The step barrier sits
+// before the last 16-k chunk of a step: by then every wavefront has read
+// all of the step's slot, so that slot is refilled at once (with the step
+// NST ahead), and the last chunk's MFMAs run while the next step's first
+// operands are read and converted (no stall between steps).  Each lane's
+// offset within the tile is
 // computed once; per step only the wave-uniform base (an SGPR pair)
 // advances.  The loads are issued from inline asm so that the compiler's
 // wait insertion, which cannot tell the ring stages apart and would drain
@@ -105,11 +109,13 @@ constexpr int WGS_PER_CU = MSUB * NSUB > 8 || WAVES == 8 ? 1 : 2;
 template <int FMT>
 constexpr int wgs_per_cu() { return FMT == QL_FMT_F16 ? 1 : WGS_PER_CU; }
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
+// epilogue use of the ring (after the main loop): the split arrival flag at
+// byte 0, the tile's row shifts from byte 256, the wavefronts' 4 KB store
+// patches from PATCH_AT
+constexpr int PATCH_AT = (256 + BM * 4 + 1023) / 1024 * 1024;
 
 template <int FMT>
 struct Geo {
-    // ring depth (LDS budget)
-    static constexpr int NST = wgs_per_cu<FMT>() == 1 || FMT == QL_FMT_Q4 ? 3 : 2;
     static constexpr int XBYTES = BM * 64 * 2;                 // activations per stage
     static constexpr int CROW = FMT == QL_FMT_INT8 ? 64 : FMT == QL_FMT_Q4 ? 32 : 128;  // weight
                                                                // bytes per row per stage
@@ -120,6 +126,9 @@ struct Geo {
     // row every 4 steps, into a 2-slot ring; a per-step load would cost one
     // memory request per row for 4 bytes
     static constexpr int SGROUP = 4, SSLOT = FMT == QL_FMT_F16 ? 0 : BN * 16;
+    // ring depth: three stages where the LDS budget of the resident
+    // workgroups allows them, else two
+    static constexpr int NST = wgs_per_cu<FMT>() * (3 * STAGE + 2 * SSLOT) <= 160 * 1024 ? 3 : 2;
     static constexpr int XLOADS = XBYTES / 16 / THREADS;
     static constexpr int CLOADS = CBYTES / 16 / THREADS;
     static constexpr int SPT = FMT == QL_FMT_F16 ? 0 : BN / THREADS;  // scale chunks per
@@ -244,9 +253,9 @@ struct Ctx {
     int f[NSUB];  // weight row (wave * WN + j * 32 + l32) enters as W * 2^f[j]
 };
 
-// Issue the direct-to-LDS loads of step s into one ring stage (and, every
-// SGROUP steps, the scales of steps s .. s + 3 into their ring slot).
-template <int FMT>
+// Issue the direct-to-LDS loads of step s into one ring stage, and with
+// SCALES (s % 4 == 0) the scales of steps s .. s + 3 into their ring slot.
+template <int FMT, bool SCALES>
 __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
 {
     using G = Geo<FMT>;
@@ -259,7 +268,7 @@ __device__ inline void issue_stage(const Ctx<FMT> &c, uint8_t *stage, int s)
 #pragma unroll
     for (int r = 0; r < G::CLOADS; ++r)
         dma16(cb, c.coff[r], base + G::XBYTES + (r * THREADS + c.wave * 64) * 16);
-    if (s % G::SGROUP == 0) {
+    if constexpr (SCALES) {
         const int g = s / G::SGROUP;
 #pragma unroll
         for (int h = 0; h < G::SPT; ++h)
@@ -307,78 +316,193 @@ __device__ inline uint32_t deq_word(const uint32_t *raw, int q, int w, half2v sp
     }
 }
 
-// One 64-k step.  Per weight fragment j the lane reads its 32 codes (one
-// block) and its block's scale once.  Per 16-k chunk q the wavefront issues
-// 4 x 2 MFMAs; behind each MFMA, in a group the compiler may not reorder,
-// go one word of the next chunk's weight dequantization and (every other
-// MFMA) one of the next chunk's activation fragment reads, so that the
-// matrix core runs while the VALU and LDS prepare the next operands.
+// An empty statement that the compiler keeps in order with the scheduling
+// barriers: a value passed through it is computed in the MFMA group it is
+// written in.  (Without it, the optimizer sinks a chunk's weight words
+// below its last MFMA, next to the vector they are assembled into, and the
+// VALU work that should overlap the MFMAs runs in one block after them.)
+__device__ inline uint32_t pin(uint32_t v)
+{
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// Operands carried from one 16-k chunk to the next, and across the step
+// boundary: the step's raw codes and scale pairs (one 32-k block per lane
+// and weight fragment j), and the activation and dequantized weight
+// fragments of the chunk about to be multiplied.
 template <int FMT>
-__device__ inline void compute_stage(const Ctx<FMT> &c, const uint8_t *stage, int s,
-                                     f32x16 (&acc)[MSUB][NSUB])
+struct Ops {
+    uint32_t raw[NSUB][Geo<FMT>::CCH / 2 * 4];
+    half2v sp[NSUB];
+    u32x4 a[MSUB], B[NSUB];
+};
+
+// scale bits of step s (block 2s + g) for this lane's row of fragment j:
+// half g of dword s % 4 of the row's chunk, ring slot (s / 4) & 1
+template <int FMT>
+__device__ inline uint32_t scale_bits(const Ctx<FMT> &c, int s, int j)
 {
     using G = Geo<FMT>;
-    // scale of block 2s + g: half g of dword s % 4 of the row's chunk, slot (s / 4) & 1
-    const uint8_t *ss =
-        c.sring + ((s / G::SGROUP) & 1) * G::SSLOT + (s % G::SGROUP) * 4 + c.g * 2;
-    half2v sp[NSUB];
-    uint32_t raw[NSUB][G::CCH / 2 * 4];
+    const int row = c.wave * WN + j * 32 + c.l32;
+    return *reinterpret_cast<const uint16_t *>(c.sring + ((s / G::SGROUP) & 1) * G::SSLOT +
+                                               row * 16 + (s % G::SGROUP) * 4 + c.g * 2);
+}
+
+// the lane's codes of one step for fragment j (its 32-k block)
+template <int FMT>
+__device__ inline void read_codes(const Ctx<FMT> &c, const uint8_t *stage, int j,
+                                  uint32_t (&raw)[Geo<FMT>::CCH / 2 * 4])
+{
+    using G = Geo<FMT>;
+    const int row = c.wave * WN + j * 32 + c.l32;
+#pragma unroll
+    for (int h = 0; h < G::CCH / 2; ++h) {
+        const int lc = c.g * (G::CCH / 2) + h;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(
+            stage + G::XBYTES + (row * G::CCH + (lc ^ cswz<FMT>(row))) * 16);
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+            raw[h * 4 + w] = v[w];
+    }
+}
+
+// activation fragment of chunk q for row block i
+template <int FMT>
+__device__ inline u32x4 read_a(const Ctx<FMT> &c, const uint8_t *stage, int q, int i)
+{
+    const int row = i * 32 + c.l32;
+    const int lc = c.g * 4 + q;
+    return *reinterpret_cast<const u32x4 *>(stage + (row * 8 + (lc ^ xswz(row))) * 16);
+}
+
+// Operands of chunk 0 of a step, from scratch (the first step of a tile).
+template <int FMT>
+__device__ inline void first_chunk(const Ctx<FMT> &c, const uint8_t *stage, int s, Ops<FMT> &op)
+{
 #pragma unroll
     for (int j = 0; j < NSUB; ++j) {
-        const int row = c.wave * WN + j * 32 + c.l32;
         if constexpr (FMT != QL_FMT_F16)
-            sp[j] = scaled_pair(*reinterpret_cast<const uint16_t *>(ss + row * 16), c.f[j]);
-#pragma unroll
-        for (int h = 0; h < G::CCH / 2; ++h) {
-            const int lc = c.g * (G::CCH / 2) + h;
-            const u32x4 v = *reinterpret_cast<const u32x4 *>(
-                stage + G::XBYTES + (row * G::CCH + (lc ^ cswz<FMT>(row))) * 16);
-#pragma unroll
-            for (int w = 0; w < 4; ++w)
-                raw[j][h * 4 + w] = v[w];
-        }
+            op.sp[j] = scaled_pair(scale_bits<FMT>(c, s, j), c.f[j]);
+        read_codes<FMT>(c, stage, j, op.raw[j]);
     }
-    auto read_a = [&](int q, int i) {
-        const int row = i * 32 + c.l32;
-        const int lc = c.g * 4 + q;
-        return *reinterpret_cast<const u32x4 *>(stage + (row * 8 + (lc ^ xswz(row))) * 16);
-    };
-    u32x4 a[MSUB], B[NSUB];
 #pragma unroll
     for (int i = 0; i < MSUB; ++i)
-        a[i] = read_a(0, i);
+        op.a[i] = read_a<FMT>(c, stage, 0, i);
 #pragma unroll
     for (int j = 0; j < NSUB; ++j)
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-            B[j][w] = deq_word<FMT>(raw[j], 0, w, sp[j]);
+            op.B[j][w] = deq_word<FMT>(op.raw[j], 0, w, op.sp[j]);
+}
+
+// The MSUB x NSUB MFMAs of chunk Q of a step.  Behind each MFMA, in a group
+// the compiler may not reorder, goes a share of the next chunk's operand
+// preparation, so that the matrix core runs while the VALU and LDS work:
+//   Q < 3: the activation fragments (from cur) and weight words of chunk
+//          Q + 1, one word per MFMA, one fragment read every NSUB MFMAs;
+//   Q = 3 with NEXT: chunk 0 of the next step, from that step's ring slot
+//          nxt: its codes and scales (all read behind the first MFMA), its
+//          activation fragments, its scale pairs, then its weight words.
+// With the last chunk of a step preparing the next step's first one, a
+// wavefront goes from the step barrier straight into MFMAs.
+template <int FMT, int Q, bool NEXT>
+__device__ inline void chunk(const Ctx<FMT> &c, const uint8_t *cur, const uint8_t *nxt, int s,
+                             Ops<FMT> &op, f32x16 (&acc)[MSUB][NSUB])
+{
+    constexpr int KK = MSUB * NSUB, W = 4 * NSUB;
+    static_assert(KK >= 4, "the next step's words start behind the fourth MFMA");
+    u32x4 an[MSUB], Bn[NSUB];
+    uint32_t sb[NSUB];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        u32x4 an[MSUB], Bn[NSUB];
+    for (int k = 0; k < KK; ++k) {
+        const int i = k / NSUB, j = k % NSUB;
+        acc[i][j] = mfma32(op.a[i], op.B[j], acc[i][j]);
+        if constexpr (Q < 3) {
+            if (k % NSUB == 0)
+                an[k / NSUB] = read_a<FMT>(c, cur, Q + 1, k / NSUB);
+            if ((k + 1) * 4 % MSUB == 0) {
+                const int wd = (k + 1) * 4 / MSUB - 1, jn = wd / 4, w = wd % 4;
+                Bn[jn][w] = pin(deq_word<FMT>(op.raw[jn], Q + 1, w, op.sp[jn]));
+            }
+        } else if constexpr (NEXT) {
+            // this step's codes and scale pairs are dead once chunk 3's
+            // weight words exist: the next step's take their registers
+            if (k == 0) {
 #pragma unroll
-        for (int k = 0; k < MSUB * NSUB; ++k) {
-            const int i = k / NSUB, j = k % NSUB;
-            acc[i][j] = mfma32(a[i], B[j], acc[i][j]);
-            if (q < 3) {
-                // MSUB reads and 4 NSUB words per MSUB * NSUB MFMAs
-                if (k % NSUB == 0)
-                    an[k / NSUB] = read_a(q + 1, k / NSUB);
-                if ((k + 1) * 4 % MSUB == 0) {
-                    const int wd = (k + 1) * 4 / MSUB - 1, jn = wd / 4, w = wd % 4;
-                    Bn[jn][w] = deq_word<FMT>(raw[jn], q + 1, w, sp[jn]);
+                for (int jj = 0; jj < NSUB; ++jj) {
+                    if constexpr (FMT != QL_FMT_F16)
+                        sb[jj] = scale_bits<FMT>(c, s + 1, jj);
+                    read_codes<FMT>(c, nxt, jj, op.raw[jj]);
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        if (q < 3) {
+            if (k % NSUB == 0)
+                an[k / NSUB] = read_a<FMT>(c, nxt, 0, k / NSUB);
+            if constexpr (FMT != QL_FMT_F16) {
+                if (k == 2)
 #pragma unroll
-            for (int i = 0; i < MSUB; ++i)
-                a[i] = an[i];
+                    for (int jj = 0; jj < NSUB; ++jj)
+                        op.sp[jj] = scaled_pair(sb[jj], c.f[jj]);
+            }
+            if (k >= 3) {
 #pragma unroll
-            for (int j = 0; j < NSUB; ++j)
-                B[j] = Bn[j];
+                for (int wd = (k - 3) * W / (KK - 3); wd < (k - 2) * W / (KK - 3); ++wd)
+                    Bn[wd / 4][wd % 4] =
+                        pin(deq_word<FMT>(op.raw[wd / 4], 0, wd % 4, op.sp[wd / 4]));
+            }
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
+    if constexpr (Q < 3 || NEXT) {
+#pragma unroll
+        for (int i = 0; i < MSUB; ++i)
+            op.a[i] = an[i];
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j)
+            op.B[j] = Bn[j];
+    }
+}
+
+// One step s = 4 t + U of a tile's main loop (ns steps, a multiple of 4).
+// TAIL: s is one of the last 4 steps (s = ns - 4 + U), where whether a
+// younger stage is in flight and whether a stage is issued depend on U.
+// Every condition is a compile-time one, so the step is one basic block
+// and no operand preparation can be moved across the barrier.
+// Chunks 0-2 prepare their successors from the step's slot; then every
+// wavefront's reads of the slot are complete (lgkmcnt), stage s + 1 has
+// landed (loads complete in issue order: only the younger stage s + 2 may
+// still be in flight), the barrier, the slot is refilled with step s + NST,
+// and chunk 3 runs while step s + 1's chunk 0 is prepared.
+template <int FMT, int U, bool TAIL>
+__device__ inline void step(const Ctx<FMT> &c, uint8_t *ring, int s, int &slot, Ops<FMT> &op,
+                            f32x16 (&acc)[MSUB][NSUB])
+{
+    using G = Geo<FMT>;
+    constexpr int NST = G::NST;
+    constexpr bool LAST = TAIL && U == 3;             // s = ns - 1
+    constexpr bool ISSUE = !TAIL || U + NST < 4;      // s + NST < ns
+    constexpr bool YOUNGER = NST == 3 && (!TAIL || U < 2);  // s + 2 < ns: in flight
+    const uint8_t *const cur = ring + slot * G::STAGE;
+    const int nslot = slot + 1 == NST ? 0 : slot + 1;
+    const uint8_t *const nxt = ring + nslot * G::STAGE;
+    chunk<FMT, 0, false>(c, cur, nxt, s, op, acc);
+    chunk<FMT, 1, false>(c, cur, nxt, s, op, acc);
+    chunk<FMT, 2, false>(c, cur, nxt, s, op, acc);
+    if constexpr (!LAST) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if constexpr (YOUNGER)
+            __builtin_amdgcn_s_waitcnt(
+                vmcnt_imm(G::LOADS + ((U + 2) % G::SGROUP == 0 ? G::SPT : 0)));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        __builtin_amdgcn_s_barrier();
+        if constexpr (ISSUE)
+            issue_stage<FMT, (U + NST) % G::SGROUP == 0>(c, ring + slot * G::STAGE, s + NST);
+        chunk<FMT, 3, true>(c, cur, nxt, s, op, acc);
+    } else {
+        chunk<FMT, 3, false>(c, cur, nxt, s, op, acc);
+    }
+    slot = nslot;
 }
 
 // EPI: some layer of the launch has an epilogue (bias, GELU, residual or
@@ -387,7 +511,7 @@ template <int FMT, bool EPI>
 __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(const GroupArgs args)
 {
     using G = Geo<FMT>;
-    constexpr int NST = G::NST, PD = NST - 1;  // prefetch distance in steps
+    constexpr int NST = G::NST;
     __shared__ __align__(16) uint8_t ring[G::LDS];
 
     // workgroup p belongs to the layer whose tile range holds p, so every
@@ -460,10 +584,11 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     c.xbase += s0 * 128;
     c.cbase += s0 * G::CROW;
     c.sbase += s0 / G::SGROUP * 16;
+    // ns >= 4 > NST: every ring slot gets its first stage
+    issue_stage<FMT, true>(c, ring, 0);
 #pragma unroll
-    for (int q = 0; q < PD; ++q)
-        if (q < ns)
-            issue_stage<FMT>(c, ring + q * G::STAGE, q);
+    for (int q = 1; q < NST; ++q)
+        issue_stage<FMT, false>(c, ring + q * G::STAGE, q);
 
     // Row shifts, behind the first stages so their latency overlaps.  Each
     // K part takes the shift of each weight row from the largest scale of
@@ -506,35 +631,34 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
             for (int r = 0; r < 16; ++r)
                 acc[i][j][r] = 0.f;
 
-    // one step: wait for stage s (loads complete in issue order, so allowing
-    // the loads of the younger stages already issued to remain outstanding
-    // means all of stage s has landed), barrier (every wavefront is done with
-    // the slot step s-1 read), refill that slot with step s+PD, compute s
-    static_assert(PD == 1 || PD == 2, "wait counts cover one or two stages in flight");
+    // Stage waits: loads complete in issue order, so waiting until only the
+    // loads of the younger stages already issued remain outstanding means
+    // all of a stage has landed.  A stage starting a scale group carries one
+    // more load per thread.  The first wait leaves stages 1 .. NST - 1 in
+    // flight (ns >= 4 > NST - 1: K parts are whole scale groups).
+    static_assert(NST == 2 || NST == 3, "wait counts cover at most one younger stage");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 1) * G::LOADS));
+    __builtin_amdgcn_s_barrier();
+    Ops<FMT> op;
+    first_chunk<FMT>(c, ring, 0, op);
+    // The main loop runs at a raised wave priority: with two workgroups on
+    // a CU, the one in its main loop is issued ahead of the other's prologue
+    // and epilogue (measured on the q4 step block call: 219.4 -> 216.8 us
+    // against raising it for the MFMAs only).
     int slot = 0;
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll 1
-    for (int s = 0; s < ns; ++s) {
-        // stage s+1's loads (one more when it starts a scale group) may
-        // remain in flight
-        if (PD == 2 && s + 1 < ns && (s + 1) % G::SGROUP == 0)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS + G::SPT));
-        else if (PD == 2 && s + 1 < ns)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(G::LOADS));
-        else
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        __builtin_amdgcn_s_barrier();
-        const int fill = slot + PD >= NST ? slot + PD - NST : slot + PD;
-        if (s + PD < ns)
-            issue_stage<FMT>(c, ring + fill * G::STAGE, s + PD);
-        // the step's MFMAs at a raised wave priority: with two workgroups
-        // on a CU, the one computing is issued ahead of the other's waits,
-        // address work and stores (measured: 221.7 -> 219.4 us per q4 step
-        // block call; raising it for the whole loop instead was slower)
-        __builtin_amdgcn_s_setprio(1);
-        compute_stage<FMT>(c, ring + slot * G::STAGE, s, acc);
-        __builtin_amdgcn_s_setprio(0);
-        slot = slot + 1 == NST ? 0 : slot + 1;
+    for (int s = 0; s + 4 < ns; s += 4) {
+        step<FMT, 0, false>(c, ring, s, slot, op, acc);
+        step<FMT, 1, false>(c, ring, s + 1, slot, op, acc);
+        step<FMT, 2, false>(c, ring, s + 2, slot, op, acc);
+        step<FMT, 3, false>(c, ring, s + 3, slot, op, acc);
     }
+    step<FMT, 0, true>(c, ring, ns - 4, slot, op, acc);
+    step<FMT, 1, true>(c, ring, ns - 3, slot, op, acc);
+    step<FMT, 2, true>(c, ring, ns - 2, slot, op, acc);
+    step<FMT, 3, true>(c, ring, ns - 1, slot, op, acc);
+    __builtin_amdgcn_s_setprio(0);
 
     // Epilogue.  Register r of tile (i, j) is row i * 32 + 8 (r / 4) + 4 g +
     // r % 4, column wave * WN + j * 32 + l32 of the tile; it returns to the
@@ -570,7 +694,7 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     // each store instruction covers 8 whole 128-byte row segments (the
     // register layout would give 4-byte stores).  A wavefront reads only
     // what it wrote, in order, so no barrier is needed.
-    float *const patch = reinterpret_cast<float *>(ring + 1024) + c.wave * 1024;
+    float *const patch = reinterpret_cast<float *>(ring + PATCH_AT) + c.wave * 1024;
     // destination: Y, or this part's plain partial output when the parts
     // are summed by a separate launch (split_sum_kernel)
     const bool to_part = (S > 1 && !d.cnt) || d.part_out;
