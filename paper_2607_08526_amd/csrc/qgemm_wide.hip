@@ -109,10 +109,6 @@ constexpr int WGS_PER_CU = MSUB * NSUB > 8 || WAVES == 8 ? 1 : 2;
 template <int FMT>
 constexpr int wgs_per_cu() { return FMT == QL_FMT_F16 ? 1 : WGS_PER_CU; }
 constexpr int MAXSPLIT = 4;  // parts per output tile (split reduction)
-// epilogue use of the ring (after the main loop): the split arrival flag at
-// byte 0, the tile's row shifts from byte 256, the wavefronts' 4 KB store
-// patches from PATCH_AT
-constexpr int PATCH_AT = (256 + BM * 4 + 1023) / 1024 * 1024;
 
 template <int FMT>
 struct Geo {
@@ -665,13 +661,18 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     // scale of X * W^T by the exact factor 2^(e[m] - f[n]).  Values are taken
     // from the accumulators as they are stored (no second copy of the tile
     // in registers).
-    // The tile's row shifts go through LDS (after every wavefront is done
-    // with the ring): 4 consecutive rows per 16-byte read.
-    int *const rowexp = reinterpret_cast<int *>(ring + 256);
-    __syncthreads();
-    for (int t = tid; t < BM; t += THREADS)
+    // Ring slot ns % NST is free now: it held step ns - NST, which every
+    // wavefront read before an earlier step barrier, and no stage is issued
+    // into it after that.  Each wavefront keeps its own copy of the tile's
+    // row shifts there (no barrier: a wavefront reads only what it wrote,
+    // and LDS operations of one wavefront complete in order), read back 4
+    // consecutive rows per 16-byte read; rows past M repeat the last row
+    // (their outputs are never stored).
+    uint8_t *const spare = ring + (ns % NST) * G::STAGE;
+    static_assert(WAVES * 4096 + WAVES * BM * 4 <= G::STAGE, "patches and row shifts fit a slot");
+    int *const rowexp = reinterpret_cast<int *>(spare + WAVES * 4096) + c.wave * BM;
+    for (int t = tid & 63; t < BM; t += 64)
         rowexp[t] = d.xexp[min(m0 + t, M - 1)];
-    __syncthreads();
     auto shifts = [&](int i, int (&ex)[16]) {
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
@@ -693,8 +694,9 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     // read back as rows, so that every lane stores 16 contiguous bytes and
     // each store instruction covers 8 whole 128-byte row segments (the
     // register layout would give 4-byte stores).  A wavefront reads only
-    // what it wrote, in order, so no barrier is needed.
-    float *const patch = reinterpret_cast<float *>(ring + PATCH_AT) + c.wave * 1024;
+    // what it wrote, in order, so no barrier is needed.  The patches live
+    // in the free ring slot too.
+    float *const patch = reinterpret_cast<float *>(spare) + c.wave * 1024;
     // destination: Y, or this part's plain partial output when the parts
     // are summed by a separate launch (split_sum_kernel)
     const bool to_part = (S > 1 && !d.cnt) || d.part_out;
@@ -835,7 +837,8 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();  // the tile's stores are complete
-        int *const flag = reinterpret_cast<int *>(ring);
+        // (the flag sits in the scale ring, clear of the store patches)
+        int *const flag = reinterpret_cast<int *>(c.sring);
         if (tid == 0)
             *flag = __hip_atomic_fetch_add(d.cnt + tile, 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
