@@ -41,6 +41,9 @@ struct LinDesc {
     int tiles_m, tiles_n;
     int tile_begin;  // first logical tile of this layer in a grouped launch
     const int *xexp; // fp16 path: per-row power-of-two shift of X (see xprep.hip)
+    // fp16 path, int8 / q4 weights: the power-of-two shift of each weight
+    // row in each K part, wshift[part][N] (set by the pre-pass, xprep.hip)
+    const int *wshift;
     // fp16 path, split reduction: each output tile is computed as ksplit
     // parts of psteps 64-k steps each.  cnt != nullptr (ksplit <=
     // wide_max_split()): parts store fp32 partial tiles in
@@ -147,16 +150,29 @@ struct XprepJob {
     uint16_t *Xh;
     int *rexp;
 };
+// The weight-row shifts of one int8 / q4 layer of the large-M launch:
+// for K part p (blocks [p * pblocks, min((p + 1) * pblocks, nb)) of each
+// row) and weight row n, f[p * N + n] puts qmax * (the row's largest scale
+// in the part) * 2^f in [2^14, 2^15) (0 for a part whose scales are all 0).
+struct WshiftJob {
+    const uint16_t *scales;  // [N][nb] fp16 bits
+    int N, nb, parts, pblocks, qmax;
+    int *f;                  // [parts][N]
+};
 struct XprepArgs {
     XprepJob j[QL_MAX_GROUP];
     int row_begin[QL_MAX_GROUP];
     int n;
+    WshiftJob w[QL_MAX_GROUP];
+    int wrow_begin[QL_MAX_GROUP];  // first item (part, weight row) of each job
+    int nw;
 };
-// All n (<= QL_MAX_GROUP) jobs in one launch, each 8-k group in Q4_SLOT
-// order if q4_slots; also sets zero[0 .. nzero) to 0 (the split counters of
-// the launch that follows on the same stream).
-hipError_t launch_xprep(const XprepJob *jobs, int n, bool q4_slots, int *zero, int nzero,
-                        hipStream_t stream);
+// All n (<= QL_MAX_GROUP) activation jobs and nw weight-shift jobs in one
+// launch, each 8-k group in Q4_SLOT order if q4_slots; also sets zero[0 ..
+// nzero) to 0 (the split counters of the launch that follows on the same
+// stream).
+hipError_t launch_xprep(const XprepJob *jobs, int n, const WshiftJob *wjobs, int nw,
+                        bool q4_slots, int *zero, int nzero, hipStream_t stream);
 
 // Few-row kernel (bf16 activations, M <= skinny_max_m()): one layer per
 // launch, workgroups of 16 weight rows with K split over their wavefronts.

@@ -211,6 +211,28 @@ __device__ inline f32x4 ld_coherent(const float *p)
     return v;
 }
 
+// 4-byte load that the compiler's wait insertion does not track: its wait
+// is explicit (wait_untracked), so that younger loads of the ring may stay
+// in flight (the compiler would wait for every load issued before the use)
+__device__ inline uint32_t ld_untracked(const int *p)
+{
+    uint32_t v;
+    asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+    return v;
+}
+
+// wait until at most YOUNGER loads are outstanding (so every load issued
+// before those has landed); the values pass through the statements, so that
+// no use can be scheduled before the wait
+template <int YOUNGER, int N>
+__device__ inline void wait_untracked(uint32_t (&v)[N])
+{
+    asm volatile("s_waitcnt %1" : "+v"(v[0]) : "i"(vmcnt_imm(YOUNGER)) : "memory");
+#pragma unroll
+    for (int j = 1; j < N; ++j)
+        asm volatile("" : "+v"(v[j]));
+}
+
 // wait for every load issued above; the values pass through the statements
 // so that no use can be scheduled before the wait
 __device__ inline void wait_loads(f32x4 (&v)[4][8])
@@ -580,43 +602,29 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     c.xbase += s0 * 128;
     c.cbase += s0 * G::CROW;
     c.sbase += s0 / G::SGROUP * 16;
+    // The shift of each of the lane's weight rows in this K part (set by
+    // the pre-pass: the largest scale of the part's blocks of the row; each
+    // part's partial outputs are scaled back exactly before they are stored
+    // or added up, so parts may differ), loaded ahead of the first stages
+    // and waited for with those stages still in flight.
+    uint32_t fr[NSUB];
+    if constexpr (FMT != QL_FMT_F16) {
+#pragma unroll
+        for (int j = 0; j < NSUB; ++j) {
+            const int n = min(n0 + c.wave * WN + j * 32 + c.l32, N - 1);
+            fr[j] = ld_untracked(d.wshift + (int64_t)part * N + n);
+        }
+    }
     // ns >= 4 > NST: every ring slot gets its first stage
     issue_stage<FMT, true>(c, ring, 0);
 #pragma unroll
     for (int q = 1; q < NST; ++q)
         issue_stage<FMT, false>(c, ring + q * G::STAGE, q);
-
-    // Row shifts, behind the first stages so their latency overlaps.  Each
-    // K part takes the shift of each weight row from the largest scale of
-    // its own blocks (its partial outputs are scaled back exactly before
-    // they are stored or added up, so parts may differ): lane (l32, g)
-    // scans half of this part's scale chunks of each of its NSUB weight
-    // rows (16-byte chunks q0 + g, q0 + g + 2, ...; K % 256 == 0 and
-    // 16-byte aligned scales, checked by the host); the two halves are then
-    // combined.  fp16 bit patterns of non-negative values order as integers.
-    const int q0 = s0 / G::SGROUP, q1 = (s0 + ns) / G::SGROUP;
+    if constexpr (FMT != QL_FMT_F16)
+        wait_untracked<NST * G::LOADS + G::SPT>(fr);
 #pragma unroll
-    for (int j = 0; j < NSUB; ++j) {
-        if constexpr (FMT == QL_FMT_F16) {
-            c.f[j] = 0;  // fp16 weights enter as they are
-            continue;
-        }
-        const int n = min(n0 + c.wave * WN + j * 32 + c.l32, N - 1);
-        const u32x4 *srow = reinterpret_cast<const u32x4 *>(d.scales + (int64_t)n * nb);
-        uint32_t mx = 0;
-#pragma unroll 4
-        for (int q = q0 + c.g; q < q1; q += 2) {
-            const u32x4 v = srow[q];
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-                mx = max(mx, max(v[t] & 0x7FFFu, (v[t] >> 16) & 0x7FFFu));
-        }
-        mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
-        const float smax = (float)__builtin_bit_cast(_Float16, (uint16_t)mx);
-        int E = 0;
-        (void)__builtin_frexpf(smax * (float)(FMT == QL_FMT_INT8 ? 127 : 7), &E);
-        c.f[j] = mx ? 15 - E : 0;  // Q * smax * 2^f in [2^14, 2^15)
-    }
+    for (int j = 0; j < NSUB; ++j)
+        c.f[j] = FMT == QL_FMT_F16 ? 0 : (int)fr[j];  // fp16 weights enter as they are
 
     f32x16 acc[MSUB][NSUB];
 #pragma unroll

@@ -766,6 +766,14 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
     }
     bytes += round256((size_t)ncnt * 4);
+    // the weight-row shifts of int8 / q4 layers, [ksplit][N] per layer (set
+    // by the pre-pass)
+    const bool quant = ord[0]->lin.fmt != QL_FMT_F16;
+    size_t woff[QL_MAX_GROUP];
+    for (int i = 0; i < n && quant; ++i) {
+        woff[i] = bytes;
+        bytes += round256((size_t)a.d[i].ksplit * a.d[i].N * 4);
+    }
     if (wsrc.dry_run) {
         wsrc.need = std::max(wsrc.need, bytes);
         return QL_OK;
@@ -779,8 +787,8 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
             a.d[i].part = (float *)(wsb + poff[i]);
             a.d[i].cnt = pl.ext || a.d[i].part_out ? nullptr : (int *)(wsb + coff[i]);
         }
-    // one pre-pass launch over every distinct activation tensor; it also
-    // clears the split counters
+    // one pre-pass launch over every distinct activation tensor and the
+    // weight-row shifts; it also clears the split counters
     XprepJob jobs[QL_MAX_GROUP];
     int njobs = 0;
     const void *xs[QL_MAX_GROUP];
@@ -797,8 +805,19 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         xs[i] = xh;
         es[i] = ex;
     }
-    hipError_t e = launch_xprep(jobs, njobs, ord[0]->lin.fmt == QL_FMT_Q4, (int *)(wsb + cnt_off),
-                                ncnt, stream);
+    WshiftJob wjobs[QL_MAX_GROUP];
+    int nw = 0;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        d.wshift = nullptr;
+        if (!quant)
+            continue;
+        d.wshift = (const int *)(wsb + woff[i]);
+        wjobs[nw++] = WshiftJob{d.scales, d.N, d.K / 32, d.ksplit, 2 * d.psteps,
+                                ord[0]->lin.fmt == QL_FMT_INT8 ? 127 : 7, (int *)(wsb + woff[i])};
+    }
+    hipError_t e = launch_xprep(jobs, njobs, wjobs, nw, ord[0]->lin.fmt == QL_FMT_Q4,
+                                (int *)(wsb + cnt_off), ncnt, stream);
     for (int i = 0; i < n; ++i) {
         a.d[i].X = xs[i];
         a.d[i].xexp = es[i];
