@@ -42,8 +42,10 @@ struct LinDesc {
     int tile_begin;  // first logical tile of this layer in a grouped launch
     const int *xexp; // fp16 path: per-row power-of-two shift of X (see xprep.hip)
     // fp16 path, int8 / q4 weights: the power-of-two shift of each weight
-    // row in each K part, wshift[part][N] (set by the pre-pass, xprep.hip)
+    // row in each K part, wshift[part][wsld] (wsld = tiles_n * BN; set by the
+    // pre-pass, xprep.hip, rows past N repeating row N - 1)
     const int *wshift;
+    int wsld;
     // fp16 path, split reduction: each output tile is computed as ksplit
     // parts of psteps 64-k steps each.  cnt != nullptr (ksplit <=
     // wide_max_split()): parts store fp32 partial tiles in
@@ -152,19 +154,20 @@ struct XprepJob {
 };
 // The weight-row shifts of one int8 / q4 layer of the large-M launch:
 // for K part p (blocks [p * pblocks, min((p + 1) * pblocks, nb)) of each
-// row) and weight row n, f[p * N + n] puts qmax * (the row's largest scale
-// in the part) * 2^f in [2^14, 2^15) (0 for a part whose scales are all 0).
+// row) and row n < ld, f[p * ld + n] puts qmax * (the largest scale of
+// weight row min(n, N - 1) in the part) * 2^f in [2^14, 2^15) (0 for a part
+// whose scales are all 0).
 struct WshiftJob {
     const uint16_t *scales;  // [N][nb] fp16 bits
-    int N, nb, parts, pblocks, qmax;
-    int *f;                  // [parts][N]
+    int N, ld, nb, parts, pblocks, qmax;
+    int *f;                  // [parts][ld]
 };
 struct XprepArgs {
     XprepJob j[QL_MAX_GROUP];
     int row_begin[QL_MAX_GROUP];
     int n;
     WshiftJob w[QL_MAX_GROUP];
-    int wrow_begin[QL_MAX_GROUP];  // first item (part, weight row) of each job
+    int wrow_begin[QL_MAX_GROUP];  // first item (part, row) of each job
     int nw;
 };
 // All n (<= QL_MAX_GROUP) activation jobs and nw weight-shift jobs in one

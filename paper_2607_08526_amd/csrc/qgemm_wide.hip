@@ -206,51 +206,15 @@ __device__ inline void st_coherent(float *p, f32x4 v)
 
 __device__ inline f32x4 ld_coherent(const float *p)
 {
+    // agent-scope atomic loads: sc1, and waited for by the compiler (a load
+    // from inline asm would not be: the compiler could reuse its destination
+    // registers before the data arrives)
+    const uint32_t *q = reinterpret_cast<const uint32_t *>(p);
     f32x4 v;
-    asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
-    return v;
-}
-
-// 4-byte load that the compiler's wait insertion does not track: its wait
-// is explicit (wait_untracked), so that younger loads of the ring may stay
-// in flight (the compiler would wait for every load issued before the use)
-__device__ inline uint32_t ld_untracked(const int *p)
-{
-    uint32_t v;
-    asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-    return v;
-}
-
-// wait until at most YOUNGER loads are outstanding (so every load issued
-// before those has landed); the values pass through the statements, so that
-// no use can be scheduled before the wait
-template <int YOUNGER, int N>
-__device__ inline void wait_untracked(uint32_t (&v)[N])
-{
-    asm volatile("s_waitcnt %1" : "+v"(v[0]) : "i"(vmcnt_imm(YOUNGER)) : "memory");
 #pragma unroll
-    for (int j = 1; j < N; ++j)
-        asm volatile("" : "+v"(v[j]));
-}
-
-// wait for every load issued above; the values pass through the statements
-// so that no use can be scheduled before the wait
-__device__ inline void wait_loads(f32x4 (&v)[4][8])
-{
-    asm volatile("s_waitcnt vmcnt(0)"
-                 : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]),
-                   "+v"(v[0][4]), "+v"(v[0][5]), "+v"(v[0][6]), "+v"(v[0][7]),
-                   "+v"(v[1][0]), "+v"(v[1][1]), "+v"(v[1][2]), "+v"(v[1][3]),
-                   "+v"(v[1][4]), "+v"(v[1][5]), "+v"(v[1][6]), "+v"(v[1][7])
-                 :
-                 : "memory");
-    asm volatile(""
-                 : "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3]),
-                   "+v"(v[2][4]), "+v"(v[2][5]), "+v"(v[2][6]), "+v"(v[2][7]),
-                   "+v"(v[3][0]), "+v"(v[3][1]), "+v"(v[3][2]), "+v"(v[3][3]),
-                   "+v"(v[3][4]), "+v"(v[3][5]), "+v"(v[3][6]), "+v"(v[3][7])
-                 :
-                 : "memory");
+    for (int k = 0; k < 4; ++k)
+        v[k] = __uint_as_float(__hip_atomic_load(q + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    return v;
 }
 
 __device__ inline int logical_tile(int p, int G)
@@ -602,29 +566,23 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     c.xbase += s0 * 128;
     c.cbase += s0 * G::CROW;
     c.sbase += s0 / G::SGROUP * 16;
-    // The shift of each of the lane's weight rows in this K part (set by
-    // the pre-pass: the largest scale of the part's blocks of the row; each
+    // The shifts of the tile's 256 weight rows in this K part (set by the
+    // pre-pass from the largest scale of the part's blocks of each row; each
     // part's partial outputs are scaled back exactly before they are stored
-    // or added up, so parts may differ), loaded ahead of the first stages
-    // and waited for with those stages still in flight.
-    uint32_t fr[NSUB];
-    if constexpr (FMT != QL_FMT_F16) {
-#pragma unroll
-        for (int j = 0; j < NSUB; ++j) {
-            const int n = min(n0 + c.wave * WN + j * 32 + c.l32, N - 1);
-            fr[j] = ld_untracked(d.wshift + (int64_t)part * N + n);
-        }
-    }
+    // or added up, so parts may differ): one direct-to-LDS load by wavefront
+    // 0, 16 bytes (4 rows) per lane, into the first KB of the scale ring's
+    // second slot (filled from step 4 on, after the shifts are read), issued
+    // before stage 0 so that the stage 0 wait covers it.
+    static_assert(FMT == QL_FMT_F16 || BN * 4 == 64 * 16, "one 16-byte load per lane of a wavefront");
+    if constexpr (FMT != QL_FMT_F16)
+        if (c.wave == 0)
+            dma16(d.wshift + (int64_t)part * d.wsld + n0, (uint32_t)(tid & 63) * 16,
+                  lds_addr(c.sring + G::SSLOT));
     // ns >= 4 > NST: every ring slot gets its first stage
     issue_stage<FMT, true>(c, ring, 0);
 #pragma unroll
     for (int q = 1; q < NST; ++q)
         issue_stage<FMT, false>(c, ring + q * G::STAGE, q);
-    if constexpr (FMT != QL_FMT_F16)
-        wait_untracked<NST * G::LOADS + G::SPT>(fr);
-#pragma unroll
-    for (int j = 0; j < NSUB; ++j)
-        c.f[j] = FMT == QL_FMT_F16 ? 0 : (int)fr[j];  // fp16 weights enter as they are
 
     f32x16 acc[MSUB][NSUB];
 #pragma unroll
@@ -639,10 +597,16 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
     // loads of the younger stages already issued remain outstanding means
     // all of a stage has landed.  A stage starting a scale group carries one
     // more load per thread.  The first wait leaves stages 1 .. NST - 1 in
-    // flight (ns >= 4 > NST - 1: K parts are whole scale groups).
+    // flight (ns >= 4 > NST - 1: K parts are whole scale groups); the
+    // shifts, issued before stage 0, have landed with it.
     static_assert(NST == 2 || NST == 3, "wait counts cover at most one younger stage");
     __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 1) * G::LOADS));
     __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int j = 0; j < NSUB; ++j)  // (fp16 weights enter as they are)
+        c.f[j] = FMT == QL_FMT_F16 ? 0
+                                   : reinterpret_cast<const int *>(
+                                         c.sring + G::SSLOT)[c.wave * WN + j * 32 + c.l32];
     Ops<FMT> op;
     first_chunk<FMT>(c, ring, 0, op);
     // The main loop runs at a raised wave priority: with two workgroups on
@@ -854,32 +818,28 @@ __global__ __launch_bounds__(THREADS, wgs_per_cu<FMT>()) void qgemm_wide_kernel(
         if (*flag != S - 1)
             return;
         // Every part, this one included, has stored its partial tile: the
-        // sum is read back from memory, two 32 x 32 tiles (8 groups of every
-        // part, up to 32 loads) per round trip, and added in part order.
-        static_assert(G4 % 8 == 0 && MAXSPLIT == 4, "two tiles of four parts per batch");
+        // sum is read back from memory, one 32 x 32 tile (4 groups of every
+        // part, up to 16 loads of 16 bytes) per round trip, and added in part
+        // order.
+        static_assert(G4 % 4 == 0, "whole 32 x 32 tiles per batch");
 #pragma unroll
-        for (int gb = 0; gb < G4; gb += 8) {
-            f32x4 v[MAXSPLIT][8];
+        for (int gb = 0; gb < G4; gb += 4) {
+            f32x4 v[MAXSPLIT][4];
 #pragma unroll
             for (int q = 0; q < MAXSPLIT; ++q)
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
+                for (int u = 0; u < 4; ++u)
                     if (q < S)
                         v[q][u] = ld_coherent(tp + (int64_t)q * (BM * BN) +
                                               ((gb + u) * THREADS + tid) * 4);
-            wait_loads(v);
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
                 for (int q = 1; q < MAXSPLIT; ++q)
                     if (q < S)
                         v[0][u] += v[q][u];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                const int gi = gb + 4 * t;
-                const f32x4 y[4] = {v[0][4 * t], v[0][4 * t + 1], v[0][4 * t + 2], v[0][4 * t + 3]};
-                store_tile(gi / (NSUB * 4), (gi / 4) % NSUB, y);
-            }
+            const f32x4 y[4] = {v[0][0], v[0][1], v[0][2], v[0][3]};
+            store_tile(gb / (NSUB * 4), (gb / 4) % NSUB, y);
             __builtin_amdgcn_sched_barrier(0);
         }
         return;

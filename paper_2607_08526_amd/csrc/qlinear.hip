@@ -766,13 +766,13 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         ncnt += a.d[i].tiles_m * a.d[i].tiles_n;
     }
     bytes += round256((size_t)ncnt * 4);
-    // the weight-row shifts of int8 / q4 layers, [ksplit][N] per layer (set
-    // by the pre-pass)
+    // the weight-row shifts of int8 / q4 layers, [ksplit][tiles_n * bn] per
+    // layer (set by the pre-pass; a tile's 256 shifts are one aligned KB)
     const bool quant = ord[0]->lin.fmt != QL_FMT_F16;
     size_t woff[QL_MAX_GROUP];
     for (int i = 0; i < n && quant; ++i) {
         woff[i] = bytes;
-        bytes += round256((size_t)a.d[i].ksplit * a.d[i].N * 4);
+        bytes += round256((size_t)a.d[i].ksplit * a.d[i].tiles_n * bn * 4);
     }
     if (wsrc.dry_run) {
         wsrc.need = std::max(wsrc.need, bytes);
@@ -813,7 +813,8 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         if (!quant)
             continue;
         d.wshift = (const int *)(wsb + woff[i]);
-        wjobs[nw++] = WshiftJob{d.scales, d.N, d.K / 32, d.ksplit, 2 * d.psteps,
+        d.wsld = d.tiles_n * bn;
+        wjobs[nw++] = WshiftJob{d.scales, d.N, d.wsld, d.K / 32, d.ksplit, 2 * d.psteps,
                                 ord[0]->lin.fmt == QL_FMT_INT8 ? 127 : 7, (int *)(wsb + woff[i])};
     }
     hipError_t e = launch_xprep(jobs, njobs, wjobs, nw, ord[0]->lin.fmt == QL_FMT_Q4,

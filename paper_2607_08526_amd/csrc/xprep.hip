@@ -81,9 +81,10 @@ __device__ inline void weight_shifts(const XprepArgs &a, int64_t t, int64_t item
             ji = i;
     const WshiftJob &w = a.w[ji];
     const int u = live ? (int)(t - a.wrow_begin[ji]) : 0;
-    const int p = u / w.N, n = u - p * w.N, sub = lane & 7;
+    const int p = u / w.ld, n = u - p * w.ld, sub = lane & 7;
     const int b0 = p * w.pblocks, b1 = min(b0 + w.pblocks, w.nb);
-    const u32x4 *row = reinterpret_cast<const u32x4 *>(w.scales + (int64_t)n * w.nb);
+    const u32x4 *row =
+        reinterpret_cast<const u32x4 *>(w.scales + (int64_t)min(n, w.N - 1) * w.nb);
     uint32_t mx = 0;
     if (live)
 #pragma unroll 4
@@ -100,7 +101,7 @@ __device__ inline void weight_shifts(const XprepArgs &a, int64_t t, int64_t item
         const float smax = (float)__builtin_bit_cast(_Float16, (uint16_t)mx);
         int E = 0;
         (void)__builtin_frexpf(smax * (float)w.qmax, &E);
-        w.f[p * w.N + n] = mx ? 15 - E : 0;
+        w.f[p * w.ld + n] = mx ? 15 - E : 0;
     }
 }
 
@@ -268,7 +269,7 @@ hipError_t launch_xprep(const XprepJob *jobs, int n, const WshiftJob *wjobs, int
     for (int i = 0; i < nw; ++i) {
         a.w[i] = wjobs[i];
         a.wrow_begin[i] = (int)items;
-        items += (int64_t)wjobs[i].parts * wjobs[i].N;
+        items += (int64_t)wjobs[i].parts * wjobs[i].ld;
     }
     a.nw = nw;
     if ((int64_t)rows + items + 32 >= ((int64_t)1 << 31))
