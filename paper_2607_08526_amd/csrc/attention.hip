@@ -113,35 +113,35 @@ void attention_kernel(const AttnArgs a)
     const int pr = tid >> 3, c8 = 8 * (tid & 7);
     const int vpr = tid & 31, vc8 = 8 * (tid >> 5);
     u32x4 pk[2], pv[2];
-    const uint16_t *const kp = a.k + (seq + 2 * pr) * a.ldk + h * DH + c8;
-    const uint16_t *const vp = a.v + (seq + 2 * vpr) * a.ldv + h * DH + vc8;
-    // (a full tile's rows are the thread's first rows advanced by whole
-    // tiles; only the last tile's are clamped)
+    // A tile's rows are read from its first row (a wave-uniform address)
+    // plus a per-lane 32-bit byte offset, fixed for full tiles; only the
+    // last tile's rows are clamped, lane by lane.
+    const uint8_t *const kbase = reinterpret_cast<const uint8_t *>(a.k + seq * a.ldk + h * DH);
+    const uint8_t *const vbase = reinterpret_cast<const uint8_t *>(a.v + seq * a.ldv + h * DH);
+    const int64_t ktile = (int64_t)BKEY * a.ldk * 2, vtile = (int64_t)BKEY * a.ldv * 2;
+    const uint32_t koff = (uint32_t)((2 * pr * a.ldk + c8) * 2), kstep = (uint32_t)(a.ldk * 2);
+    const uint32_t voff = (uint32_t)((2 * vpr * a.ldv + vc8) * 2), vstep = (uint32_t)(a.ldv * 2);
     auto fetch_k = [&](int kt) {
-        if ((kt + 1) * BKEY <= T) {
-            const uint16_t *p = kp + (int64_t)kt * BKEY * a.ldk;
-            pk[0] = *reinterpret_cast<const u32x4 *>(p);
-            pk[1] = *reinterpret_cast<const u32x4 *>(p + a.ldk);
-        } else {
+        const uint8_t *const t = kbase + kt * ktile;
+        uint32_t o[2] = {koff, koff + kstep};
+        if ((kt + 1) * BKEY > T)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int key = min(kt * BKEY + 2 * pr + i, T - 1) - 2 * pr;
-                pk[i] = *reinterpret_cast<const u32x4 *>(kp + (int64_t)key * a.ldk);
-            }
-        }
+            for (int i = 0; i < 2; ++i)
+                o[i] = (uint32_t)(((min(kt * BKEY + 2 * pr + i, T - 1) - kt * BKEY) * a.ldk + c8) * 2);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            pk[i] = *reinterpret_cast<const u32x4 *>(t + o[i]);
     };
     auto fetch_v = [&](int kt) {
-        if ((kt + 1) * BKEY <= T) {
-            const uint16_t *p = vp + (int64_t)kt * BKEY * a.ldv;
-            pv[0] = *reinterpret_cast<const u32x4 *>(p);
-            pv[1] = *reinterpret_cast<const u32x4 *>(p + a.ldv);
-        } else {
+        const uint8_t *const t = vbase + kt * vtile;
+        uint32_t o[2] = {voff, voff + vstep};
+        if ((kt + 1) * BKEY > T)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int key = min(kt * BKEY + 2 * vpr + i, T - 1) - 2 * vpr;
-                pv[i] = *reinterpret_cast<const u32x4 *>(vp + (int64_t)key * a.ldv);
-            }
-        }
+            for (int i = 0; i < 2; ++i)
+                o[i] = (uint32_t)(((min(kt * BKEY + 2 * vpr + i, T - 1) - kt * BKEY) * a.ldv + vc8) * 2);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            pv[i] = *reinterpret_cast<const u32x4 *>(t + o[i]);
     };
     auto put_k = [&](uint16_t *ks) {
 #pragma unroll
@@ -149,12 +149,13 @@ void attention_kernel(const AttnArgs a)
             *reinterpret_cast<u32x4 *>(ks + (2 * pr + i) * KROW + c8) = pk[i];
     };
     auto put_v = [&](uint16_t *vt) {
+        // channel e of the two keys: half e % 2 of word e / 2 of each row,
+        // paired by one byte permute (the low half of row 2 vpr first)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const uint32_t lo = (pv[0][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            const uint32_t hi = (pv[1][e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            *reinterpret_cast<uint32_t *>(vt + (vc8 + e) * VROW + 2 * vpr) = lo | (hi << 16);
-        }
+        for (int e = 0; e < 8; ++e)
+            *reinterpret_cast<uint32_t *>(vt + (vc8 + e) * VROW + 2 * vpr) =
+                __builtin_amdgcn_perm(pv[1][e >> 1], pv[0][e >> 1],
+                                      (e & 1) ? 0x07060302u : 0x05040100u);
     };
     // scores of this lane's query against keys 32 sub + 8 (r / 4) + 4 hf + r % 4
     // (all eight K fragments are read before the first MFMA)
@@ -273,28 +274,31 @@ void attention_kernel(const AttnArgs a)
         put_k(kbuf(1));
     }
     __syncthreads();
-    // one step: tile kt, whose scores are in cur (it is full, and tile kt + 1
-    // exists); the scores of tile kt + 1 go to nxt
-    auto step = [&](int kt, const f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+    // one step: tile kt (of parity ODD: its buffers are known at compile
+    // time, so LDS addresses fold into offsets), whose scores are in cur (it
+    // is full, and tile kt + 1 exists); the scores of tile kt + 1 go to nxt
+    auto step = [&](auto oddc, int kt, const f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+        constexpr int P = decltype(oddc)::value ? 1 : 0;
         __syncthreads();  // K of tile kt + 1 and V of tile kt are in LDS
         if (kt + 2 < nkt)
             fetch_k(kt + 2);
         fetch_v(kt + 1);
         tile_max(Flag<false>{}, kt, cur);
-        scores(kbuf((kt + 1) & 1), nxt);
-        tile_pv(Flag<false>{}, kt, cur, vbuf(kt & 1));
+        scores(kbuf(P ^ 1), nxt);
+        tile_pv(Flag<false>{}, kt, cur, vbuf(P));
         if (kt + 2 < nkt)
-            put_k(kbuf(kt & 1));
-        put_v(vbuf((kt + 1) & 1));
+            put_k(kbuf(P));
+        put_v(vbuf(P ^ 1));
     };
-    auto last = [&](int kt, const f32x16 (&cur)[2]) {
+    auto last = [&](auto oddc, int kt, const f32x16 (&cur)[2]) {
+        constexpr int P = decltype(oddc)::value ? 1 : 0;
         __syncthreads();  // V of the last tile is in LDS
         if (nkt * BKEY > T) {
             tile_max(Flag<true>{}, kt, cur);
-            tile_pv(Flag<true>{}, kt, cur, vbuf(kt & 1));
+            tile_pv(Flag<true>{}, kt, cur, vbuf(P));
         } else {
             tile_max(Flag<false>{}, kt, cur);
-            tile_pv(Flag<false>{}, kt, cur, vbuf(kt & 1));
+            tile_pv(Flag<false>{}, kt, cur, vbuf(P));
         }
     };
     // two score buffers in turn (no copies between steps)
@@ -302,14 +306,14 @@ void attention_kernel(const AttnArgs a)
     scores(kbuf(0), sa);
     int kt = 0;
     for (; kt + 2 < nkt; kt += 2) {
-        step(kt, sa, sb);
-        step(kt + 1, sb, sa);
+        step(Flag<false>{}, kt, sa, sb);
+        step(Flag<true>{}, kt + 1, sb, sa);
     }
     if (kt + 1 < nkt) {
-        step(kt, sa, sb);
-        last(kt + 1, sb);
+        step(Flag<false>{}, kt, sa, sb);
+        last(Flag<true>{}, kt + 1, sb);
     } else {
-        last(kt, sa);
+        last(Flag<false>{}, kt, sa);
     }
 
     // normalize and store: channel 32 t + 8 (r / 4) + 4 hf + r % 4 of query q
