@@ -24,9 +24,10 @@
  * Y [M][N], all row-major.
  *
  * Accuracy of the forward product against the exact sum above: fp32
- * activations and bf16 activations at M <= 64 (or when K % 256 != 0) are
- * contracted with the exact codes and fp32 block partials (error a few fp32
- * roundings).  bf16 activations at larger M take the fp16 path: X is copied
+ * activations, and bf16 activations at M <= 256 (or when K % 256 != 0 or
+ * an operand is not 16-byte aligned), are contracted with the exact codes
+ * and fp32 block partials (error a few fp32 roundings).  bf16 activations
+ * at larger M take the fp16 path: X is copied
  * exactly to fp16 with a power-of-two shift per row, each weight enters the
  * matrix cores as fp16(c * fp16(s * 2^f)) with one shift f per weight row
  * and K part (the library may cut a long reduction into parts; Q * max_b s
@@ -325,6 +326,9 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
  *   QL_PATH_TILED   tiled exact MFMA kernel: any M, bf16 or fp32 X
  *   QL_PATH_WIDE    the large-M fp16 path: bf16 X, K % 256 == 0,
  *                   K < 2^23, 16-byte aligned scales
+ *   QL_PATH_MID     the mid-M exact kernel (the normal choice for
+ *                   64 < M <= 256): bf16 X, K % 256 == 0, K < 2^23,
+ *                   16-byte aligned X, codes and scales
  * A call whose layers a forced kernel cannot take returns
  * QL_ERR_UNSUPPORTED and enqueues nothing.  fp16 weights (QL_FMT_F16) are
  * not affected.  The setting is process-wide (not per thread or stream);
@@ -336,7 +340,8 @@ typedef enum {
     QL_PATH_STREAM = 2,
     QL_PATH_SKINNY = 3,
     QL_PATH_TILED = 4,
-    QL_PATH_WIDE = 5
+    QL_PATH_WIDE = 5,
+    QL_PATH_MID = 6
 } ql_path;
 
 int qlinear_force_path(int path);

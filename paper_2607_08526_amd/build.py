@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libqlinear.so")
 SOURCES = ["qlinear.hip", "quantize.hip", "qgemm.hip", "qgemm_wide.hip", "qgemm_skinny.hip", "xprep.hip", "qgemm_stream.hip", "qgemv.hip",
-           "qgemm_w8a8.hip", "steer.hip", "attention.hip"]
+           "qgemm_w8a8.hip", "steer.hip", "attention.hip", "qgemm_mid.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -34,7 +34,7 @@ DEVICE_FLAGS = [
 VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
 SOURCE_FLAGS = {"qgemm.hip": VGPR_FORM, "qgemm_skinny.hip": VGPR_FORM,
                 "qgemm_stream.hip": VGPR_FORM, "qgemm_w8a8.hip": VGPR_FORM,
-                "attention.hip": VGPR_FORM}
+                "attention.hip": VGPR_FORM, "qgemm_mid.hip": VGPR_FORM}
 
 
 def _compile(src):

@@ -128,6 +128,15 @@ int wide_max_split();
 int wide_wgs_per_cu(int fmt);  // resident workgroups per CU (LDS and register budget)
 hipError_t launch_qgemm_wide(int fmt, const GroupArgs &args, hipStream_t stream);
 
+// Mid-M kernel (bf16 activations, int8 / q4 weights, exact per-block form,
+// no pre-pass): 128 x 128 tiles; K % 256 == 0, K < 2^23, 16-byte aligned
+// X, codes and scales; LinDesc::psteps % 4 == 0, and ksplit > 1 stores plain
+// partial outputs part[ksplit][M][N] for launch_split_sum.
+int mid_tile_bm();
+int mid_tile_bn();
+int mid_wgs_per_cu();  // resident workgroups per CU
+hipError_t launch_qgemm_mid(int fmt, const GroupArgs &args, hipStream_t stream);
+
 // Y[M][N] = sum over s < S of P[s][M][N], added in order s = 0, 1, ..., for
 // n (<= QL_MAX_GROUP) split layers in one launch
 struct SplitSum {

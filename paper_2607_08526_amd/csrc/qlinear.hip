@@ -636,6 +636,159 @@ int launch_tiled(int fmt, bool xf32, TileCfg t, GroupArgs &a, WsSource &wsrc,
     return e == hipSuccess ? QL_OK : QL_ERR_HIP;
 }
 
+// The mid-M kernel (qgemm_mid.hip: bf16 X, int8 / q4 weights, 128 x 128
+// tiles) over a group of layers.  Plan: one common part length L (a
+// multiple of 4 steps of 64 k) cuts each layer into ceil(steps / L) parts
+// (at most MID_MAX_SPLIT); among the lengths from each layer's whole
+// reduction halved down to 4 steps, the one with the smallest estimated
+// time: the makespan of the parts on the resident workgroups (times in
+// steps, a part costing its steps plus MID_OVH), plus, when a layer is
+// split, the sum launch (MID_SUM_GAP and the bytes of the partials it reads
+// and the outputs it writes).
+constexpr double MID_OVH = 4.0;
+constexpr double MID_SUM_GAP = 4.0;
+constexpr double MID_SUM_BYTES_PER_STEP = 2.5e6;
+constexpr int MID_MAX_SPLIT = 16;
+// largest M the dispatch sends to the mid-M kernel (above it, the large-M
+// kernel's wider tiles and fp16 fold win)
+constexpr int64_t MID_MAX_M = 256;
+// (measured crossover, q4 blocks at 214 rows: d = 1024 with 12 steps per CU
+// is 1.12x faster here, d = 1536 with 27 is 1.2x slower)
+constexpr double MID_MAX_STEPS_PER_CU = 16.0;
+
+bool mid_fits(const ql_linear &l)
+{
+    return l.xdt == QL_DT_BF16 && (l.fmt == QL_FMT_INT8 || l.fmt == QL_FMT_Q4) &&
+           l.K % 256 == 0 && l.K < ((int64_t)1 << 23) && aligned(l.X, 16) &&
+           aligned(l.codes, 16) && aligned(l.scales, 16);
+}
+
+void plan_mid(GroupArgs &a)
+{
+    const int n = a.n;
+    const int slots = mid_wgs_per_cu() * device_cus();
+    std::vector<int> lens;
+    for (int i = 0; i < n; ++i)
+        for (int L = a.d[i].K / 64; L >= 4; L /= 2)
+            lens.push_back(L & ~3);
+    auto parts_of = [](const LinDesc &d, int L, int &S, int &ps) {
+        const int ns = d.K / 64;
+        S = std::min(MID_MAX_SPLIT, (ns + L - 1) / L);
+        ps = ((ns + S - 1) / S + 3) & ~3;
+        S = (ns + ps - 1) / ps;
+    };
+    double best_t = 0.0;
+    int best_L = 0;
+    for (const int L : lens) {
+        if (L < 4)
+            continue;
+        // every XCD takes its share of each layer's parts (launch order:
+        // longest reduction first); parts go to the earliest free slot
+        double t = 0.0, sum_bytes = 0.0;
+        bool split = false;
+        for (int x = 0; x < XCDS; ++x) {
+            std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+            for (int k = 0; k < slots / XCDS; ++k)
+                free_at.push(0.0);
+            for (int i = 0; i < n; ++i) {
+                const LinDesc &d = a.d[i];
+                int S, ps;
+                parts_of(d, L, S, ps);
+                if (x == 0 && S > 1) {
+                    split = true;
+                    sum_bytes += (S + 1) * (double)d.M * d.N * 4;
+                }
+                const int64_t parts = (int64_t)d.tiles_m * d.tiles_n * S;
+                const int64_t mine = parts / XCDS + (x < parts % XCDS ? 1 : 0);
+                for (int64_t q = 0; q < mine; ++q) {
+                    const double e = free_at.top() + ps + MID_OVH;
+                    free_at.pop();
+                    free_at.push(e);
+                    t = std::max(t, e);
+                }
+            }
+        }
+        if (split)
+            t += MID_SUM_GAP + sum_bytes / MID_SUM_BYTES_PER_STEP;
+        if (best_L == 0 || t < best_t) {
+            best_t = t;
+            best_L = L;
+        }
+    }
+    for (int i = 0; i < n; ++i) {
+        int S, ps;
+        parts_of(a.d[i], best_L, S, ps);
+        a.d[i].ksplit = S;
+        a.d[i].psteps = ps;
+    }
+}
+
+// ls: layers of one quantized format with bf16 X, mid_fits each.
+int launch_mid(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream_t stream)
+{
+    const int bm = mid_tile_bm(), bn = mid_tile_bn();
+    // longest reduction first, so the long tiles start early
+    const ql_linear_ep *ord[QL_MAX_GROUP];
+    std::copy(ls, ls + n, ord);
+    std::stable_sort(ord, ord + n,
+                     [](const ql_linear_ep *x, const ql_linear_ep *y) { return x->lin.K > y->lin.K; });
+    GroupArgs a{};
+    a.n = n;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        d.X = ord[i]->lin.X;
+        d.codes = (const uint8_t *)ord[i]->lin.codes;
+        d.scales = ord[i]->lin.scales;
+        d.Y = ord[i]->lin.Y;
+        d.ep = to_epilogue(ord[i]->ep);
+        d.M = (int)ord[i]->lin.M;
+        d.N = (int)ord[i]->lin.N;
+        d.K = (int)ord[i]->lin.K;
+        d.tiles_m = (int)((ord[i]->lin.M + bm - 1) / bm);
+        d.tiles_n = (int)((ord[i]->lin.N + bn - 1) / bn);
+    }
+    plan_mid(a);
+    int64_t total = 0;
+    size_t part_off[QL_MAX_GROUP], bytes = 0;
+    for (int i = 0; i < n; ++i) {
+        LinDesc &d = a.d[i];
+        d.tile_begin = (int)total;
+        total += (int64_t)d.tiles_m * d.tiles_n * d.ksplit;
+        part_off[i] = bytes;
+        if (d.ksplit > 1)
+            bytes += round256((size_t)d.ksplit * d.M * d.N * 4);
+    }
+    if (total >= I31)
+        return QL_ERR_UNSUPPORTED;
+    a.total_tiles = (int)total;
+    wsrc.need = std::max(wsrc.need, bytes);
+    if (wsrc.dry_run)
+        return QL_OK;
+    Workspace ws{};
+    if (bytes > 0) {
+        if (!get_workspace(wsrc, bytes, stream, ws))
+            return wsrc.fixed ? QL_ERR_UNSUPPORTED : QL_ERR_HIP;
+        for (int i = 0; i < n; ++i)
+            if (a.d[i].ksplit > 1)
+                a.d[i].part = (float *)(ws.ptr + part_off[i]);
+    }
+    hipError_t e = launch_qgemm_mid(ord[0]->lin.fmt, a, stream);
+    if (e == hipSuccess && bytes > 0) {
+        SplitSum sums[QL_MAX_GROUP];
+        int ns = 0;
+        for (int i = 0; i < n; ++i)
+            if (a.d[i].ksplit > 1)
+                sums[ns++] = SplitSum{a.d[i].part, a.d[i].ksplit, a.d[i].M, a.d[i].N, a.d[i].Y,
+                                      a.d[i].ep};
+        e = launch_split_sum(sums, ns, stream);
+    }
+    if (ws.own_alloc) {
+        const hipError_t ef = hipFreeAsync(ws.ptr, stream);
+        e = e == hipSuccess ? ef : e;
+    }
+    return e == hipSuccess ? QL_OK : QL_ERR_HIP;
+}
+
 // One grouped launch over layers that share fmt and xdt (M > 0 each).
 int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream_t stream)
 {
@@ -656,6 +809,27 @@ int launch_group(const ql_linear_ep *const *ls, int n, WsSource &wsrc, hipStream
         return QL_ERR_UNSUPPORTED;  // the few-row kernels take bf16 activations
     if (per_layer)
         return launch_rows(ls, n, forced, wsrc, stream);
+    // a few hundred rows: the exact single-launch kernel where every layer
+    // fits it and the group's work is short (its 64-k steps of 128 x 128
+    // tiles, per CU, at most MID_MAX_STEPS_PER_CU; beyond that the large-M
+    // path's wider tiles outweigh its pre-pass)
+    if (forced == QL_PATH_MID || (forced == QL_PATH_AUTO && !xf32 && !f16 && maxM <= MID_MAX_M)) {
+        bool ok = true, wide_ok = true;
+        double steps = 0.0;
+        for (int i = 0; i < n; ++i) {
+            const ql_linear &l = ls[i]->lin;
+            ok = ok && mid_fits(l);
+            wide_ok = wide_ok && wide_fits(l);
+            steps += (double)((l.M + mid_tile_bm() - 1) / mid_tile_bm()) *
+                     ((l.N + mid_tile_bn() - 1) / mid_tile_bn()) * (l.K / 64);
+        }
+        if (forced == QL_PATH_AUTO && wide_ok && steps > MID_MAX_STEPS_PER_CU * device_cus())
+            ok = false;
+        if (ok)
+            return launch_mid(ls, n, wsrc, stream);
+        if (forced == QL_PATH_MID)
+            return QL_ERR_UNSUPPORTED;
+    }
     if (forced == QL_PATH_WIDE)
         for (int i = 0; i < n; ++i)
             if (!wide_fits(ls[i]->lin))
@@ -1121,7 +1295,7 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
 
 int qlinear_force_path(int path)
 {
-    if (path < QL_PATH_AUTO || path > QL_PATH_WIDE)
+    if (path < QL_PATH_AUTO || path > QL_PATH_MID)
         return QL_ERR_INVALID;
     g_forced_path.store(path, std::memory_order_relaxed);
     return QL_OK;

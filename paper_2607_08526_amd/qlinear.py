@@ -35,7 +35,7 @@ EXPORTS = [
     "qlinear_force_path", "qlinear_block_forward_ep_noalloc",
 ]
 
-PATH_AUTO, PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED, PATH_WIDE = range(6)
+PATH_AUTO, PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED, PATH_WIDE, PATH_MID = range(7)
 
 
 class QLinearError(RuntimeError):
@@ -492,7 +492,7 @@ def attention(q, k, v, B, T, H, dh=64, scale=None, O=None, odtype=torch.float32,
 
 class forced_path:
     """Context manager: every quantized forward call inside it runs on one
-    kernel (PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED or PATH_WIDE;
+    kernel (PATH_GEMV, PATH_STREAM, PATH_SKINNY, PATH_TILED, PATH_WIDE or PATH_MID;
     qlinear_force_path).  Process-wide; restores automatic choice on exit."""
 
     def __init__(self, path):

@@ -49,11 +49,11 @@ def test_header_declares_the_boundary():
 
 
 def test_force_path_values(lib):
-    """The path knob takes the six documented values (setting it launches
+    """The path knob takes the seven documented values (setting it launches
     nothing) and rejects others; left at automatic choice."""
-    for p in range(6):
+    for p in range(7):
         assert lib.qlinear_force_path(p) == OK
-    for bad in (-1, 6, 99):
+    for bad in (-1, 7, 99):
         assert lib.qlinear_force_path(bad) == INVALID
     assert lib.qlinear_force_path(0) == OK
 

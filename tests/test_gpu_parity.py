@@ -148,6 +148,81 @@ def test_forward_large_m_ragged_tiles(gpu, orc, fmt):
 
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
+def test_forward_mid_m(gpu, orc, fmt):
+    """The mid-M exact kernel (64 < M <= 256, K % 256 == 0): partial
+    128 x 128 tiles in both directions, one-chunk and long reductions, K
+    parts summed by a second launch (up to 16 parts), the paper's 214-token
+    rows and the 256-row single-layer workload's shape.  Exact per-block
+    form: within 1e-5 of the oracle; every output written (Y starts as NaN);
+    results repeat bit for bit."""
+    torch, ql = gpu
+    cases = [(65, 130, 256), (100, 129, 8192), (128, 2048, 2048), (129, 300, 1024),
+             (200, 1000, 4096), (214, 1027, 1536), (256, 6144, 1536), (97, 8192, 512)]
+    for M, N, K in cases:
+        W, X = si.small_case(90 + M + N + K + fmt, M, N, K)
+        codes, scales = quantize_both(gpu, orc, fmt, W)
+        cd = torch.from_numpy(codes).cuda()
+        sd = torch.from_numpy(scales.view(np.int16)).cuda()
+        xd = dev_x(torch, X, O.DT_BF16)
+        outs = []
+        for _ in range(2):
+            Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+            ql.forward(fmt, xd, cd, sd, N, Y)
+            torch.cuda.synchronize()
+            outs.append(Y.cpu().numpy())
+        assert np.isfinite(outs[0]).all(), (M, N, K)
+        Yr = orc.forward(fmt, X, O.DT_BF16, codes, scales, N)
+        e = rel_err(outs[0], Yr)
+        assert e <= 1e-5, (M, N, K, e)
+        assert np.array_equal(outs[0], outs[1]), (M, N, K)
+
+
+def test_mid_split_graph_replay(gpu, orc):
+    """The mid-M path's K parts, whose partial outputs pass through the
+    stream's workspace to the sum launch: a captured call replayed several
+    times, with and without other calls in between that overwrite that
+    workspace (a large-M call, a mid-M call with 16 parts), equals the eager
+    result bit for bit every time."""
+    torch, ql = gpu
+    fmt = O.FMT_Q4
+    shapes = {"mid": (128, 2048, 2048), "wide": (640, 1024, 4096), "ext": (100, 129, 8192)}
+    data = {}
+    for name, (M, N, K) in shapes.items():
+        W, X = si.small_case(500 + M + N + K, M, N, K)
+        codes, scales = orc.quantize(fmt, W)
+        data[name] = (dev_x(torch, X, O.DT_BF16), torch.from_numpy(codes).cuda(),
+                      torch.from_numpy(scales.view(np.int16)).cuda(), N,
+                      torch.empty((M, N), dtype=torch.float32, device="cuda"), (X, codes, scales))
+
+    def run(name):
+        xd, cd, sd, N, Y, _ = data[name]
+        ql.forward(fmt, xd, cd, sd, N, Y)
+
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        run("wide")  # sizes the workspace beyond the mid call's needs
+        run("mid")
+    s.synchronize()
+    ref = data["mid"][4].clone()
+    X, codes, scales = data["mid"][5]
+    assert rel_err(ref.cpu().numpy(), orc.forward(fmt, X, O.DT_BF16, codes, scales, 2048)) <= 1e-5
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        run("mid")
+    for rep in range(4):
+        data["mid"][4].fill_(float("nan"))
+        if rep % 2 == 1:
+            with torch.cuda.stream(s):
+                run("wide" if rep == 1 else "ext")
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g.replay()
+        s.synchronize()
+        assert torch.equal(data["mid"][4], ref), rep
+
+
+@pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forward_streaming_ragged(gpu, orc, fmt):
     """The weight-streaming path (M <= 32, K % 256 == 0; M <= 4 goes to the
     GEMV when it fits): row counts around its 8- to 64-row workgroups,
@@ -678,7 +753,7 @@ def test_block_forward_mixed_group(gpu, orc):
 # the same shapes through every kernel that takes them (qlinear_force_path)
 # --------------------------------------------------------------------------
 
-EXACT_PATHS = ("GEMV", "STREAM", "SKINNY", "TILED")
+EXACT_PATHS = ("GEMV", "STREAM", "SKINNY", "TILED", "MID")
 
 
 def takes(path, M, K):
@@ -687,13 +762,14 @@ def takes(path, M, K):
             "STREAM": M <= 32 and K % 256 == 0,
             "SKINNY": M <= 64,
             "TILED": True,
-            "WIDE": K % 256 == 0}[path]
+            "WIDE": K % 256 == 0,
+            "MID": K % 256 == 0}[path]
 
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forced_paths_agree(gpu, orc, fmt):
     """Each shape runs through every kernel that takes it: the exact kernels
-    (GEMV, streaming, few-row MFMA, tiled MFMA) each within 1e-5 of the
+    (GEMV, streaming, few-row MFMA, tiled MFMA, mid-M) each within 1e-5 of the
     oracle and within 2e-6 of one another; the large-M fp16 path within the
     bf16 tolerance.  A kernel that cannot take a shape refuses it
     (QL_ERR_UNSUPPORTED) and leaves Y untouched."""
@@ -743,7 +819,7 @@ def test_forced_path_fp32_activations(gpu, orc):
     sd = torch.from_numpy(scales.view(np.int16)).cuda()
     xd = dev_x(torch, X, O.DT_F32)
     try:
-        for name in ("GEMV", "STREAM", "SKINNY", "WIDE"):
+        for name in ("GEMV", "STREAM", "SKINNY", "WIDE", "MID"):
             ql.load().qlinear_force_path(getattr(ql, "PATH_" + name))
             with pytest.raises(ql.QLinearError) as err:
                 ql.forward(O.FMT_INT8, xd, cd, sd, N)
