@@ -24,8 +24,14 @@
 //    keys is unchanged.  The accumulator of query l % 32 stays in the lanes
 //    that hold its softmax state, so the per-query rescaling is local.
 // Per workgroup: 128 queries (4 wavefronts x 32) of one (b, h); keys in
-// tiles of 64, double-buffered in LDS (K row-major, V transposed) through
-// registers.
+// tiles of 64, double-buffered in LDS.  K and V tiles move from global memory
+// to LDS with the direct-to-LDS loads (no registers, no LDS write
+// instructions), both row-major (one key per 128-byte row, 16-byte chunks
+// XOR-swizzled per row against bank conflicts).  The V^T operand is read
+// with gfx950's transposing LDS read (ds_read_b64_tr_b16): within each group
+// of 16 lanes, result lane 4q + p receives element p of the 8 bytes that
+// source lanes q, 4 + q, 8 + q and 12 + q address, so 16 lanes that
+// address 4 keys x 4 runs of 4 channels receive 4 keys of one channel each.
 #include "internal.h"
 
 namespace qlk {
@@ -40,12 +46,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int DH = 64;             // head dimension
 constexpr int BQ = 128, BKEY = 64;  // queries per workgroup, keys per tile
 constexpr int THREADS = 256;
-constexpr int PAD = 8;             // bf16 elements of padding per LDS row
-constexpr int KROW = DH + PAD;     // Ks row: one key
-// Vt row: one value channel, 34 words (= 2 mod 32 banks), so that the 16
-// rows of one phase of 8-byte operand reads land on distinct banks
-constexpr int VROW = BKEY + 4;
-constexpr int KBYTES = BKEY * KROW * 2, VBYTES = DH * VROW * 2;
+constexpr int KBYTES = BKEY * DH * 2, VBYTES = BKEY * DH * 2;  // one tile, row-major
+constexpr int TLOADS = KBYTES / 16 / THREADS;  // 16-byte loads per thread per tile
+// physical 16-byte chunk = logical ^ swizzle(key row): the K fragment reads
+// (32 rows, one chunk) and the transposing V reads (8 rows, two chunk pairs)
+// spread over the banks
+__device__ inline int kswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ inline int vswz(int r) { return ((r >> 1) & 1) << 2; }
 // The running maximum m may trail the true one: it moves only when a tile's
 // scores exceed it by more than 2^LAZY in the exponent (so p <= 2^LAZY), and
 // then the accumulators are rescaled; the quotient O / l is the same for any
@@ -59,6 +66,39 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ inline uint32_t pack_bf16(float lo, float hi)
 {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+// wave-uniform 64-bit base in an SGPR pair (readfirstlane returns int: widen
+// through uint32_t)
+__device__ inline uint64_t sbase(const void *p)
+{
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+
+// Direct-to-LDS 16-byte load from (wave-uniform base + per-lane offset):
+// lane t's data lands at lds + t * 16.
+__device__ inline void dma16(const void *base, uint32_t off, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(sbase(base)), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "memory");
+}
+
+__device__ inline uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)p; }
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// 8 bytes of LDS at byte offset `off` of `base`, transposed across each
+// group of 16 lanes (see the header)
+__device__ inline u32x2 read_tr(const uint8_t *base, uint32_t off)
+{
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4 *)(base + off));
+    return __builtin_bit_cast(u32x2, v);
 }
 
 template <bool B>
@@ -89,8 +129,8 @@ void attention_kernel(const AttnArgs a)
     const int bh = L / nq, qblk = L - bh * nq, b = bh / a.H, h = bh - b * a.H;
     const int64_t seq = (int64_t)b * T;  // first row of this sequence
     const int q = qblk * BQ + wave * 32 + l32;  // this lane's query
-    auto kbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + i * KBYTES); };
-    auto vbuf = [&](int i) { return reinterpret_cast<uint16_t *>(lds + 2 * KBYTES + i * VBYTES); };
+    auto kbuf = [&](int i) { return lds + i * KBYTES; };
+    auto vbuf = [&](int i) { return lds + 2 * KBYTES + i * VBYTES; };
 
     // the query's B operands: head-dim chunk s, elements 16 s + 8 hf .. + 7
     bf16x8 qb[4];
@@ -103,71 +143,65 @@ void attention_kernel(const AttnArgs a)
         qb[s] = __builtin_bit_cast(bf16x8, v);
     }
 
-    // staging: thread t moves rows 2 (t / 8) and 2 (t / 8) + 1 of the K tile,
-    // elements 8 (t % 8) .. + 7, and rows 2 (t % 32), 2 (t % 32) + 1 of the V
-    // tile, elements 8 (t / 32) .. + 7.  V is written transposed, the two
-    // keys of a row pair packed into one 32-bit word; with 32 row pairs per
-    // wavefront those writes spread over the LDS banks (8 row pairs per
-    // wavefront put every write of an instruction into 8 banks).  Keys at or
-    // beyond T repeat key T - 1 (their probabilities are set to 0).
-    const int pr = tid >> 3, c8 = 8 * (tid & 7);
-    const int vpr = tid & 31, vc8 = 8 * (tid >> 5);
-    u32x4 pk[2], pv[2];
-    // A tile's rows are read from its first row (a wave-uniform address)
-    // plus a per-lane 32-bit byte offset, fixed for full tiles; only the
-    // last tile's rows are clamped, lane by lane.
+    // staging: the tile's 512 chunks of 16 bytes (K and V alike), slot
+    // i = j * 256 + t for thread t's load j: key row i / 8, physical chunk
+    // i % 8, holding logical chunk (i % 8) ^ swizzle(row) of the row.  Offsets
+    // are from the tile's first key row (a wave-uniform base); keys at or
+    // beyond T repeat key T - 1 in the last tile (their probabilities are set
+    // to 0).
     const uint8_t *const kbase = reinterpret_cast<const uint8_t *>(a.k + seq * a.ldk + h * DH);
     const uint8_t *const vbase = reinterpret_cast<const uint8_t *>(a.v + seq * a.ldv + h * DH);
     const int64_t ktile = (int64_t)BKEY * a.ldk * 2, vtile = (int64_t)BKEY * a.ldv * 2;
-    const uint32_t koff = (uint32_t)((2 * pr * a.ldk + c8) * 2), kstep = (uint32_t)(a.ldk * 2);
-    const uint32_t voff = (uint32_t)((2 * vpr * a.ldv + vc8) * 2), vstep = (uint32_t)(a.ldv * 2);
-    auto fetch_k = [&](int kt) {
-        const uint8_t *const t = kbase + kt * ktile;
-        uint32_t o[2] = {koff, koff + kstep};
+    auto offs = [&](int kt, int64_t ld, bool isk, uint32_t (&o)[TLOADS]) {
+#pragma unroll
+        for (int j = 0; j < TLOADS; ++j) {
+            const int i = j * THREADS + tid, r = i >> 3;
+            const int lc = (i & 7) ^ (isk ? kswz(r) : vswz(r));
+            const int key = min(kt * BKEY + r, T - 1) - kt * BKEY;
+            o[j] = (uint32_t)((key * ld + 8 * lc) * 2);
+        }
+    };
+    uint32_t kof[TLOADS], vof[TLOADS];  // offsets of a full tile
+    offs(0, a.ldk, true, kof);
+    offs(0, a.ldv, false, vof);
+    auto fetch = [&](int kt, const uint8_t *tbase, int64_t tstep, int64_t ld, bool isk,
+                     const uint32_t (&full)[TLOADS], uint8_t *buf) {
+        uint32_t o[TLOADS];
+#pragma unroll
+        for (int j = 0; j < TLOADS; ++j)
+            o[j] = full[j];
         if ((kt + 1) * BKEY > T)
+            offs(kt, ld, isk, o);
+        const uint8_t *const t = tbase + kt * tstep;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                o[i] = (uint32_t)(((min(kt * BKEY + 2 * pr + i, T - 1) - kt * BKEY) * a.ldk + c8) * 2);
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            pk[i] = *reinterpret_cast<const u32x4 *>(t + o[i]);
+        for (int j = 0; j < TLOADS; ++j)
+            dma16(t, o[j], lds_addr(buf) + (j * THREADS + wave * 64) * 16);
     };
-    auto fetch_v = [&](int kt) {
-        const uint8_t *const t = vbase + kt * vtile;
-        uint32_t o[2] = {voff, voff + vstep};
-        if ((kt + 1) * BKEY > T)
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-                o[i] = (uint32_t)(((min(kt * BKEY + 2 * vpr + i, T - 1) - kt * BKEY) * a.ldv + vc8) * 2);
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            pv[i] = *reinterpret_cast<const u32x4 *>(t + o[i]);
-    };
-    auto put_k = [&](uint16_t *ks) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            *reinterpret_cast<u32x4 *>(ks + (2 * pr + i) * KROW + c8) = pk[i];
-    };
-    auto put_v = [&](uint16_t *vt) {
-        // channel e of the two keys: half e % 2 of word e / 2 of each row,
-        // paired by one byte permute (the low half of row 2 vpr first)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            *reinterpret_cast<uint32_t *>(vt + (vc8 + e) * VROW + 2 * vpr) =
-                __builtin_amdgcn_perm(pv[1][e >> 1], pv[0][e >> 1],
-                                      (e & 1) ? 0x07060302u : 0x05040100u);
+    auto fetch_k = [&](int kt, uint8_t *buf) { fetch(kt, kbase, ktile, a.ldk, true, kof, buf); };
+    auto fetch_v = [&](int kt, uint8_t *buf) { fetch(kt, vbase, vtile, a.ldv, false, vof, buf); };
+    // the transposed V operand: this lane addresses key 16 kc + 8 u + 4 hf +
+    // (lane % 16) / 4 and channels 32 t + 16 ((lane / 16) % 2) + 4 (lane % 4)
+    // .. + 3, i.e. unit (8 bytes) 8 t + 4 ((lane / 16) % 2) + lane % 4 of its
+    // row; the transpose hands lane l the 4 keys of channel 32 t + l % 32
+    const int vkey0 = 4 * hf + ((lane & 15) >> 2);
+    const int vunit0 = 4 * ((lane >> 4) & 1) + (lane & 3);
+    auto voff = [&](int kc, int u, int t) {
+        const int key = 16 * kc + 8 * u + vkey0, unit = 8 * t + vunit0;
+        return (uint32_t)(key * 128 + (((unit >> 1) ^ vswz(key)) * 16) + (unit & 1) * 8);
     };
     // scores of this lane's query against keys 32 sub + 8 (r / 4) + 4 hf + r % 4
     // (all eight K fragments are read before the first MFMA)
-    auto scores = [&](const uint16_t *ks, f32x16 (&sc)[2]) {
+    auto scores = [&](const uint8_t *ks, f32x16 (&sc)[2]) {
         bf16x8 ka[4][2];
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int sub = 0; sub < 2; ++sub)
+            for (int sub = 0; sub < 2; ++sub) {
+                const int r = 32 * sub + l32;
                 ka[s][sub] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4 *>(ks + (32 * sub + l32) * KROW +
-                                                             16 * s + 8 * hf));
+                    bf16x8, *reinterpret_cast<const u32x4 *>(ks + r * 128 +
+                                                             ((2 * s + hf) ^ kswz(r)) * 16));
+            }
         const f32x16 zero = {};
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
@@ -222,7 +256,7 @@ void attention_kernel(const AttnArgs a)
                     oacc[t][r] *= alpha;
         }
     };
-    auto tile_pv = [&](auto tailc, int kt, const f32x16 (&sc)[2], const uint16_t *vt) {
+    auto tile_pv = [&](auto tailc, int kt, const f32x16 (&sc)[2], const uint8_t *vt) {
         constexpr bool TAIL = decltype(tailc)::value;
         auto valid = [&](int sub, int r) {
             return !TAIL || kt * BKEY + 32 * sub + 8 * (r >> 2) + 4 * hf + (r & 3) < T;
@@ -255,9 +289,8 @@ void attention_kernel(const AttnArgs a)
         for (int kc = 0; kc < 4; ++kc)
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const uint16_t *row = vt + (32 * t + l32) * VROW + 16 * kc + 4 * hf;
-                const u32x2 lo = *reinterpret_cast<const u32x2 *>(row);
-                const u32x2 hi = *reinterpret_cast<const u32x2 *>(row + 8);
+                const u32x2 lo = read_tr(vt, voff(kc, 0, t));
+                const u32x2 hi = read_tr(vt, voff(kc, 1, t));
                 const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
                 oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     va, __builtin_bit_cast(bf16x8, pb[kc >> 1][kc & 1]), oacc[t], 0, 0, 0);
@@ -265,33 +298,32 @@ void attention_kernel(const AttnArgs a)
     };
 
     const int nkt = (T + BKEY - 1) / BKEY;
-    fetch_k(0);
-    fetch_v(0);
-    put_k(kbuf(0));
-    put_v(vbuf(0));
-    if (nkt > 1) {
-        fetch_k(1);
-        put_k(kbuf(1));
-    }
-    __syncthreads();
+    fetch_k(0, kbuf(0));
+    fetch_v(0, vbuf(0));
+    if (nkt > 1)
+        fetch_k(1, kbuf(1));
     // one step: tile kt (of parity ODD: its buffers are known at compile
     // time, so LDS addresses fold into offsets), whose scores are in cur (it
-    // is full, and tile kt + 1 exists); the scores of tile kt + 1 go to nxt
+    // is full, and tile kt + 1 exists); the scores of tile kt + 1 go to nxt.
+    // At its start every load issued so far has landed (K of tile kt + 1, V
+    // of tile kt: the last issued, one step ago) and every wavefront has
+    // finished the previous step, so K's buffer of tile kt (read in step
+    // kt - 1) takes tile kt + 2 and V's buffer of tile kt - 1 takes tile
+    // kt + 1 while this step reads the other two.
     auto step = [&](auto oddc, int kt, const f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
         constexpr int P = decltype(oddc)::value ? 1 : 0;
-        __syncthreads();  // K of tile kt + 1 and V of tile kt are in LDS
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
         if (kt + 2 < nkt)
-            fetch_k(kt + 2);
-        fetch_v(kt + 1);
+            fetch_k(kt + 2, kbuf(P));
+        fetch_v(kt + 1, vbuf(P ^ 1));
         tile_max(Flag<false>{}, kt, cur);
         scores(kbuf(P ^ 1), nxt);
         tile_pv(Flag<false>{}, kt, cur, vbuf(P));
-        if (kt + 2 < nkt)
-            put_k(kbuf(P));
-        put_v(vbuf(P ^ 1));
     };
     auto last = [&](auto oddc, int kt, const f32x16 (&cur)[2]) {
         constexpr int P = decltype(oddc)::value ? 1 : 0;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();  // V of the last tile is in LDS
         if (nkt * BKEY > T) {
             tile_max(Flag<true>{}, kt, cur);
@@ -303,6 +335,8 @@ void attention_kernel(const AttnArgs a)
     };
     // two score buffers in turn (no copies between steps)
     f32x16 sa[2], sb[2];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // K of tiles 0 and 1, V of tile 0 are in LDS
     scores(kbuf(0), sa);
     int kt = 0;
     for (; kt + 2 < nkt; kt += 2) {
