@@ -194,6 +194,18 @@ def counter_point_list(torch, ql, si):
         block_point(f"paper width {name} d={d} q4 M={si.PAPER_TOKENS}", ql.FMT_Q4,
                     lambda cpy, i, w=w: si.paper_weight(w, cpy, i), d, si.PAPER_TOKENS, 2,
                     900 + w)
+    # the fused attention at the DiT shape (2 x 1024 tokens, 32 heads of 64),
+    # read in place from a fused QKV tensor; bytes = Q, K, V read + O written
+    B, T, d = 2, 1024, si.D_MODEL
+    H = d // 64
+    rng = np.random.default_rng(17)
+    qkv = torch.from_numpy(si.f32_to_bf16_bits(rng.standard_normal((B * T, 3 * d)).astype(
+        np.float32)).view(np.int16)).to(dev)
+    Oa = torch.empty((B * T, d), dtype=torch.bfloat16, device=dev)
+    calls = [(lambda: ql.attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], B, T, H, O=Oa))
+             for _ in range(POINT_CALLS)]
+    pts.append((f"attention B={B} T={T} H={H} dh=64 bf16", 4 * B * T * d * 2,
+                4.0 * B * H * T * T * 64, calls))
     return pts
 
 
@@ -337,8 +349,10 @@ def summarize_points(dirs, write_traffic=False):
     kern = collections.defaultdict(lambda: collections.defaultdict(
         lambda: collections.defaultdict(float)))
     cal = {}
+    taken = set()  # a counter read in several runs (GRBM_GUI_ACTIVE) counts from the first
     for d in dirs:
         pts, calib = _split_points(_dispatches(d))
+        here = set()
         for _, k, _, c in calib:
             for cn, v in c.items():
                 if cn in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -350,8 +364,12 @@ def summarize_points(dirs, write_traffic=False):
             for _, k, _, c in recs:
                 short = k.replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
                 for cn, v in c.items():
+                    here.add(cn)
+                    if cn in taken:
+                        continue
                     vals[pid][cn] += v / calls
                     kern[pid][short][cn] += v / calls
+        taken |= here
     fcal = cal.get(("read", "FETCH_SIZE"), 0.0) / CALIB_BYTES
     wcal = cal.get(("fill", "WRITE_SIZE"), 0.0) / CALIB_BYTES
     lines = [f"calibration: FETCH_SIZE of a pure 1 GiB read = {fcal:.4f} x its bytes; "
@@ -359,7 +377,7 @@ def summarize_points(dirs, write_traffic=False):
              f"(read of the fill: FETCH {cal.get(('fill', 'FETCH_SIZE'), 0) / CALIB_BYTES:.4f}, "
              f"write of the read: WRITE {cal.get(('read', 'WRITE_SIZE'), 0) / CALIB_BYTES:.4f})", ""]
     hdr = (f"{'id':>3} {'point':<44} {'algo_MB':>8} {'fetch_MB':>9} {'write_MB':>9} "
-           f"{'hbm/algo':>8} {'mfma_busy':>9} {'valu/mfma':>9}")
+           f"{'hbm/algo':>8} {'mfma_busy':>9} {'valu/mfma':>9} {'lds_conf':>8}")
     lines.append(hdr)
     rows = []
     for pid in sorted(vals):
@@ -369,11 +387,15 @@ def summarize_points(dirs, write_traffic=False):
         mf = v.get("SQ_INSTS_MFMA", 0.0)
         mb = _mfma_busy(v)
         vpm = (v.get("SQ_INSTS_VALU", float("nan")) - mf) / mf if mf > 0 else float("nan")
+        lact = v.get("SQ_ACTIVE_INST_LDS", 0.0)
+        lcf = v.get("SQ_LDS_BANK_CONFLICT", float("nan")) / lact if lact > 0 else float("nan")
         rows.append({"id": pid, "point": m["name"], "algo_bytes": m["algo_bytes"],
                      "fetch_bytes": fb, "write_bytes": wb, "mfma_busy": mb, "valu_per_mfma": vpm,
+                     "lds_conflict_per_active": lcf,
                      "counters": {k: round(x, 1) for k, x in v.items()}})
         lines.append(f"{pid:3d} {m['name'][:44]:<44} {m['algo_bytes'] / 1e6:8.2f} {fb / 1e6:9.2f} "
-                     f"{wb / 1e6:9.2f} {(fb + wb) / m['algo_bytes']:8.2f} {mb:9.3f} {vpm:9.2f}")
+                     f"{wb / 1e6:9.2f} {(fb + wb) / m['algo_bytes']:8.2f} {mb:9.3f} {vpm:9.2f} "
+                     f"{lcf:8.3f}")
     lines.append("")
     lines.append("per kernel (per call):")
     for pid in sorted(kern):
