@@ -452,14 +452,19 @@ int stream_max_k() { return 1 << 24; }
 // parts of about one common length (so that its workgroups take about as
 // long as the others'); the launch takes as many workgroup rounds as the
 // grid needs over the CUs, and a split adds the partial round trip and the
-// sum launch.  The plan minimizes that estimate over the rows per
-// workgroup, the wavefronts and the part length.
+// sum launch.  No plan is faster than its total bytes (every workgroup
+// reads the activations of its part, so few rows per workgroup re-read them
+// more often) at the streaming rate.  The plan minimizes that estimate over
+// the rows per workgroup, the wavefronts and the part length.
 StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *psteps)
 {
-    constexpr double RT = 2.0;           // us per memory round trip under load
+    // fitted to a sweep of every plan on single layers and the grouped
+    // d = 2048 block at M = 8, 16, 24 and 32, int8 and q4
+    constexpr double RT = 2.5;           // us per memory round trip under load
     constexpr double SUM_LAUNCH = 3.0;   // us: split_sum launch and its gap
     constexpr double SUM_RATE = 4.0e6;   // bytes per us the sum launch moves
-    constexpr double PART_COST = 0.3;    // us per part (fitted to a sweep of configurations)
+    constexpr double PART_COST = 0.3;    // us per part
+    constexpr double STREAM_RATE = 7.0e6;  // bytes per us all workgroups stream together
     constexpr int MAXS = 16;
     int M = 0, nbmax = 0;
     for (int i = 0; i < n; ++i) {
@@ -492,7 +497,7 @@ StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *
                 const int L = lens[li];
                 int Si[QL_MAX_GROUP], Pi[QL_MAX_GROUP], Smax = 1;
                 int64_t wgs = 0;
-                double sum_bytes = 0.0, trips_max = 0.0;
+                double sum_bytes = 0.0, trips_max = 0.0, total_bytes = 0.0;
                 bool ok = true;
                 for (int i = 0; i < n && ok; ++i) {
                     const int nb = ds[i].K / 32;
@@ -504,8 +509,10 @@ StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *
                     Si[i] = S;
                     Pi[i] = pb;
                     Smax = std::max(Smax, S);
-                    wgs += (int64_t)((ds[i].N + rw - 1) / rw) * S;
+                    const int64_t wi = (int64_t)((ds[i].N + rw - 1) / rw) * S;
+                    wgs += wi;
                     const double bytes = (double)pb * 32 * (mx * 2 + rw * cb);
+                    total_bytes += (double)wi * bytes;
                     trips_max = std::max(trips_max,
                                          std::ceil(bytes / ((double)kw * (ring - 1) * stage)) + 1);
                     if (S > 1)
@@ -514,7 +521,7 @@ StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *
                 if (!ok)
                     continue;
                 const double rounds = std::ceil((double)wgs / ((double)cus * per_cu));
-                double t = rounds * trips_max * RT;
+                double t = std::max(rounds * trips_max * RT, total_bytes / STREAM_RATE);
                 if (Smax > 1)
                     t += RT + SUM_LAUNCH + sum_bytes / SUM_RATE + PART_COST * Smax;
                 if (t < best_t * 0.97) {
