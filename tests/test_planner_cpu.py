@@ -139,3 +139,17 @@ def test_stream_plans_keep_the_kernel_invariants(probe):
             assert 1 <= S <= 16, what
             assert pb % 8 == 0 and pb >= 8 * kw or S == 1, what
             assert (S - 1) * pb < nb <= S * pb or (S == 1 and pb >= nb), what
+
+
+def test_stream_plans_of_the_documented_workloads(probe):
+    # the grouped d = 2048 block (QKV, out, FFN-up, FFN-down) at few rows:
+    # int8 at M = 8 must not take 8-row workgroups, which tie with wider
+    # ones in round trips but re-read the activations twice as often (the
+    # plan's byte floor separates them); q4 at M = 8 keeps its 32-row plan
+    lay = [(6144, 2048), (2048, 2048), (8192, 2048), (2048, 8192)]
+    out = probe([f"stream {f} {M} " + " ".join(f"{N} {K}" for N, K in lay)
+                 for f, M in ((INT8, 8), (Q4, 8), (INT8, 32))])
+    i8, q4, i8_32 = ([int(x) for x in t[1:4]] for t in out)
+    assert i8[0] >= 16 and i8[2] == 8, out[0]
+    assert q4[0] == 32 and q4[2] == 8, out[1]
+    assert i8_32[0] == 32 and i8_32[2] == 32, out[2]
