@@ -202,7 +202,7 @@ int stream_max_m();
 // longest reduction the streaming kernel takes: its per-lane 32-bit load
 // offsets span up to 64 weight rows (64 K bytes) and 32 activation rows
 int stream_max_k();
-// mx: activation rows staged (4, 8, 16, 32); rw: weight rows per workgroup;
+// mx: activation rows staged (8, 16, 32); rw: weight rows per workgroup;
 // kw: wavefronts per workgroup (common to a group); S: the largest layer's
 // K parts, psteps: the common part length in 32-blocks.  Per layer the
 // LinDesc carries ksplit and psteps (ksplit > 1: LinDesc::part receives

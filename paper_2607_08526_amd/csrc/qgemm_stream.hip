@@ -132,7 +132,7 @@ struct SGeo {
     static constexpr int NCI = (CODE + 1023) / 1024;            // code loads per chunk
     static constexpr int NXI = MX * XROW / 1024;                // activation loads per chunk
     static constexpr int N = NCI + NXI;                         // loads per chunk (+NSL every 8)
-    static constexpr int R = MX <= 4 ? 6 : MX <= 8 ? 4 : 3;     // ring depth (chunks)
+    static constexpr int R = MX <= 8 ? 4 : 3;                   // ring depth (chunks)
     static constexpr int NF = MX / 16 > 1 ? MX / 16 : 1;        // 16-row activation fragments
     static constexpr int SLOT = RW * 64;                        // scales of 32 blocks
     static constexpr int WAVE = R * STAGE + 2 * SLOT;           // LDS bytes per wavefront
@@ -405,7 +405,6 @@ template <int FMT>
 hipError_t launch_fmt(const StreamPlan &p, const LayerGroup &g, hipStream_t s)
 {
     switch (p.mx) {
-    case 4: return launch_mx<FMT, 4>(p.rw, p.kw, g, s);
     case 8: return launch_mx<FMT, 8>(p.rw, p.kw, g, s);
     case 16: return launch_mx<FMT, 16>(p.rw, p.kw, g, s);
     case 32: return launch_mx<FMT, 32>(p.rw, p.kw, g, s);
@@ -432,7 +431,6 @@ int stream_geo(int fmt, int mx, int rw, int &stage, int &ring)
 {
     const bool i8 = fmt == QL_FMT_INT8;
     switch (mx) {
-    case 4: return i8 ? geo<QL_FMT_INT8, 4>(rw, stage, ring) : geo<QL_FMT_Q4, 4>(rw, stage, ring);
     case 8: return i8 ? geo<QL_FMT_INT8, 8>(rw, stage, ring) : geo<QL_FMT_Q4, 8>(rw, stage, ring);
     case 16: return i8 ? geo<QL_FMT_INT8, 16>(rw, stage, ring) : geo<QL_FMT_Q4, 16>(rw, stage, ring);
     default: return i8 ? geo<QL_FMT_INT8, 32>(rw, stage, ring) : geo<QL_FMT_Q4, 32>(rw, stage, ring);
@@ -471,7 +469,9 @@ StreamPlan stream_plan(int fmt, const LinDesc *ds, int n, int cus, int *S, int *
         M = std::max(M, ds[i].M);
         nbmax = std::max(nbmax, ds[i].K / 32);
     }
-    const int mx = M <= 4 ? 4 : M <= 8 ? 8 : M <= 16 ? 16 : 32;
+    // at most 4 rows still stage 8: the 4-row stage's deeper ring measured
+    // 15-25% slower on the d = 2048 block
+    const int mx = M <= 8 ? 8 : M <= 16 ? 16 : 32;
     const double cb = fmt == QL_FMT_INT8 ? 1.0 : 0.5;
     StreamPlan best{mx, 16, 4, 1, nbmax};
     double best_t = 1e30;

@@ -495,8 +495,13 @@ int launch_rows(const ql_linear_ep *const *ls, int n, int forced, WsSource &wsrc
             path[i] = RowPath::SKINNY;
             break;
         default:
-            path[i] = gemv_ok(d) ? RowPath::GEMV
-                    : stream_fits(d) ? RowPath::STREAM : RowPath::SKINNY;
+            // the GEMV's time grows with the rows, the streaming kernel's
+            // hardly below 8: at four rows of q4 the streaming kernel is ahead
+            // (a d = 2048 block 17.1 against 19.7 us); int8, with twice the
+            // code bytes per row, keeps the GEMV up to four rows (22.5 / 23.0)
+            path[i] = gemv_ok(d) && !(fmt == QL_FMT_Q4 && d.M == 4 && stream_fits(d))
+                          ? RowPath::GEMV
+                          : stream_fits(d) ? RowPath::STREAM : RowPath::SKINNY;
         }
     }
     // the streaming layers: one launch over all of them, their K parts
