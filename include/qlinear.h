@@ -327,7 +327,7 @@ int qlinear_attention(const uint16_t *q, int64_t ldq, const uint16_t *k, int64_t
  *   QL_PATH_WIDE    the large-M fp16 path: bf16 X, K % 256 == 0,
  *                   K < 2^23, 16-byte aligned scales
  *   QL_PATH_MID     the mid-M exact kernel (the normal choice for
- *                   64 < M <= 256): bf16 X, K % 256 == 0, K < 2^23,
+ *                   32 < M <= 256): bf16 X, K % 256 == 0, K < 2^23,
  *                   16-byte aligned X, codes and scales
  * A call whose layers a forced kernel cannot take returns
  * QL_ERR_UNSUPPORTED and enqueues nothing.  fp16 weights (QL_FMT_F16) are

@@ -1,5 +1,5 @@
 // Quantized linear forward for a few hundred activation rows (bf16 X, int8
-// or q4 weights; the dispatch sends 64 < M <= mid_max_m() here):
+// or q4 weights; the dispatch sends 32 < M <= mid_max_m() here):
 //
 //   Y[m][n] = sum_b s[n][b] * sum_{k in b} X[m][k] * c[n][k]
 //
