@@ -149,15 +149,17 @@ def test_forward_large_m_ragged_tiles(gpu, orc, fmt):
 
 @pytest.mark.parametrize("fmt", [O.FMT_INT8, O.FMT_Q4])
 def test_forward_mid_m(gpu, orc, fmt):
-    """The mid-M exact kernel (64 < M <= 256, K % 256 == 0): partial
-    128 x 128 tiles in both directions, one-chunk and long reductions, K
+    """The mid-M exact kernel (32 < M <= 256, K % 256 == 0): partial
+    128 x 128 tiles in both directions (a single row tile below 65 rows),
+    one-chunk and long reductions, K
     parts summed by a second launch (up to 16 parts), the paper's 214-token
     rows and the 256-row single-layer workload's shape.  Exact per-block
     form: within 1e-5 of the oracle; every output written (Y starts as NaN);
     results repeat bit for bit."""
     torch, ql = gpu
     cases = [(65, 130, 256), (100, 129, 8192), (128, 2048, 2048), (129, 300, 1024),
-             (200, 1000, 4096), (214, 1027, 1536), (256, 6144, 1536), (97, 8192, 512)]
+             (200, 1000, 4096), (214, 1027, 1536), (256, 6144, 1536), (97, 8192, 512),
+             (33, 520, 2048), (48, 2049, 8192), (64, 300, 768)]
     for M, N, K in cases:
         W, X = si.small_case(90 + M + N + K + fmt, M, N, K)
         codes, scales = quantize_both(gpu, orc, fmt, W)
