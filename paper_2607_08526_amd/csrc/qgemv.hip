@@ -318,11 +318,14 @@ template <int FMT>
 hipError_t launch_fmt(const LayerGroup &g, hipStream_t s)
 {
     // two weight rows per wavefront while that still leaves two workgroups
-    // per CU, one otherwise
+    // per CU, one otherwise; q4 at two activation rows keeps one (a d = 2048
+    // block 14.6 -> 13.0 us; int8 at two rows and both formats at three and
+    // four measured slower with one)
     int64_t rows = 0;
     for (int i = 0; i < g.n; ++i)
         rows += g.d[i].N;
-    const bool two = (rows + 2 * WAVES - 1) / (2 * WAVES) >= 512;
+    const bool two = !(FMT == QL_FMT_Q4 && g.d[0].M == 2) &&
+                     (rows + 2 * WAVES - 1) / (2 * WAVES) >= 512;
     switch (g.d[0].M) {
     case 1: return two ? launch_bpl<FMT, 1, 2>(g, s) : launch_bpl<FMT, 1, 1>(g, s);
     case 2: return two ? launch_bpl<FMT, 2, 2>(g, s) : launch_bpl<FMT, 2, 1>(g, s);
